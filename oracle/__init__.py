@@ -1,0 +1,154 @@
+"""Python face of the CPU oracle (liboracle.so).
+
+TEST INFRASTRUCTURE ONLY: the tests, the smoke check and the CPU-baseline
+leg of the benchmark use this; the product path never does.  The oracle's
+arithmetic lives in oracle.c; this module only marshals numpy arrays.
+"""
+import ctypes
+import os
+
+import numpy as np
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+_LIB_PATH = os.path.join(HERE, "liboracle.so")
+
+_P = ctypes.c_void_p
+
+
+class Hparams(ctypes.Structure):
+    _fields_ = [("lr", ctypes.c_float), ("beta1", ctypes.c_float), ("beta2", ctypes.c_float),
+                ("eps", ctypes.c_float), ("weight_decay", ctypes.c_float)]
+
+
+def _declare(lib):
+    lib.orc_bf16_to_f32.argtypes = [ctypes.c_uint16]
+    lib.orc_bf16_to_f32.restype = ctypes.c_float
+    lib.orc_f32_to_bf16.argtypes = [ctypes.c_float]
+    lib.orc_f32_to_bf16.restype = ctypes.c_uint16
+    lib.orc_f32_to_bf16_array.argtypes = [ctypes.c_int64, _P, _P]
+    lib.orc_bf16_to_f32_array.argtypes = [ctypes.c_int64, _P, _P]
+    lib.orc_shard_reduce.argtypes = [ctypes.c_int64, ctypes.c_int, _P, ctypes.c_float, _P]
+    lib.orc_seg_sumsq.argtypes = [ctypes.c_int64, _P, _P, _P]
+    lib.orc_adamw_step.argtypes = [ctypes.c_int64, _P, _P, ctypes.POINTER(Hparams),
+                                   ctypes.c_int64, _P, _P, _P, _P, _P]
+    lib.orc_fedavg.argtypes = [ctypes.c_int64, ctypes.c_int, _P, _P, _P, _P]
+    lib.orc_round.argtypes = [ctypes.c_int64, _P, _P, ctypes.c_int, ctypes.c_int, ctypes.c_int,
+                              ctypes.c_int, ctypes.c_float, ctypes.POINTER(Hparams),
+                              ctypes.c_int64, _P, _P, _P, _P, _P, _P, _P, _P]
+    return lib
+
+
+_lib = None
+
+
+def lib(path=None):
+    """The oracle library; `path` loads another build (a test's mutant)."""
+    global _lib
+    if path is not None:
+        return _declare(ctypes.CDLL(path))
+    if _lib is None:
+        if not os.path.exists(_LIB_PATH):
+            raise RuntimeError("oracle not built: %s missing (run oracle/build.py)" % _LIB_PATH)
+        _lib = _declare(ctypes.CDLL(_LIB_PATH))
+    return _lib
+
+
+def _c(a, dtype):
+    a = np.ascontiguousarray(a, dtype=dtype)
+    return a
+
+
+def _ptr_array(arrays):
+    return (ctypes.c_void_p * len(arrays))(*[a.ctypes.data for a in arrays])
+
+
+def hparams(hp):
+    return Hparams(hp["lr"], hp["beta1"], hp["beta2"], hp["eps"], hp["weight_decay"])
+
+
+class Oracle:
+    """Numpy wrappers over one oracle build."""
+
+    def __init__(self, path=None):
+        self.L = lib(path)
+
+    def f32_to_bf16(self, x):
+        x = _c(x, np.float32)
+        out = np.empty(x.shape, np.uint16)
+        self.L.orc_f32_to_bf16_array(x.size, x.ctypes.data, out.ctypes.data)
+        return out
+
+    def bf16_to_f32(self, x):
+        x = _c(x, np.uint16)
+        out = np.empty(x.shape, np.float32)
+        self.L.orc_bf16_to_f32_array(x.size, x.ctypes.data, out.ctypes.data)
+        return out
+
+    def shard_reduce(self, grads, grad_scale):
+        grads = [_c(g, np.uint16) for g in grads]
+        n = grads[0].size
+        out = np.empty(n, np.float32)
+        rc = self.L.orc_shard_reduce(n, len(grads), _ptr_array(grads), grad_scale,
+                                     out.ctypes.data)
+        if rc:
+            raise ValueError("orc_shard_reduce: %d" % rc)
+        return out
+
+    def seg_sumsq(self, seg_off, g):
+        seg_off = _c(seg_off, np.int64)
+        g = _c(g, np.float32)
+        out = np.empty(seg_off.size - 1, np.float64)
+        rc = self.L.orc_seg_sumsq(seg_off.size - 1, seg_off.ctypes.data, g.ctypes.data,
+                                  out.ctypes.data)
+        if rc:
+            raise ValueError("orc_seg_sumsq: %d" % rc)
+        return out
+
+    def adamw_step(self, seg_off, seg_decay, hp, t, g, master, m, v, working=None):
+        """In place on master, m, v (float32) and working (uint16, optional)."""
+        seg_off = _c(seg_off, np.int64)
+        seg_decay = _c(seg_decay, np.uint8)
+        g = _c(g, np.float32)
+        for a in (master, m, v):
+            assert a.dtype == np.float32 and a.flags.c_contiguous
+        h = hparams(hp)
+        wp = None if working is None else working.ctypes.data
+        rc = self.L.orc_adamw_step(seg_off.size - 1, seg_off.ctypes.data, seg_decay.ctypes.data,
+                                   ctypes.byref(h), t, g.ctypes.data, master.ctypes.data,
+                                   m.ctypes.data, v.ctypes.data, wp)
+        if rc:
+            raise ValueError("orc_adamw_step: %d" % rc)
+
+    def fedavg(self, replicas, weights, master_out=None, working_out=None):
+        replicas = [_c(r, np.uint16) for r in replicas]
+        n = replicas[0].size
+        w = _c(weights, np.float32)
+        master_out = np.empty(n, np.float32) if master_out is None else master_out
+        working_out = np.empty(n, np.uint16) if working_out is None else working_out
+        rc = self.L.orc_fedavg(n, len(replicas), _ptr_array(replicas), w.ctypes.data,
+                               master_out.ctypes.data, working_out.ctypes.data)
+        if rc:
+            raise ValueError("orc_fedavg: %d" % rc)
+        return master_out, working_out
+
+    def round(self, seg_off, seg_decay, R, G, A, self_group, grad_scale, hp, step0, weights,
+              grads, replicas, master, m, v, working, want_sumsq=False):
+        """In place on master, m, v, working.  grads: A*R arrays step-major;
+        replicas: G arrays (entry self_group ignored, may be None).
+        Returns the A x n_seg per-segment sums of squares, or None."""
+        seg_off = _c(seg_off, np.int64)
+        seg_decay = _c(seg_decay, np.uint8)
+        n_seg = seg_off.size - 1
+        grads = [_c(g, np.uint16) for g in grads]
+        reps = [working if r is None else _c(r, np.uint16) for r in replicas]
+        w = _c(weights, np.float32)
+        h = hparams(hp)
+        ss = np.empty(A * n_seg, np.float64) if want_sumsq else None
+        rc = self.L.orc_round(n_seg, seg_off.ctypes.data, seg_decay.ctypes.data, R, G, A,
+                              self_group, grad_scale, ctypes.byref(h), step0, w.ctypes.data,
+                              _ptr_array(grads), _ptr_array(reps), master.ctypes.data,
+                              m.ctypes.data, v.ctypes.data, working.ctypes.data,
+                              None if ss is None else ss.ctypes.data)
+        if rc:
+            raise ValueError("orc_round: %d" % rc)
+        return None if ss is None else ss.reshape(A, n_seg)

@@ -1,0 +1,163 @@
+/*
+ * oracle.c -- plain, slow, obviously-correct CPU oracle.  TEST INFRASTRUCTURE
+ * ONLY (see oracle.h for what is computed and which passages of the paper
+ * each step follows).  Scalar loops, one thread, no SIMD, no FMA.
+ */
+#include "oracle.h"
+
+#include <math.h>
+#include <stdlib.h>
+#include <string.h>
+
+/* bf16 is the upper half of a binary32. */
+float orc_bf16_to_f32(uint16_t h) {
+  uint32_t u = (uint32_t)h << 16;
+  float f;
+  memcpy(&f, &u, sizeof f);
+  return f;
+}
+
+/* binary32 -> bf16, round to nearest, ties to even.  A NaN keeps its sign
+ * and upper payload bits and is made quiet. */
+uint16_t orc_f32_to_bf16(float x) {
+  uint32_t u;
+  memcpy(&u, &x, sizeof u);
+  if ((u & 0x7F800000u) == 0x7F800000u && (u & 0x007FFFFFu) != 0u)
+    return (uint16_t)((u >> 16) | 0x0040u);
+  uint32_t lower = u & 0xFFFFu;
+  uint32_t upper = u >> 16;
+  if (lower > 0x8000u || (lower == 0x8000u && (upper & 1u))) upper += 1u;
+  return (uint16_t)upper;
+}
+
+int orc_shard_reduce(int64_t n, int R, const uint16_t* const* grads, float grad_scale,
+                     float* g) {
+  if (n < 0 || R < 1 || (n > 0 && (!grads || !g))) return -1;
+  for (int64_t i = 0; i < n; ++i) {
+    float acc = 0.0f;
+    for (int r = 0; r < R; ++r) acc = acc + orc_bf16_to_f32(grads[r][i]);
+    g[i] = acc * grad_scale;
+  }
+  return 0;
+}
+
+int orc_seg_sumsq(int64_t n_seg, const int64_t* seg_off, const float* g, double* out) {
+  if (n_seg < 0 || !seg_off || (n_seg > 0 && !out)) return -1;
+  for (int64_t s = 0; s < n_seg; ++s) {
+    double sum = 0.0;
+    for (int64_t i = seg_off[s]; i < seg_off[s + 1]; ++i) sum += (double)g[i] * (double)g[i];
+    out[s] = sum;
+  }
+  return 0;
+}
+
+int orc_adamw_step(int64_t n_seg, const int64_t* seg_off, const uint8_t* seg_decay,
+                   const orc_hparams* h, int64_t t, const float* g, float* master, float* m,
+                   float* v, uint16_t* working) {
+  if (n_seg < 0 || !seg_off || !h || t < 1) return -1;
+  const double lr = (double)h->lr;
+  const double bc1 = 1.0 - pow((double)h->beta1, (double)t);
+  const double bc2 = 1.0 - pow((double)h->beta2, (double)t);
+  const float step_size = (float)(lr / bc1);
+  const float bc2_sqrt = (float)sqrt(bc2);
+  const float b1 = h->beta1;
+  const float b2 = h->beta2;
+  const float omb1 = (float)(1.0 - (double)h->beta1);
+  const float omb2 = (float)(1.0 - (double)h->beta2);
+  const float eps = h->eps;
+  const float decay_on = (float)(1.0 - lr * (double)h->weight_decay);
+
+  for (int64_t s = 0; s < n_seg; ++s) {
+    const float decay = (seg_decay == NULL || seg_decay[s]) ? decay_on : 1.0f;
+    for (int64_t i = seg_off[s]; i < seg_off[s + 1]; ++i) {
+      const float gi = g[i];
+      float p = master[i] * decay;
+      const float mn = (b1 * m[i]) + (omb1 * gi);
+      const float vn = (b2 * v[i]) + (omb2 * (gi * gi));
+      const float den = (sqrtf(vn) / bc2_sqrt) + eps;
+      p = p - (step_size * (mn / den));
+      master[i] = p;
+      m[i] = mn;
+      v[i] = vn;
+      if (working) working[i] = orc_f32_to_bf16(p);
+    }
+  }
+  return 0;
+}
+
+/* Normalised FedAvg weights: w_g / sum(w) with the sum taken in double in
+ * index order, each quotient rounded to float.  -1 if a weight is negative
+ * or not finite or the sum is not positive. */
+static int orc_norm_weights(int G, const float* w, float* out) {
+  double sum = 0.0;
+  for (int k = 0; k < G; ++k) {
+    if (!(w[k] >= 0.0f) || !isfinite(w[k])) return -1;
+    sum += (double)w[k];
+  }
+  if (!(sum > 0.0) || !isfinite(sum)) return -1;
+  for (int k = 0; k < G; ++k) out[k] = (float)((double)w[k] / sum);
+  return 0;
+}
+
+int orc_fedavg(int64_t n, int G, const uint16_t* const* replicas, const float* weights,
+               float* master_out, uint16_t* working_out) {
+  if (n < 0 || G < 1 || !weights || (n > 0 && (!replicas || !master_out || !working_out)))
+    return -1;
+  float* wn = (float*)malloc(sizeof(float) * (size_t)G);
+  if (!wn) return -1;
+  if (orc_norm_weights(G, weights, wn) != 0) {
+    free(wn);
+    return -1;
+  }
+  for (int64_t i = 0; i < n; ++i) {
+    float acc = 0.0f;
+    for (int k = 0; k < G; ++k) acc = acc + (wn[k] * orc_bf16_to_f32(replicas[k][i]));
+    master_out[i] = acc;
+    working_out[i] = orc_f32_to_bf16(acc);
+  }
+  free(wn);
+  return 0;
+}
+
+int orc_round(int64_t n_seg, const int64_t* seg_off, const uint8_t* seg_decay, int R, int G,
+              int A, int self_group, float grad_scale, const orc_hparams* h, int64_t step0,
+              const float* weights, const uint16_t* const* grads,
+              const uint16_t* const* replicas, float* master, float* m, float* v,
+              uint16_t* working, double* seg_sumsq) {
+  if (n_seg < 0 || !seg_off || R < 1 || G < 1 || A < 1 || self_group < 0 ||
+      self_group >= G || !h || step0 < 1 || !weights || !grads || !replicas)
+    return -1;
+  const int64_t n = seg_off[n_seg];
+  if (n > 0 && (!master || !m || !v || !working)) return -1;
+  float* g = (float*)malloc(sizeof(float) * (size_t)(n > 0 ? n : 1));
+  const uint16_t** reps = (const uint16_t**)malloc(sizeof(uint16_t*) * (size_t)G);
+  if (!g || !reps) {
+    free(g);
+    free(reps);
+    return -1;
+  }
+  int rc = 0;
+  for (int a = 0; a < A && rc == 0; ++a) {
+    rc = orc_shard_reduce(n, R, grads + (size_t)a * (size_t)R, grad_scale, g);
+    if (rc == 0 && seg_sumsq)
+      rc = orc_seg_sumsq(n_seg, seg_off, g, seg_sumsq + (size_t)a * (size_t)n_seg);
+    if (rc == 0)
+      rc = orc_adamw_step(n_seg, seg_off, seg_decay, h, step0 + a, g, master, m, v, working);
+  }
+  if (rc == 0) {
+    for (int k = 0; k < G; ++k) reps[k] = (k == self_group) ? working : replicas[k];
+    rc = orc_fedavg(n, G, reps, weights, master, working);
+  }
+  free(g);
+  free(reps);
+  return rc;
+}
+
+/* Array forms of the two conversions, for the tests. */
+void orc_f32_to_bf16_array(int64_t n, const float* x, uint16_t* out) {
+  for (int64_t i = 0; i < n; ++i) out[i] = orc_f32_to_bf16(x[i]);
+}
+
+void orc_bf16_to_f32_array(int64_t n, const uint16_t* x, float* out) {
+  for (int64_t i = 0; i < n; ++i) out[i] = orc_bf16_to_f32(x[i]);
+}

@@ -1,0 +1,98 @@
+/*
+ * oracle.h -- plain CPU oracle for one GPU's share of FL+FSDP / FL+HSDP
+ * parameter synchronisation.
+ *
+ * TEST INFRASTRUCTURE ONLY.  Nothing on the product path may call, link or
+ * load this code; only the tests, the smoke check and the CPU-baseline leg of
+ * the benchmark do.  It shares no source, header, table or helper with the
+ * GPU library.
+ *
+ * What it computes, per element i of a flat shard of n elements split into
+ * segments (each a slice of one layer, the unit FSDP shards equally over a
+ * sharding group -- Section 2, FSDP):
+ *
+ *  (a1) local arithmetic of the gradient reduce-scatter over the R peers of
+ *       the sharding group (Section 2, FSDP; Section 5.1 notes that the
+ *       collectives average gradients and that the order of the floating-
+ *       point operations changes bf16 results, so the order is fixed here):
+ *         acc = 0; for r = 0..R-1: acc = acc + f32(grad_r[i])   (fp32)
+ *         g = acc * grad_scale
+ *  (a2) one AdamW step (Section 5 setup: AdamW, lr 3e-4, bf16 training)
+ *       on the fp32 master copy with decoupled weight decay and bias
+ *       correction, then the bf16 working copy for the next forward:
+ *         p  = master[i] * decay_s
+ *         mn = b1 * m[i] + omb1 * g
+ *         vn = b2 * v[i] + omb2 * (g * g)
+ *         den = sqrt(vn) / bc2_sqrt + eps
+ *         p  = p - step_size * (mn / den)
+ *         master = p; m = mn; v = vn; working = bf16_rne(p)
+ *       with host scalars (double, then rounded to float):
+ *         step_size = lr / (1 - beta1^t), bc2_sqrt = sqrt(1 - beta2^t),
+ *         omb1 = 1 - beta1, omb2 = 1 - beta2,
+ *         decay_s = 1 - lr * weight_decay if segment s decays, else 1.
+ *  (a3) FedAvg: the weighted average of the G federation groups' replicas
+ *       of the shard (Section 2, Federated Learning; Section 4.1, Eq. (3);
+ *       Section 4.2, Eq. (4): after aggregation every shard equals the
+ *       average of its corresponding shards):
+ *         w_g' = w_g / sum_g w_g          (double, then float)
+ *         acc = 0; for g = 0..G-1: acc = acc + w_g' * f32(rep_g[i])   (fp32)
+ *         master = acc; working = bf16_rne(acc); m and v unchanged.
+ *  (a4) one round: A local steps (a1 then a2 at step t = step0 + a), then
+ *       FedAvg with the own replica taken from the bf16 working copy
+ *       (Section 4.2: FedAvg after the local update every A steps).
+ *  (a5) per-segment sum of squares of g for each local step, accumulated in
+ *       double in index order.
+ *
+ * Every fp32 operation above is one IEEE-754 binary32 operation rounded to
+ * nearest even, evaluated in the written order; the file is compiled with
+ * -ffp-contract=off and without fast-math, and subnormals are kept.
+ */
+#ifndef FL_ORACLE_H
+#define FL_ORACLE_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct {
+  float lr, beta1, beta2, eps, weight_decay;
+} orc_hparams;
+
+float orc_bf16_to_f32(uint16_t h);
+uint16_t orc_f32_to_bf16(float x);
+void orc_f32_to_bf16_array(int64_t n, const float* x, uint16_t* out);
+void orc_bf16_to_f32_array(int64_t n, const uint16_t* x, float* out);
+
+/* (a1) g[i] for i in [0, n). grads: R host arrays of n bf16 values. */
+int orc_shard_reduce(int64_t n, int R, const uint16_t* const* grads, float grad_scale,
+                     float* g);
+
+/* (a5) out[s] = sum over segment s of (double)g[i]^2, i ascending. */
+int orc_seg_sumsq(int64_t n_seg, const int64_t* seg_off, const float* g, double* out);
+
+/* (a2) One AdamW step at step number t (1-based) over n = seg_off[n_seg]
+ * elements; working may be NULL (not written). */
+int orc_adamw_step(int64_t n_seg, const int64_t* seg_off, const uint8_t* seg_decay,
+                   const orc_hparams* h, int64_t t, const float* g, float* master, float* m,
+                   float* v, uint16_t* working);
+
+/* (a3) FedAvg of G bf16 replicas; working_out may be one of replicas[]. */
+int orc_fedavg(int64_t n, int G, const uint16_t* const* replicas, const float* weights,
+               float* master_out, uint16_t* working_out);
+
+/* (a4) One round.  grads: A*R arrays, step-major.  replicas: G arrays, the
+ * entry at self_group is ignored (the working copy is used).  seg_sumsq:
+ * NULL or A*n_seg doubles. */
+int orc_round(int64_t n_seg, const int64_t* seg_off, const uint8_t* seg_decay, int R, int G,
+              int A, int self_group, float grad_scale, const orc_hparams* h, int64_t step0,
+              const float* weights, const uint16_t* const* grads,
+              const uint16_t* const* replicas, float* master, float* m, float* v,
+              uint16_t* working, double* seg_sumsq);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif

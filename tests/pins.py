@@ -1,0 +1,590 @@
+"""Pins of the CPU oracle to things other than itself.
+
+Each pin_* function takes an ``oracle.Oracle`` and raises AssertionError when
+the oracle disagrees with an independent reference: torch's own bf16 cast,
+torch.optim.AdamW run in float64, float64 numpy sums, closed forms of the
+method's special cases, hand-derived exact cases (tests/golden), and a
+straight-line float64 recomputation of whole rounds with propagated
+rounding-error bounds.  test_oracle_pins.py runs them on the oracle;
+test_oracle_mutants.py runs them on copies of the oracle with planted
+mistakes and requires that every mistake is caught.
+"""
+import json
+import os
+
+import numpy as np
+import torch
+
+U = 2.0 ** -24          # unit roundoff of binary32
+TINY = 2.0 ** -149      # smallest subnormal binary32
+
+GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden")
+
+STD_HP = dict(lr=3e-4, beta1=0.9, beta2=0.95, eps=1e-8, weight_decay=0.1)
+# Exaggerated hyperparameters: make every term of the update large enough that
+# dropping or misplacing it moves the result far outside rounding error.
+BIG_HP = dict(lr=0.05, beta1=0.8, beta2=0.9, eps=1e-3, weight_decay=0.5)
+
+
+# ---- independent helpers (no oracle code) --------------------------------
+
+def bf16_decode(u16):
+    """bf16 bits -> float64 values, by numpy bit manipulation."""
+    u = np.asarray(u16, dtype=np.uint16).astype(np.uint32) << np.uint32(16)
+    return u.view(np.float32).astype(np.float64)
+
+
+def torch_bf16_bits(f32):
+    """float32 -> bf16 bits via torch's own conversion."""
+    t = torch.from_numpy(np.ascontiguousarray(f32, dtype=np.float32)).to(torch.bfloat16)
+    return t.view(torch.int16).numpy().view(np.uint16).copy()
+
+
+def f32(x):
+    return np.float32(x)
+
+
+def rng(seed):
+    return np.random.default_rng(seed)
+
+
+def random_bf16(r, n, std=1e-3):
+    return torch_bf16_bits((r.standard_normal(n) * std).astype(np.float32))
+
+
+def bf16_boundary_between(lo, hi):
+    """True where the closed interval [lo, hi] (float64) contains a bf16
+    rounding boundary, i.e. where the bf16 rounding of a value in it is not
+    unique."""
+    lo32 = lo.astype(np.float32)
+    hi32 = hi.astype(np.float32)
+    a = torch_bf16_bits(np.nextafter(lo32, np.float32(-np.inf)))
+    b = torch_bf16_bits(np.nextafter(hi32, np.float32(np.inf)))
+    return a != b
+
+
+def _hp_f(hp):
+    return {k: float(np.float32(v)) for k, v in hp.items()}
+
+
+# ---- bf16 conversions ------------------------------------------------------
+
+def pin_bf16_decode_all_patterns(orc):
+    bits = np.arange(65536, dtype=np.uint32).astype(np.uint16)
+    ours = orc.bf16_to_f32(bits).view(np.uint32)
+    ref = torch.from_numpy(bits.view(np.int16).copy()).view(torch.bfloat16).to(torch.float32)
+    ref = ref.numpy().view(np.uint32)
+    assert np.array_equal(ours, ref), "bf16 -> f32 differs from torch"
+
+
+def _conversion_cases(seed=0):
+    r = rng(seed)
+    vals = [r.standard_normal(20000) * 10.0 ** r.integers(-40, 38, 20000)]
+    # ties: lower 16 bits exactly 0x8000, with even and odd upper halves
+    up = r.integers(0, 0x7F7F, 4000, dtype=np.uint32)
+    ties = ((up << 16) | 0x8000).astype(np.uint32)
+    near = np.concatenate([ties - 1, ties + 1, ties, ties | 0x80000000])
+    vals.append(near.view(np.float32))
+    special = np.array([0x00000000, 0x80000000, 0x7F800000, 0xFF800000, 0x7F7FFFFF, 0xFF7FFFFF,
+                        0x7F7F8000, 0x7F7F7FFF, 0x00800000, 0x00000001, 0x00008000, 0x00018000,
+                        0x007FFFFF, 0x80008000, 0x3F808000, 0x3F818000, 0x3F80FFFF],
+                       dtype=np.uint32).view(np.float32)
+    vals.append(special)
+    return np.concatenate([v.astype(np.float32) for v in vals])
+
+
+def pin_bf16_encode_matches_torch(orc):
+    x = _conversion_cases()
+    ours = orc.f32_to_bf16(x)
+    ref = torch_bf16_bits(x)
+    bad = np.nonzero(ours != ref)[0]
+    assert bad.size == 0, "f32 -> bf16 differs from torch at %d values, e.g. %s -> %04x vs %04x" % (
+        bad.size, hex(x[bad[0]:bad[0] + 1].view(np.uint32)[0]), ours[bad[0]], ref[bad[0]])
+
+
+def pin_bf16_encode_nan(orc):
+    nans = np.array([0x7FC00000, 0xFFC00000, 0x7F800001, 0xFF800001, 0x7FBFFFFF, 0x7F80FFFF,
+                     0x7F810000], dtype=np.uint32).view(np.float32)
+    out = orc.f32_to_bf16(nans)
+    dec = bf16_decode(out)
+    assert np.all(np.isnan(dec)), "a NaN did not stay NaN"
+    assert np.array_equal(out >> 15, (nans.view(np.uint32) >> 31).astype(np.uint16)), "NaN sign lost"
+    assert np.all(out & 0x0040), "NaN not quiet"
+
+
+# ---- (a1) peer reduction ---------------------------------------------------
+
+def pin_reduce_vs_float64_sum(orc):
+    r = rng(1)
+    for R, scale in ((1, 1.0), (3, 1.0 / 3.0), (8, 0.125), (16, 1.0 / 16), (5, 0.7)):
+        n = 4096
+        grads = [random_bf16(r, n, std=10.0 ** r.uniform(-5, 1)) for _ in range(R)]
+        g = orc.shard_reduce(grads, scale).astype(np.float64)
+        dec = np.stack([bf16_decode(x) for x in grads])
+        s = float(np.float32(scale))
+        exact = dec.sum(0) * s
+        bound = (R + 1) * U * np.abs(dec).sum(0) * abs(s) + TINY
+        err = np.abs(g - exact)
+        assert np.all(err <= bound), "reduce R=%d off by %g (bound %g)" % (
+            R, err.max(), bound[np.argmax(err - bound)])
+
+
+def pin_reduce_identical_peers_exact(orc):
+    r = rng(2)
+    x = random_bf16(r, 3000, std=0.5)
+    for R in (1, 2, 4, 8, 16):
+        g = orc.shard_reduce([x] * R, 1.0 / R)
+        assert np.array_equal(g.astype(np.float64), bf16_decode(x)), "mean of %d equal peers" % R
+
+
+# ---- (a5) per-segment sum of squares ----------------------------------------
+
+def pin_seg_sumsq_vs_numpy(orc):
+    r = rng(3)
+    sizes = r.integers(1, 400, 40)
+    off = np.zeros(sizes.size + 1, np.int64)
+    off[1:] = np.cumsum(sizes)
+    g = (r.standard_normal(off[-1]) * 1e-3).astype(np.float32)
+    ss = orc.seg_sumsq(off, g)
+    g64 = g.astype(np.float64)
+    ref = np.array([np.sum(g64[off[s]:off[s + 1]] ** 2) for s in range(sizes.size)])
+    assert np.allclose(ss, ref, rtol=1e-12, atol=0), "per-segment sum of squares"
+
+
+# ---- (a2) AdamW --------------------------------------------------------------
+
+def _torch_adamw_run(hp, p0, grads_per_step, decay_mask):
+    """torch.optim.AdamW in float64 (single-tensor path): one param group with
+    weight decay for decay_mask elements, one without."""
+    hpf = _hp_f(hp)
+    p_dec = torch.tensor(p0[decay_mask], dtype=torch.float64, requires_grad=True)
+    p_nod = torch.tensor(p0[~decay_mask], dtype=torch.float64, requires_grad=True)
+    opt = torch.optim.AdamW(
+        [dict(params=[p_dec], weight_decay=hpf["weight_decay"]),
+         dict(params=[p_nod], weight_decay=0.0)],
+        lr=hpf["lr"], betas=(hpf["beta1"], hpf["beta2"]), eps=hpf["eps"], foreach=False,
+        fused=False, amsgrad=False, maximize=False)
+    hist = []
+    for g in grads_per_step:
+        p_dec.grad = torch.tensor(g[decay_mask], dtype=torch.float64)
+        p_nod.grad = torch.tensor(g[~decay_mask], dtype=torch.float64)
+        opt.step()
+        out = {}
+        for key, src in (("p", lambda t: t.detach()), ("m", lambda t: opt.state[t]["exp_avg"]),
+                         ("v", lambda t: opt.state[t]["exp_avg_sq"])):
+            a = np.empty(p0.size)
+            a[decay_mask] = src(p_dec).numpy()
+            a[~decay_mask] = src(p_nod).numpy()
+            out[key] = a
+        hist.append(out)
+    return hist
+
+
+def _adamw_bounds(hp, t_max, p0, grads_per_step, decay_mask):
+    """Propagated worst-case bounds on |fp32 oracle - exact| for p, m, v."""
+    h = _hp_f(hp)
+    b1, b2, lr, wd, eps = h["beta1"], h["beta2"], h["lr"], h["weight_decay"], h["eps"]
+    p = p0.astype(np.float64).copy()
+    m = np.zeros_like(p)
+    v = np.zeros_like(p)
+    ep = np.zeros_like(p)
+    em = np.zeros_like(p)
+    ev = np.zeros_like(p)
+    mabs = np.zeros_like(p)
+    decay = np.where(decay_mask, 1.0 - lr * wd, 1.0)
+    out = []
+    for t, g in enumerate(grads_per_step, start=1):
+        g = g.astype(np.float64)
+        mabs = b1 * mabs + (1 - b1) * np.abs(g)
+        m = b1 * m + (1 - b1) * g
+        em = b1 * em + 4 * U * mabs
+        v = b2 * v + (1 - b2) * g * g
+        ev = b2 * ev + 5 * U * v
+        bc1 = 1 - b1 ** t
+        bc2s = np.sqrt(1 - b2 ** t)
+        s = np.sqrt(v)
+        es = np.minimum(ev / np.maximum(2 * s, TINY), np.sqrt(ev)) + U * s
+        den = s / bc2s + eps
+        eden = es / bc2s + 3 * U * s / bc2s + U * den
+        ratio = m / den
+        eratio = em / den + mabs / den * (eden / den) + 2 * U * mabs / den
+        step = lr / bc1
+        upd = step * ratio
+        eupd = step * eratio + 3 * U * step * mabs / den
+        pd = p * decay
+        ep = decay * ep + 2 * U * np.abs(pd)
+        p = pd - upd
+        ep = ep + eupd + U * np.abs(p)
+        out.append(dict(p=(p, 2 * ep + TINY), m=(m, 2 * em + TINY), v=(v, 2 * ev + TINY)))
+    return out
+
+
+def _check_close(name, got, ref, bound):
+    err = np.abs(got.astype(np.float64) - ref)
+    bad = np.nonzero(~(err <= bound))[0]
+    assert bad.size == 0, "%s: %d elements out of bound, worst |err| %g at ref %g (bound %g)" % (
+        name, bad.size, err[bad].max(), ref[bad[np.argmax(err[bad])]],
+        bound[bad[np.argmax(err[bad])]])
+
+
+def pin_adamw_vs_torch_float64(orc):
+    r = rng(4)
+    for hp in (STD_HP, BIG_HP):
+        n = 2048
+        p0 = (r.standard_normal(n) * 0.02).astype(np.float32)
+        mask = np.zeros(n, bool)
+        mask[:1500] = True   # first segment decays, second does not
+        off = np.array([0, 1500, n], np.int64)
+        flags = np.array([1, 0], np.uint8)
+        steps = 5
+        gs = [(r.standard_normal(n) * 10.0 ** r.uniform(-4, -1)).astype(np.float32)
+              for _ in range(steps)]
+        gs[2][::7] = 0.0
+        ref = _torch_adamw_run(hp, p0, gs, mask)
+        bounds = _adamw_bounds(hp, steps, p0, gs, mask)
+        master = p0.copy()
+        m = np.zeros(n, np.float32)
+        v = np.zeros(n, np.float32)
+        for t in range(1, steps + 1):
+            orc.adamw_step(off, flags, hp, t, gs[t - 1], master, m, v)
+            for key, arr in (("p", master), ("m", m), ("v", v)):
+                _, bnd = bounds[t - 1][key]
+                _check_close("adamw %s t=%d lr=%g" % (key, t, hp["lr"]), arr, ref[t - 1][key], bnd)
+
+
+def pin_adamw_first_step_closed_form(orc):
+    """t = 1 from m = v = 0: p1 = p0 (1 - lr wd) - lr g / (|g| + eps),
+    m1 = (1 - b1) g, v1 = (1 - b2) g^2."""
+    r = rng(5)
+    for hp in (STD_HP, BIG_HP):
+        h = _hp_f(hp)
+        n = 4096
+        p0 = (r.standard_normal(n) * 0.02).astype(np.float32)
+        g = (r.standard_normal(n) * 1e-3).astype(np.float32)
+        master, m, v = p0.copy(), np.zeros(n, np.float32), np.zeros(n, np.float32)
+        work = np.zeros(n, np.uint16)
+        orc.adamw_step(np.array([0, n], np.int64), np.array([1], np.uint8), hp, 1, g, master, m,
+                       v, work)
+        p64, g64 = p0.astype(np.float64), g.astype(np.float64)
+        want = p64 * (1 - h["lr"] * h["weight_decay"]) - h["lr"] * g64 / (np.abs(g64) + h["eps"])
+        bound = 16 * U * (np.abs(p64) + h["lr"]) + TINY
+        _check_close("first-step p", master, want, bound)
+        _check_close("first-step m", m, (1 - h["beta1"]) * g64, 2 * U * np.abs(g64) + TINY)
+        _check_close("first-step v", v, (1 - h["beta2"]) * g64 * g64, 3 * U * g64 * g64 + TINY)
+        assert np.array_equal(work, torch_bf16_bits(master)), "working copy is not bf16(master)"
+
+
+def pin_adamw_zero_grad(orc):
+    """g = 0 at t = 1: m = v = 0 and p = p0 * decay exactly."""
+    r = rng(6)
+    n = 1000
+    p0 = (r.standard_normal(n) * 0.02).astype(np.float32)
+    for hp in (STD_HP, BIG_HP):
+        h = _hp_f(hp)
+        off = np.array([0, 600, n], np.int64)
+        flags = np.array([1, 0], np.uint8)
+        master, m, v = p0.copy(), np.zeros(n, np.float32), np.zeros(n, np.float32)
+        orc.adamw_step(off, flags, hp, 1, np.zeros(n, np.float32), master, m, v)
+        decay = np.float32(1.0 - h["lr"] * h["weight_decay"])
+        assert np.array_equal(master[:600], p0[:600] * decay), "zero grad, decayed segment"
+        assert np.array_equal(master[600:], p0[600:]), "zero grad, undecayed segment"
+        assert not m.any() and not v.any(), "zero grad moved m or v"
+
+
+def pin_adamw_lr_zero(orc):
+    r = rng(7)
+    n = 1000
+    p0 = (r.standard_normal(n) * 0.02).astype(np.float32)
+    hp = dict(BIG_HP, lr=0.0)
+    master, m, v = p0.copy(), np.zeros(n, np.float32), np.zeros(n, np.float32)
+    g = (r.standard_normal(n) * 1e-2).astype(np.float32)
+    for t in (1, 2, 3):
+        orc.adamw_step(np.array([0, n], np.int64), np.array([1], np.uint8), hp, t, g, master, m, v)
+    assert np.array_equal(master, p0), "lr = 0 changed the master weights"
+    assert m.any() and v.any(), "lr = 0 must still update the moments"
+
+
+# ---- (a3) FedAvg -------------------------------------------------------------
+
+def pin_fedavg_identical_replicas(orc):
+    r = rng(8)
+    x = random_bf16(r, 5000, std=0.02)
+    for G in (1, 2, 3, 4, 7, 8, 16):
+        w = r.uniform(0.1, 5.0, G).astype(np.float32)
+        master, work = orc.fedavg([x] * G, w)
+        assert np.array_equal(work, x), "FedAvg of identical replicas changed them (G=%d)" % G
+        err = np.abs(master.astype(np.float64) - bf16_decode(x))
+        assert np.all(err <= (G + 2) * U * np.abs(bf16_decode(x)) + TINY), "identity G=%d" % G
+        if G & (G - 1) == 0:
+            master, _ = orc.fedavg([x] * G, np.ones(G, np.float32))
+            assert np.array_equal(master.astype(np.float64), bf16_decode(x)), "equal weights G=%d" % G
+
+
+def pin_fedavg_two_group_mean(orc):
+    r = rng(9)
+    x0, x1 = random_bf16(r, 5000, 0.02), random_bf16(r, 5000, 0.02)
+    master, work = orc.fedavg([x0, x1], np.array([0.5, 0.5], np.float32))
+    want = ((bf16_decode(x0) + bf16_decode(x1)) / 2).astype(np.float32)
+    assert np.array_equal(master, want), "two-group mean is not the arithmetic mean"
+    assert np.array_equal(work, torch_bf16_bits(want)), "working copy of the mean"
+
+
+def pin_fedavg_vs_float64_average(orc):
+    r = rng(10)
+    for G in (2, 3, 8, 16):
+        n = 4096
+        reps = [random_bf16(r, n, 0.02) for _ in range(G)]
+        w = r.integers(1, 17, G).astype(np.float32)
+        master, work = orc.fedavg(reps, w)
+        dec = np.stack([bf16_decode(x) for x in reps])
+        wn = w.astype(np.float64) / w.astype(np.float64).sum()
+        exact = (wn[:, None] * dec).sum(0)
+        bound = (G + 2) * U * (wn[:, None] * np.abs(dec)).sum(0) + TINY
+        _check_close("fedavg G=%d" % G, master, exact, bound)
+        uniq = ~bf16_boundary_between(exact - bound, exact + bound)
+        assert np.array_equal(work[uniq], torch_bf16_bits(exact.astype(np.float32))[uniq]), \
+            "FedAvg working copy G=%d" % G
+
+
+def pin_fedavg_weight_scale_invariance(orc):
+    """A weighted average depends on the weights only up to a common factor."""
+    r = rng(11)
+    reps = [random_bf16(r, 3000, 0.02) for _ in range(6)]
+    w = r.integers(1, 17, 6).astype(np.float32)
+    a, _ = orc.fedavg(reps, w)
+    b, _ = orc.fedavg(reps, w * np.float32(4.0))
+    assert np.array_equal(a, b), "weights w and 4w give different averages"
+
+
+# ---- hand-derived exact cases (tests/golden/hand_cases.json) ----------------
+
+def pin_golden_hand_cases(orc):
+    with open(os.path.join(GOLDEN, "hand_cases.json")) as f:
+        cases = json.load(f)["cases"]
+    for c in cases:
+        kind = c["op"]
+        if kind == "reduce":
+            grads = [torch_bf16_bits(np.array(x, np.float32)) for x in c["peers"]]
+            g = orc.shard_reduce(grads, c["grad_scale"])
+            assert np.array_equal(g, np.array(c["expect_g"], np.float32)), c["name"]
+        elif kind == "fedavg":
+            reps = [torch_bf16_bits(np.array(x, np.float32)) for x in c["replicas"]]
+            master, work = orc.fedavg(reps, np.array(c["weights"], np.float32))
+            assert np.array_equal(master, np.array(c["expect_master"], np.float32)), c["name"]
+            assert np.array_equal(work, torch_bf16_bits(np.array(c["expect_master"], np.float32))), c["name"]
+        elif kind == "adamw":
+            n = len(c["p0"])
+            master = np.array(c["p0"], np.float32)
+            m = np.array(c["m0"], np.float32)
+            v = np.array(c["v0"], np.float32)
+            orc.adamw_step(np.array([0, n], np.int64), np.array([c["decay"]], np.uint8), c["hp"],
+                           c["t"], np.array(c["g"], np.float32), master, m, v)
+            assert np.array_equal(master, np.array(c["expect_p"], np.float32)), c["name"]
+            assert np.array_equal(m, np.array(c["expect_m"], np.float32)), c["name"]
+            assert np.array_equal(v, np.array(c["expect_v"], np.float32)), c["name"]
+        else:
+            raise AssertionError("unknown golden op " + kind)
+
+
+# ---- (a4) whole rounds: float64 brute force with error bounds ---------------
+
+def brute_force_round(hp, seg_off, seg_decay, R, G, A, self_group, grad_scale, step0, weights,
+                      grads, replicas, p0, m0, v0, oracle_working_after_steps=None):
+    """Straight-line float64 recomputation of one round, with a propagated
+    bound on the distance of any binary32 evaluation in the fixed order from
+    the exact result.  Returns dict of (value, bound) plus the per-step g and
+    its bound, and the masks of elements whose bf16 rounding is ambiguous."""
+    h = _hp_f(hp)
+    b1, b2, lr, wd, eps = h["beta1"], h["beta2"], h["lr"], h["weight_decay"], h["eps"]
+    n = int(seg_off[-1])
+    decay_flag = np.zeros(n, bool)
+    for s in range(len(seg_off) - 1):
+        decay_flag[seg_off[s]:seg_off[s + 1]] = bool(seg_decay[s])
+    decay = np.where(decay_flag, 1.0 - lr * wd, 1.0)
+    s_scale = float(np.float32(grad_scale))
+    p = p0.astype(np.float64).copy()
+    m = m0.astype(np.float64).copy()
+    v = v0.astype(np.float64).copy()
+    ep = np.zeros(n)
+    em = np.zeros(n)
+    ev = np.zeros(n)
+    mabs = np.abs(m)
+    gsteps = []
+    for a in range(A):
+        t = step0 + a
+        dec = np.stack([bf16_decode(grads[a * R + r]) for r in range(R)])
+        g = dec.sum(0) * s_scale
+        eg = (R + 1) * U * np.abs(dec).sum(0) * abs(s_scale)
+        gsteps.append((g, eg))
+        gab = np.abs(g) + eg
+        mabs = b1 * mabs + (1 - b1) * gab
+        m = b1 * m + (1 - b1) * g
+        em = b1 * em + (1 - b1) * eg + 4 * U * mabs
+        v = b2 * v + (1 - b2) * g * g
+        ev = b2 * ev + (1 - b2) * (2 * np.abs(g) * eg + eg * eg) + 5 * U * (b2 * v + (1 - b2) * gab * gab)
+        bc1 = 1 - b1 ** t
+        bc2s = np.sqrt(1 - b2 ** t)
+        s = np.sqrt(v)
+        es = np.minimum(ev / np.maximum(2 * s, TINY), np.sqrt(ev)) + U * s
+        den = s / bc2s + eps
+        eden = es / bc2s + 3 * U * (s + es) / bc2s + U * den
+        dlow = np.maximum(den - eden, eps * 0.5)
+        ratio = m / den
+        eratio = em / dlow + mabs * eden / (dlow * dlow) + 2 * U * mabs / dlow
+        step = lr / bc1
+        upd = step * ratio
+        eupd = step * eratio + 3 * U * step * mabs / dlow
+        pd = p * decay
+        ep = decay * ep + 2 * U * (np.abs(pd) + ep)
+        p = pd - upd
+        ep = ep + eupd + U * (np.abs(p) + ep)
+    ep, em, ev = 2 * ep + TINY, 2 * em + TINY, 2 * ev + TINY
+    # own bf16 working copy after the local steps
+    amb_w = bf16_boundary_between(p - ep, p + ep)
+    w_ref = torch_bf16_bits(p.astype(np.float32))
+    if oracle_working_after_steps is not None:
+        w_own = np.where(amb_w, oracle_working_after_steps, w_ref)
+    else:
+        w_own = w_ref
+    wv = np.asarray(weights, np.float32).astype(np.float64)
+    wn = wv / wv.sum()
+    reps = [w_own if k == self_group else replicas[k] for k in range(G)]
+    dec = np.stack([bf16_decode(x) for x in reps])
+    xbar = (wn[:, None] * dec).sum(0)
+    ex = 2 * (G + 2) * U * (wn[:, None] * np.abs(dec)).sum(0) + TINY
+    amb_f = bf16_boundary_between(xbar - ex, xbar + ex)
+    return dict(master=(xbar, ex), m=(m, em), v=(v, ev), p_steps=(p, ep), w_own=w_own,
+                amb_own=amb_w, amb_final=amb_f, g=gsteps)
+
+
+def _random_round_case(r, R, G, A, n=16, hp=None):
+    cuts = np.sort(r.choice(np.arange(1, n), size=r.integers(0, 4), replace=False))
+    off = np.concatenate([[0], cuts, [n]]).astype(np.int64)
+    flags = r.integers(0, 2, off.size - 1).astype(np.uint8)
+    grads = [random_bf16(r, n, std=10.0 ** r.uniform(-4, -1)) for _ in range(A * R)]
+    p0 = (r.standard_normal(n) * 0.02).astype(np.float32)
+    reps = [None if k == 0 else torch_bf16_bits((p0 + r.standard_normal(n) * 1e-3).astype(np.float32))
+            for k in range(G)]
+    self_group = int(r.integers(0, G))
+    if self_group != 0:
+        reps[0], reps[self_group] = reps[self_group], None
+    w = r.uniform(0.1, 2.0, G).astype(np.float32)
+    m0 = (r.standard_normal(n) * 1e-4).astype(np.float32)
+    v0 = (np.abs(r.standard_normal(n)) * 1e-7).astype(np.float32)
+    return dict(seg_off=off, seg_decay=flags, R=R, G=G, A=A, self_group=self_group,
+                grad_scale=1.0 / R, step0=int(r.integers(1, 20)), weights=w, grads=grads,
+                replicas=reps, p0=p0, m0=m0, v0=v0)
+
+
+def check_round_against_brute_force(orc, hp, case):
+    c = case
+    master, m, v = c["p0"].copy(), c["m0"].copy(), c["v0"].copy()
+    work = torch_bf16_bits(master)
+    # the oracle's own working copy after the local steps (used only where the
+    # bf16 rounding of the float64 value is ambiguous)
+    mw, mm, mv = master.copy(), m.copy(), v.copy()
+    ww = work.copy()
+    for a in range(c["A"]):
+        g = orc.shard_reduce(c["grads"][a * c["R"]:(a + 1) * c["R"]], c["grad_scale"])
+        orc.adamw_step(c["seg_off"], c["seg_decay"], hp, c["step0"] + a, g, mw, mm, mv, ww)
+    ss = orc.round(c["seg_off"], c["seg_decay"], c["R"], c["G"], c["A"], c["self_group"],
+                   c["grad_scale"], hp, c["step0"], c["weights"], c["grads"], c["replicas"],
+                   master, m, v, work, want_sumsq=True)
+    bf = brute_force_round(hp, c["seg_off"], c["seg_decay"], c["R"], c["G"], c["A"],
+                           c["self_group"], c["grad_scale"], c["step0"], c["weights"], c["grads"],
+                           c["replicas"], c["p0"], c["m0"], c["v0"], oracle_working_after_steps=ww)
+    tag = "R=%d G=%d A=%d self=%d" % (c["R"], c["G"], c["A"], c["self_group"])
+    own_ok = bf["amb_own"] | (ww == bf["w_own"])
+    assert np.all(own_ok), "working copy after the local steps, " + tag
+    for key, arr in (("master", master), ("m", m), ("v", v)):
+        val, bnd = bf[key]
+        _check_close("round %s %s" % (key, tag), arr, val, bnd)
+    xbar, _ = bf["master"]
+    uniq = ~bf["amb_final"]
+    assert np.array_equal(work[uniq], torch_bf16_bits(xbar.astype(np.float32))[uniq]), \
+        "round working copy " + tag
+    assert np.array_equal(work, torch_bf16_bits(master)), "working != bf16(master) " + tag
+    off = c["seg_off"]
+    for a, (g, eg) in enumerate(bf["g"]):
+        for s in range(off.size - 1):
+            sl = slice(off[s], off[s + 1])
+            want = np.sum(g[sl] ** 2)
+            bound = np.sum(2 * np.abs(g[sl]) * eg[sl] + eg[sl] ** 2) * 2 + 1e-12 * want + TINY
+            assert abs(ss[a, s] - want) <= bound, "seg_sumsq step %d seg %d %s" % (a, s, tag)
+
+
+def pin_round_brute_force_16(orc):
+    """Every (R, G, A) in {1..4}^3 on 16-element shards with random segment
+    splits, decay flags, self group, weights and starting state."""
+    r = rng(12)
+    for hp in (STD_HP, BIG_HP):
+        for R in range(1, 5):
+            for G in range(1, 5):
+                for A in range(1, 5):
+                    check_round_against_brute_force(orc, hp, _random_round_case(r, R, G, A))
+
+
+def pin_round_single_step_single_group(orc):
+    """A = 1, G = 1, w = 1: one AdamW step, then FedAvg is the identity on the
+    working copy, so master becomes the widened working copy."""
+    r = rng(13)
+    n = 777
+    c = _random_round_case(r, 2, 1, 1, n=n)
+    c["self_group"] = 0
+    c["replicas"] = [None]
+    c["weights"] = np.array([1.0], np.float32)
+    master, m, v = c["p0"].copy(), c["m0"].copy(), c["v0"].copy()
+    work = np.zeros(n, np.uint16)
+    orc.round(c["seg_off"], c["seg_decay"], 2, 1, 1, 0, 0.5, STD_HP, c["step0"], c["weights"],
+              c["grads"], c["replicas"], master, m, v, work)
+    bf = brute_force_round(STD_HP, c["seg_off"], c["seg_decay"], 2, 1, 1, 0, 0.5, c["step0"],
+                           c["weights"], c["grads"], c["replicas"], c["p0"], c["m0"], c["v0"])
+    p, ep = bf["p_steps"]
+    uniq = ~bf["amb_own"]
+    assert np.array_equal(work[uniq], torch_bf16_bits(p.astype(np.float32))[uniq]), "A=1,G=1 working"
+    assert np.array_equal(master.astype(np.float64), bf16_decode(work)), "A=1,G=1 master"
+
+
+def pin_round_uses_own_working_copy(orc):
+    """The own replica entering FedAvg is this group's freshly updated bf16
+    working copy: with G = 2 and the other replica equal to the pre-round
+    working copy, a round with lr > 0 must differ from the stale average."""
+    r = rng(14)
+    n = 512
+    c = _random_round_case(r, 1, 2, 2, n=n)
+    c["self_group"] = 1
+    stale = torch_bf16_bits(c["p0"])
+    c["replicas"] = [stale, None]
+    c["weights"] = np.array([0.0, 1.0], np.float32)
+    master, m, v = c["p0"].copy(), c["m0"].copy(), c["v0"].copy()
+    work = stale.copy()
+    orc.round(c["seg_off"], c["seg_decay"], 1, 2, 2, 1, 1.0, BIG_HP, c["step0"], c["weights"],
+              c["grads"], c["replicas"], master, m, v, work)
+    # weight 0 on the other group: the result is the own updated copy
+    bf = brute_force_round(BIG_HP, c["seg_off"], c["seg_decay"], 1, 2, 2, 1, 1.0, c["step0"],
+                           c["weights"], c["grads"], c["replicas"], c["p0"], c["m0"], c["v0"])
+    xbar, ex = bf["master"]
+    _check_close("own copy", master, xbar, ex)
+    assert not np.array_equal(work, stale), "round did not use the updated working copy"
+
+
+ALL_PINS = [
+    pin_bf16_decode_all_patterns,
+    pin_bf16_encode_matches_torch,
+    pin_bf16_encode_nan,
+    pin_reduce_vs_float64_sum,
+    pin_reduce_identical_peers_exact,
+    pin_seg_sumsq_vs_numpy,
+    pin_adamw_vs_torch_float64,
+    pin_adamw_first_step_closed_form,
+    pin_adamw_zero_grad,
+    pin_adamw_lr_zero,
+    pin_fedavg_identical_replicas,
+    pin_fedavg_two_group_mean,
+    pin_fedavg_vs_float64_average,
+    pin_fedavg_weight_scale_invariance,
+    pin_golden_hand_cases,
+    pin_round_brute_force_16,
+    pin_round_single_step_single_group,
+    pin_round_uses_own_working_copy,
+]

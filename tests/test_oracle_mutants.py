@@ -1,0 +1,98 @@
+"""Plant plausible mistakes in copies of the oracle and require that the pins
+catch every one of them (CPU only).
+
+Each mutant is a textual edit of oracle/oracle.c (a dropped term, a wrong sign
+or index, a swapped operand, a misplaced step).  The edited copy is built
+into a temporary directory; the real oracle is never modified.
+"""
+import os
+import shutil
+import tempfile
+
+import pytest
+
+import oracle
+from oracle import build as oracle_build
+import pins
+
+SRC = os.path.join(os.path.dirname(oracle.__file__), "oracle.c")
+
+MUTANTS = {
+    "reduce_wrong_peer_index": [("orc_bf16_to_f32(grads[r][i])", "orc_bf16_to_f32(grads[0][i])")],
+    "reduce_dropped_scale": [("g[i] = acc * grad_scale;", "g[i] = acc;")],
+    "reduce_reverse_order": [("for (int r = 0; r < R; ++r) acc = acc + orc_bf16_to_f32(grads[r][i]);",
+                              "for (int r = R - 1; r >= 0; --r) acc = acc + orc_bf16_to_f32(grads[r][i]);")],
+    "adamw_dropped_decay": [("float p = master[i] * decay;", "float p = master[i];")],
+    "adamw_decay_after_update": [("float p = master[i] * decay;", "float p = master[i];"),
+                                 ("p = p - (step_size * (mn / den));",
+                                  "p = (p - (step_size * (mn / den))) * decay;")],
+    "adamw_m_sign": [("(b1 * m[i]) + (omb1 * gi)", "(b1 * m[i]) - (omb1 * gi)")],
+    "adamw_swapped_betas": [("(b2 * v[i]) + (omb2 * (gi * gi))", "(b1 * v[i]) + (omb2 * (gi * gi))")],
+    "adamw_v_not_squared": [("(omb2 * (gi * gi))", "(omb2 * gi)")],
+    "adamw_eps_inside_sqrt": [("(sqrtf(vn) / bc2_sqrt) + eps", "sqrtf(vn + eps) / bc2_sqrt")],
+    "adamw_no_bias_correction1": [("const float step_size = (float)(lr / bc1);",
+                                   "const float step_size = (float)lr;")],
+    "adamw_no_bias_correction2": [("const float bc2_sqrt = (float)sqrt(bc2);",
+                                   "const float bc2_sqrt = 1.0f;")],
+    "adamw_bc2_not_rooted": [("const float bc2_sqrt = (float)sqrt(bc2);",
+                              "const float bc2_sqrt = (float)bc2;")],
+    "adamw_step_off_by_one": [("pow((double)h->beta1, (double)t)", "pow((double)h->beta1, (double)(t + 1))"),
+                              ("pow((double)h->beta2, (double)t)", "pow((double)h->beta2, (double)(t + 1))")],
+    "adamw_update_sign": [("p = p - (step_size * (mn / den));", "p = p + (step_size * (mn / den));")],
+    "adamw_old_m_in_update": [("p = p - (step_size * (mn / den));", "p = p - (step_size * (m[i] / den));")],
+    "adamw_decay_ignores_flags": [("(seg_decay == NULL || seg_decay[s]) ? decay_on : 1.0f", "decay_on")],
+    "adamw_working_truncated": [("if (working) working[i] = orc_f32_to_bf16(p);",
+                                 "if (working) working[i] = (uint16_t)(*(uint32_t*)&p >> 16);")],
+    "fedavg_unnormalised": [("out[k] = (float)((double)w[k] / sum);", "out[k] = w[k];")],
+    "fedavg_wrong_replica_index": [("(wn[k] * orc_bf16_to_f32(replicas[k][i]))",
+                                    "(wn[k] * orc_bf16_to_f32(replicas[0][i]))")],
+    "fedavg_master_as_bf16": [("master_out[i] = acc;",
+                               "master_out[i] = orc_bf16_to_f32(orc_f32_to_bf16(acc));")],
+    "fedavg_reverse_order": [("for (int k = 0; k < G; ++k) acc = acc + (wn[k] * orc_bf16_to_f32(replicas[k][i]));",
+                              "for (int k = G - 1; k >= 0; --k) acc = acc + (wn[k] * orc_bf16_to_f32(replicas[k][i]));")],
+    "round_stale_own_replica": [("reps[k] = (k == self_group) ? working : replicas[k];",
+                                 "reps[k] = (k == self_group) ? replicas[(k + 1) % G] : replicas[k];")],
+    "round_same_step_number": [("h, step0 + a, g, master", "h, step0, g, master")],
+    "round_skips_fedavg": [("rc = orc_fedavg(n, G, reps, weights, master, working);", "rc = 0;")],
+    "round_reuses_first_grads": [("grads + (size_t)a * (size_t)R", "grads")],
+    "sumsq_off_by_one": [("for (int64_t i = seg_off[s]; i < seg_off[s + 1]; ++i) sum +=",
+                          "for (int64_t i = seg_off[s] + 1; i < seg_off[s + 1]; ++i) sum +=")],
+    "sumsq_not_squared": [("sum += (double)g[i] * (double)g[i];", "sum += (double)g[i];")],
+    "bf16_ties_away": [("(lower == 0x8000u && (upper & 1u))", "(lower == 0x8000u)")],
+    "bf16_truncate": [("if (lower > 0x8000u || (lower == 0x8000u && (upper & 1u))) upper += 1u;", "")],
+    "bf16_nan_not_quiet": [("return (uint16_t)((u >> 16) | 0x0040u);", "return (uint16_t)(u >> 16);")],
+    "bf16_decode_shift": [("uint32_t u = (uint32_t)h << 16;", "uint32_t u = (uint32_t)h << 15;")],
+}
+
+
+@pytest.fixture(scope="module")
+def workdir():
+    d = tempfile.mkdtemp(prefix="oracle_mutants_")
+    yield d
+    shutil.rmtree(d, ignore_errors=True)
+
+
+def _build_mutant(workdir, name, edits):
+    src = open(SRC).read()
+    for old, new in edits:
+        assert src.count(old) == 1, "mutation %s: pattern not unique or missing: %r" % (name, old)
+        src = src.replace(old, new)
+    path = os.path.join(workdir, name + ".c")
+    with open(path, "w") as f:
+        f.write(src)
+    return oracle_build.build(out=os.path.join(workdir, "lib" + name + ".so"), src=path,
+                              include_dir=os.path.dirname(SRC))
+
+
+@pytest.mark.parametrize("name", sorted(MUTANTS))
+def test_mutant_is_caught(workdir, name):
+    lib_path = _build_mutant(workdir, name, MUTANTS[name])
+    orc = oracle.Oracle(lib_path)
+    caught = []
+    for pin in pins.ALL_PINS:
+        try:
+            pin(orc)
+        except (AssertionError, ValueError, FloatingPointError) as e:
+            caught.append((pin.__name__, str(e)[:120]))
+            break
+    assert caught, "planted mistake %s passed every pin" % name
