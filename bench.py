@@ -1,0 +1,203 @@
+"""Benchmark of one GPU's share of the FL+FSDP parameter sync (fl_round).
+
+A step is one fl_round: A = 8 fused local steps (R = 8 peer gradients ->
+AdamW on the fp32 master shard -> bf16 working copy) and one FedAvg of G = 4
+federation-group replicas, on the Llama-3.1-8B shard of a rank in a sharding
+group of 8 (N = 1,003,782,144 parameters in 290 segments), with every input
+already resident in HBM.  Prints one JSON line.
+
+    python bench.py [--steps K] [--warmup W] [--workload NAME] [--no-cpu]
+"""
+import argparse
+import hashlib
+import json
+import os
+import re
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "effective HBM GB/s (% of MI355X peak) and params/s per fl_round, 8B-shaped shard"
+PEAK_HBM_GBS = 8000.0   # MI355X HBM3E, 8 TB/s
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_local_step_llama31_8b_s8.md")
+KERNEL_SOURCES = [os.path.join(ROOT, "paper_2609_20359_amd", "csrc", f)
+                  for f in ("flround_kernels.hip", "flr_internal.h")]
+
+
+def log(*a):
+    print("[bench]", *a, file=sys.stderr, flush=True)
+
+
+def kernel_source_hash():
+    h = hashlib.sha256()
+    for p in KERNEL_SOURCES:
+        with open(p, "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def read_traffic(current_hash):
+    """Counter-measured HBM bytes per local-step launch (from the rocprofv3
+    --pmc summary committed under profiles/), or None if there is none or the
+    kernel source changed since it was taken."""
+    if not os.path.exists(TRAFFIC_FILE):
+        return None
+    txt = open(TRAFFIC_FILE).read()
+    fields = dict(re.findall(r"^- (\w+): (\S+)$", txt, flags=re.M))
+    if fields.get("kernel_source_hash") != current_hash:
+        return None
+    try:
+        return float(fields["hbm_bytes_per_launch"])
+    except (KeyError, ValueError):
+        return None
+
+
+def cpu_baseline(w, n_sample):
+    """The oracle as it stands, one thread, one full round on the first
+    n_sample elements of the same shard (same generator, same segments)."""
+    import numpy as np
+
+    import oracle
+    import synth.buffers as B
+
+    orc = oracle.Oracle()
+    idx = np.arange(n_sample, dtype=np.int64)
+    off = w.seg_offsets[w.seg_offsets < n_sample]
+    off = np.append(off, n_sample).astype(np.int64)
+    dec = w.seg_decay[:off.size - 1]
+    host = B.HostInputs(w, idx)
+    t0 = time.perf_counter()
+    orc.round(off, dec, w.R, w.G, w.A, w.self_group, w.grad_scale, w.hp, w.step0, w.weights,
+              host.grads, host.replicas, host.master, host.m, host.v, host.working)
+    dt = time.perf_counter() - t0
+    bytes_round = n_sample * (w.A * w.step_bytes_per_param() + w.fedavg_bytes_per_param())
+    return dict(value=round(bytes_round / dt / 1e9, 4), unit="GB/s", cores=1, kind="oracle",
+                params_per_s=round(n_sample / dt, 1), seconds=round(dt, 3),
+                sample="one fl_round (A=%d, R=%d, G=%d) on the first %d elements of the same "
+                       "shard (%d segment(s)), single-threaded C oracle" % (
+                           w.A, w.R, w.G, n_sample, off.size - 1))
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="llama8b_s8")
+    ap.add_argument("--cpu-sample", type=int, default=32 << 20)
+    ap.add_argument("--no-cpu", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print("bench.py measures one GPU's share of the path; the multi-GPU collectives are "
+              "not part of this build, so --gpus %d is not supported (use --gpus 1)"
+              % args.gpus, file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    import paper_2609_20359_amd as P
+    import synth.buffers as B
+    from synth import workloads as W
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(1)
+    torch.cuda.set_device(0)
+    P.lib()
+    w = W.ALL[args.workload]()
+    log("workload", w.describe())
+    lay = P.Layout(w.seg_offsets, w.seg_decay)
+    t0 = time.perf_counter()
+    dev = B.DeviceInputs(w)
+    torch.cuda.synchronize()
+    log("inputs resident: %.1f GB in %.1f s" % (dev.bytes() / 1e9, time.perf_counter() - t0))
+
+    stream = torch.cuda.current_stream()
+    K, Wm = args.steps, args.warmup
+    events = [P.HipEvents(w.A + 2) for _ in range(K)]
+    cfg_plain = P.make_round_cfg(w.R, w.G, w.A, w.weights, w.hp, self_group=w.self_group,
+                                 grad_scale=w.grad_scale, step0=w.step0)
+    for i in range(Wm):
+        P.fl_round(lay, cfg_plain, dev.grads, dev.replicas, dev.master, dev.m, dev.v, dev.working)
+    torch.cuda.synchronize()
+    log("warmup done (%d rounds)" % Wm)
+
+    cfgs = [P.make_round_cfg(w.R, w.G, w.A, w.weights, w.hp, self_group=w.self_group,
+                             grad_scale=w.grad_scale, step0=w.step0 + w.A * (Wm + k),
+                             phase_events=events[k].handles) for k in range(K)]
+    start = torch.cuda.Event(enable_timing=True)
+    stop = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t_wall = time.perf_counter()
+    start.record(stream)
+    for k in range(K):
+        P.fl_round(lay, cfgs[k], dev.grads, dev.replicas, dev.master, dev.m, dev.v, dev.working)
+    stop.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t_wall
+    total_ms = start.elapsed_time(stop)
+    ms_round = total_ms / K
+    step_ms = [events[k].elapsed_ms(a, a + 1) for k in range(K) for a in range(w.A)]
+    fed_ms = [events[k].elapsed_ms(w.A, w.A + 1) for k in range(K)]
+    avg_step = sum(step_ms) / len(step_ms)
+    avg_fed = sum(fed_ms) / len(fed_ms)
+    log("timed %d rounds: %.3f ms/round (wall %.3f s); local step %.3f ms, fedavg %.3f ms"
+        % (K, ms_round, wall, avg_step, avg_fed))
+
+    bytes_round = w.round_bytes()
+    gbs = bytes_round / (ms_round * 1e-3) / 1e9
+    step_bytes = w.n * w.step_bytes_per_param()
+    fed_bytes = w.n * w.fedavg_bytes_per_param()
+    achieved = step_bytes / (avg_step * 1e-3) / 1e9
+    src_hash = kernel_source_hash()
+    traffic = read_traffic(src_hash)
+    out = {
+        "metric": METRIC,
+        "value": round(gbs, 2),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": K,
+        "warmup": Wm,
+        "ms_per_step": round(ms_round, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": dict(workload=w.name, n_params=w.n, segments=w.n_seg, R=w.R, G=w.G, A=w.A,
+                       storage="bf16 gradients/replicas/working copy, fp32 master/m/v",
+                       bytes_per_round=bytes_round, parallelism="one GPU's shard"),
+        "pct_of_peak": round(100.0 * gbs / PEAK_HBM_GBS, 2),
+        "params_per_s": round(w.n / (ms_round * 1e-3), 1),
+        "phases_ms": dict(local_step=round(avg_step, 4), fedavg=round(avg_fed, 4),
+                          fedavg_gbs=round(fed_bytes / (avg_fed * 1e-3) / 1e9, 2)),
+        "roofline": {
+            "bound": "hbm",
+            "kernel": "k_step<R=8, fused> (one local step)",
+            "achieved": round(achieved, 2),
+            "peak": PEAK_HBM_GBS,
+            "unit": "GB/s",
+            "frac": round(achieved / PEAK_HBM_GBS, 4),
+            "traffic": traffic,
+            "algorithmic_bytes": step_bytes,
+            "kernel_source_hash": src_hash,
+        },
+    }
+    del dev
+    torch.cuda.empty_cache()
+    if not args.no_cpu:
+        log("cpu baseline: oracle on %d elements" % args.cpu_sample)
+        out["cpu_baseline"] = cpu_baseline(w, args.cpu_sample)
+        log("cpu baseline done: %.1f s" % out["cpu_baseline"]["seconds"])
+    else:
+        out["cpu_baseline"] = None
+    print(json.dumps(out), flush=True)
+    for e in events:
+        e.close()
+    lay.close()
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,238 @@
+/*
+ * flround.h -- C ABI of libflround: one GPU's share of the parameter
+ * synchronisation in FL+FSDP and FL+HSDP training, on AMD Instinct MI355X
+ * (gfx950).
+ *
+ * The method (Section 4.2) runs F federation groups, each an FSDP (or HSDP)
+ * deployment with the same sharding policy.  Every local step, each rank
+ * reduce-scatters the gradients of its sharding group and applies the inner
+ * optimiser (AdamW, Section 5) to its shard; every A steps the ranks that hold
+ * corresponding shards in the F groups replace them by their weighted average
+ * (FedAvg, Section 2 and Section 4.1 Eq. (3); Eq. (4) and Eq. (5) for the
+ * FSDP and HSDP variants).  This library computes, for one rank's flat shard
+ * of N elements, the arithmetic of that schedule with the collectives already
+ * done: the peers' gradient contributions and the other groups' replicas are
+ * plain device buffers.
+ *
+ * Notation: N shard elements, split into n_seg segments (slices of layers,
+ * the unit FSDP shards equally -- Section 2); R peers of the sharding group
+ * (the paper's S); G federation groups (the paper's F); A local steps
+ * between aggregations.
+ *
+ * Conventions, for every function below:
+ *  - Return value: an fl_status.  Nothing throws, aborts or prints.
+ *  - Every argument is checked before anything is enqueued; on an error
+ *    nothing has been launched and no output has been touched.
+ *  - "Device pointer" arguments point to device memory of the device that
+ *    was current when the layout was created; that device must be current at
+ *    the call (else FL_ERR_DEVICE).  They must be 16-byte aligned
+ *    (FL_ERR_ALIGN).  They may be NULL only when N == 0.  The caller owns all
+ *    of them; the library keeps no pointer after a call returns.
+ *  - Arrays of pointers ("host array of device pointers") and weight or
+ *    fingerprint arrays live in host memory and are read during the call.
+ *  - Work is enqueued on `stream` (a hipStream_t; NULL = the null stream)
+ *    and the call returns without waiting for it.  A launch failure returns
+ *    FL_ERR_HIP.
+ *  - bf16 values are passed as their 16-bit patterns (uint16_t).
+ *  - Arithmetic: fp32, in the operation order stated per function, each
+ *    operation correctly rounded (no contraction into FMA, subnormals kept);
+ *    bf16 results are rounded to nearest even from fp32, NaN stays NaN.
+ *    Results are bitwise independent of the launch configuration.
+ *  - Calls that write the same buffers must not overlap in time.
+ */
+#ifndef FLROUND_H
+#define FLROUND_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  FL_OK = 0,
+  FL_ERR_INVALID = -1, /* NULL where not allowed, value out of range, non-finite */
+  FL_ERR_ALIGN = -2,   /* a device pointer is not 16-byte aligned               */
+  FL_ERR_LAYOUT = -3,  /* a replica's layout fingerprint differs from ours      */
+  FL_ERR_DEVICE = -4,  /* current device is not the layout's device             */
+  FL_ERR_HIP = -5,     /* a HIP runtime call or a kernel launch failed          */
+  FL_ERR_NOMEM = -6    /* host or device allocation failed                      */
+} fl_status;
+
+#define FL_MAX_PEERS 64  /* upper bound on R */
+#define FL_MAX_GROUPS 64 /* upper bound on G */
+
+/* Human-readable name of a status code (static storage). */
+const char* fl_status_string(int status);
+
+/* ABI version: (major << 16) | minor. */
+int fl_version(void);
+
+/* ------------------------------------------------------------------------
+ * Shard layout.  The flat shard of N elements is the concatenation of
+ * n_seg segments; segment s covers [seg_offsets[s], seg_offsets[s+1]) and
+ * takes weight decay iff seg_decay[s] != 0.  All federation groups must use
+ * the same layout (the alignment constraint of Section 4.2); the
+ * fingerprint lets a caller check that before averaging.
+ *
+ * fl_layout_create: n >= 0; n_seg >= 1 when n > 0 (n_seg == 0 allowed only
+ *   for n == 0); seg_offsets: host array of n_seg + 1 values, [0] == 0,
+ *   strictly increasing, [n_seg] == n; seg_decay: host array of n_seg flags,
+ *   or NULL for "every segment decays".  Uploads small per-segment and
+ *   per-tile tables (about 16 bytes per 2048 elements) to the current device;
+ *   returns FL_ERR_NOMEM / FL_ERR_HIP if that fails.  *out receives an
+ *   immutable handle that may be used from several streams at once.
+ * fl_layout_destroy: frees the handle and its device tables (NULL is OK).
+ *   The caller must ensure no enqueued call still uses it.
+ * ---------------------------------------------------------------------- */
+typedef struct fl_layout fl_layout;
+
+int fl_layout_create(int64_t n, int64_t n_seg, const int64_t* seg_offsets,
+                     const uint8_t* seg_decay, fl_layout** out);
+int fl_layout_destroy(fl_layout* layout);
+int64_t fl_layout_numel(const fl_layout* layout);        /* N, or -1 on NULL     */
+int64_t fl_layout_num_segments(const fl_layout* layout); /* n_seg, or -1 on NULL */
+
+/* 64-bit FNV-1a hash of (n, n_seg, seg_offsets, decay flags as 0/1).
+ * fl_fingerprint computes it on the host without a GPU (0 if the arguments
+ * would not make a valid layout); fl_layout_fingerprint returns the
+ * layout's (0 on NULL). */
+uint64_t fl_fingerprint(int64_t n, int64_t n_seg, const int64_t* seg_offsets,
+                        const uint8_t* seg_decay);
+uint64_t fl_layout_fingerprint(const fl_layout* layout);
+
+/* AdamW hyperparameters (Section 5: AdamW, lr 3e-4).  Requirements:
+ * finite; lr >= 0; 0 <= beta1 < 1; 0 <= beta2 < 1; eps > 0;
+ * weight_decay >= 0. */
+typedef struct {
+  float lr, beta1, beta2, eps, weight_decay;
+} fl_adamw_hparams;
+
+/* ------------------------------------------------------------------------
+ * fl_shard_reduce -- local arithmetic of the intra-group gradient
+ * reduce-scatter (Section 2, FSDP; Eq. (1)): the R peers' bf16 contributions
+ * to this rank's shard, summed in fp32 in ascending peer order and scaled
+ * (grad_scale = 1/R averages, as the collectives of Section 5.1 do):
+ *     acc = 0; for r in 0..R-1: acc = acc + f32(peer_grads[r][i]);
+ *     grad_out[i] = acc * grad_scale
+ * peer_grads: host array of R device pointers to N bf16 values (may repeat).
+ * grad_out: device pointer, N floats (must not overlap an input).
+ * seg_sumsq: NULL, or device pointer to n_seg floats receiving, per segment,
+ *   the sum of grad_out[i]^2 (fp32 squares, partial sums in a fixed tree,
+ *   final sum in double): per-layer gradient-norm telemetry.  Needs a
+ *   stream-ordered temporary of 4 bytes per (2048-element tile, segment)
+ *   pair, allocated and freed on `stream`.
+ * 1 <= R <= FL_MAX_PEERS; grad_scale finite.
+ * ---------------------------------------------------------------------- */
+int fl_shard_reduce(const fl_layout* layout, int R, const uint16_t* const* peer_grads,
+                    float grad_scale, float* grad_out, float* seg_sumsq, void* stream);
+
+/* ------------------------------------------------------------------------
+ * fl_adamw_step -- one AdamW step (Section 5) of the fp32 master shard at
+ * step number `step` (1-based), decoupled weight decay first, bias-corrected
+ * moments, eps outside the square root; then the bf16 working copy that the
+ * next forward pass all-gathers (Section 2, FSDP):
+ *     p  = master[i] * decay_s            (decay_s = 1 - lr*wd if segment s
+ *                                          decays, else 1)
+ *     mn = beta1 * m[i] + (1 - beta1) * g[i]
+ *     vn = beta2 * v[i] + (1 - beta2) * (g[i] * g[i])
+ *     p  = p - step_size * (mn / (sqrt(vn) / bc2_sqrt + eps))
+ *     master[i] = p; m[i] = mn; v[i] = vn; working[i] = bf16(p)
+ * with step_size = lr / (1 - beta1^step), bc2_sqrt = sqrt(1 - beta2^step),
+ * 1 - beta and decay_s computed on the host in double and rounded to float.
+ * grad: device, N floats.  master, m, v: device, N floats each, updated in
+ * place, pairwise distinct.  working: device, N bf16, or NULL to skip.
+ * ---------------------------------------------------------------------- */
+int fl_adamw_step(const fl_layout* layout, const fl_adamw_hparams* h, int64_t step,
+                  const float* grad, float* master, float* m, float* v, uint16_t* working,
+                  void* stream);
+
+/* ------------------------------------------------------------------------
+ * fl_local_step -- fl_shard_reduce followed by fl_adamw_step in one pass:
+ * the reduced gradient stays in registers (nothing runs between the
+ * reduce-scatter's completion and the optimiser on the shard).  Bitwise
+ * equal to the two-call chain.  working is required here.
+ * ---------------------------------------------------------------------- */
+int fl_local_step(const fl_layout* layout, const fl_adamw_hparams* h, int64_t step, int R,
+                  const uint16_t* const* peer_grads, float grad_scale, float* master, float* m,
+                  float* v, uint16_t* working, float* seg_sumsq, void* stream);
+
+/* ------------------------------------------------------------------------
+ * fl_fedavg -- FedAvg of G federation-group replicas of this shard
+ * (Section 2, Federated Learning; Section 4.1 Eq. (3); Section 4.2: after
+ * aggregation every shard equals the average of its corresponding shards,
+ * so every group sums the same bf16 inputs in the same ascending order and
+ * ends bit-identical):
+ *     w'_g = w_g / sum_g w_g        (host, double, rounded to float)
+ *     acc = 0; for g in 0..G-1: acc = acc + w'_g * f32(replicas[g][i])
+ *     master_out[i] = acc; working_out[i] = bf16(acc)
+ * Optimiser moments are not touched.
+ * replicas: host array of G device pointers to N bf16 values; the caller's
+ *   own replica is its working copy and may be passed as one entry, and
+ *   working_out may then be that same pointer (in-place average).  Any
+ *   other overlap of outputs with inputs is undefined.
+ * weights: host array of G finite values >= 0 with a positive sum
+ *   (e.g. per-group sample counts).
+ * replica_fp: NULL, or host array of G layout fingerprints, one per replica;
+ *   any entry that differs from this layout's -> FL_ERR_LAYOUT.
+ * master_out: device, N floats.  working_out: device, N bf16.
+ * 1 <= G <= FL_MAX_GROUPS.
+ * ---------------------------------------------------------------------- */
+int fl_fedavg(const fl_layout* layout, int G, const uint16_t* const* replicas,
+              const float* weights, const uint64_t* replica_fp, float* master_out,
+              uint16_t* working_out, void* stream);
+
+/* ------------------------------------------------------------------------
+ * fl_round -- one federated round on this shard (Section 4.2, Eq. (4) and
+ * Eq. (5)): A local steps, then FedAvg after the A-th local update:
+ *     for a in 0..A-1: fl_local_step(step = step0 + a,
+ *                                    peer_grads = grads[a*R .. a*R+R-1])
+ *     fl_fedavg(replicas with replicas[self_group] := working,
+ *               master_out = master, working_out = working)
+ * Bitwise equal to that chain of calls.
+ * grads: host array of A*R device pointers (step-major; entries may repeat).
+ * replicas: host array of G device pointers; entry self_group is ignored
+ *   (may be NULL).
+ * master, m, v: device, N floats; working: device, N bf16; all updated in
+ *   place and pairwise distinct.
+ * seg_sumsq: NULL, or device pointer to A*n_seg floats (row a = local step a;
+ *   see fl_shard_reduce).
+ * Configuration: 1 <= R <= FL_MAX_PEERS, 1 <= G <= FL_MAX_GROUPS, A >= 1,
+ *   0 <= self_group < G, step0 >= 1, grad_scale finite, h and weights as
+ *   above, replica_fp as in fl_fedavg.
+ * phase_events: NULL, or host array of A+2 hipEvent_t created by the caller;
+ *   event a (a < A) is recorded on `stream` before local step a, event A
+ *   before FedAvg, event A+1 after it (per-phase timing of the round, like
+ *   the optimiser / aggregation split of Table 4).
+ * ---------------------------------------------------------------------- */
+typedef struct {
+  int R;                     /* peers in the sharding group                 */
+  int G;                     /* federation groups                           */
+  int A;                     /* local steps between aggregations            */
+  int self_group;            /* index of this rank's group among the G      */
+  float grad_scale;          /* 1/R for averaging                           */
+  fl_adamw_hparams h;        /* inner optimiser                             */
+  int64_t step0;             /* step number of the round's first local step */
+  const float* weights;      /* host, G FedAvg weights                      */
+  const uint64_t* replica_fp;/* NULL or host, G fingerprints                */
+  void* const* phase_events; /* NULL or host, A+2 hipEvent_t                */
+} fl_round_cfg;
+
+int fl_round(const fl_layout* layout, const fl_round_cfg* cfg, const uint16_t* const* grads,
+             const uint16_t* const* replicas, float* master, float* m, float* v,
+             uint16_t* working, float* seg_sumsq, void* stream);
+
+/* ------------------------------------------------------------------------
+ * Launch-shape control, for tuning sweeps and for tests that check that
+ * results do not depend on the launch shape.  blocks_per_cu > 0 caps the
+ * grid of the streaming kernels at blocks_per_cu * (number of CUs); 0
+ * restores the default.  Process-wide; returns the previous value.
+ * ---------------------------------------------------------------------- */
+int fl_set_blocks_per_cu(int blocks_per_cu);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* FLROUND_H */

@@ -1,0 +1,16 @@
+"""MI355X-native parameter-sync path of FL+FSDP / FL+HSDP training.
+
+One GPU's share of the method of "Accelerating Sharded Data Parallelism at
+Scale with Federated Learning" (Section 4.2): the local arithmetic of the
+gradient reduce-scatter, the AdamW step on the fp32 master shard, and the
+FedAvg of the federation groups' replicas, as a C-ABI library (libflround.so,
+include/flround.h) of hand-written gfx950 kernels.  The Python face below is a
+thin ctypes binding with the same names.
+"""
+from .flround import (FL_MAX_GROUPS, FL_MAX_PEERS, FlError, HipEvents, Layout, fingerprint,
+                      fl_adamw_step, fl_fedavg, fl_local_step, fl_round, fl_shard_reduce, lib,
+                      make_round_cfg, set_blocks_per_cu, status_string)
+
+__all__ = ["FL_MAX_GROUPS", "FL_MAX_PEERS", "FlError", "HipEvents", "Layout", "fingerprint",
+           "fl_adamw_step", "fl_fedavg", "fl_local_step", "fl_round", "fl_shard_reduce", "lib",
+           "make_round_cfg", "set_blocks_per_cu", "status_string"]

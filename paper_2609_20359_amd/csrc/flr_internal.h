@@ -1,0 +1,80 @@
+// flr_internal.h -- types shared by the C-ABI layer (flround_api.cpp) and the
+// gfx950 kernels (flround_kernels.hip).  Not part of the public ABI.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace flr {
+
+constexpr int kBlock = 256;            // threads per workgroup (4 wave64)
+constexpr int kVec = 8;                // elements per thread per tile (16 B of bf16)
+constexpr int kTile = kBlock * kVec;   // elements per tile: 2048
+constexpr int kMaxPeers = 64;
+constexpr int kMaxGroups = 64;
+
+// Per-tile descriptor of the segment structure, 16 bytes.
+//   seg0   first segment overlapping the tile
+//   nseg   number of segments overlapping it (1: the whole tile is in seg0)
+//   piece0 index of the tile's first (tile, segment) piece; the tile owns
+//          pieces piece0 .. piece0 + nseg - 1, one per overlapping segment
+//   decay  when nseg == 1: seg0's weight-decay flag
+struct TileInfo {
+  int32_t seg0;
+  int32_t nseg;
+  int32_t piece0;
+  int32_t decay;
+};
+
+// Device view of a layout.
+struct LayoutDev {
+  int64_t n;
+  int64_t n_seg;
+  int64_t n_tiles;
+  int64_t n_pieces;
+  const int64_t* seg_off;     // n_seg + 1
+  const uint8_t* seg_decay;   // n_seg, 0/1
+  const TileInfo* tiles;      // n_tiles
+  const int64_t* seg_piece0;  // n_seg + 1: pieces of segment s are
+                              // [seg_piece0[s], seg_piece0[s+1])
+};
+
+// Per-step AdamW scalars, computed on the host in double, rounded to float.
+struct AdamScalars {
+  float b1, omb1, b2, omb2;
+  float step_size, bc2_sqrt, eps, decay;
+};
+
+// Arguments of the local-step family (reduce, AdamW, fused step).
+struct StepArgs {
+  LayoutDev L;
+  const uint16_t* grads[kMaxPeers];
+  int R;
+  float grad_scale;
+  AdamScalars s;
+  float* master;
+  float* m;
+  float* v;
+  uint16_t* working;   // may be null for the standalone AdamW step
+  float* g_out;        // standalone reduce: fp32 reduced gradient
+  const float* g_in;   // standalone AdamW: fp32 gradient
+  float* partials;     // per-piece sums of squares (null: not requested)
+};
+
+struct FedArgs {
+  int64_t n;
+  const uint16_t* reps[kMaxGroups];
+  float w[kMaxGroups];
+  int G;
+  float* master;
+  uint16_t* working;
+};
+
+hipError_t launch_local_step(const StepArgs& a, int grid, hipStream_t st);
+hipError_t launch_reduce(const StepArgs& a, int grid, hipStream_t st);
+hipError_t launch_adamw(const StepArgs& a, int grid, hipStream_t st);
+hipError_t launch_fedavg(const FedArgs& a, int grid, hipStream_t st);
+hipError_t launch_seg_finalize(const LayoutDev& L, const float* partials, float* out,
+                               hipStream_t st);
+
+}  // namespace flr

@@ -1,0 +1,516 @@
+// flround_api.cpp -- the C ABI of libflround (declared in include/flround.h).
+//
+// This layer validates every argument before anything is enqueued, turns the
+// paper-level description of a round (group size, number of groups, local
+// steps between aggregations, per-group weights) into per-step scalars on the
+// host in double, and enqueues the gfx950 kernels on the caller's stream.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdint>
+#include <cstdlib>
+#include <cstring>
+#include <new>
+#include <vector>
+
+#include "flr_internal.h"
+#include "flround.h"
+
+using flr::kTile;
+
+struct fl_layout {
+  int device;
+  int num_cus;
+  uint64_t fingerprint;
+  void* dev_mem;  // one allocation holding all device tables
+  flr::LayoutDev L;
+};
+
+namespace {
+
+int g_blocks_per_cu = 0;  // 0: default
+constexpr int kDefaultBlocksPerCu = 8;
+
+constexpr uint64_t kFnvOffset = 0xCBF29CE484222325ULL;
+constexpr uint64_t kFnvPrime = 0x100000001B3ULL;
+
+uint64_t fnv_bytes(uint64_t h, const void* p, size_t n) {
+  const unsigned char* b = static_cast<const unsigned char*>(p);
+  for (size_t i = 0; i < n; ++i) {
+    h ^= b[i];
+    h *= kFnvPrime;
+  }
+  return h;
+}
+
+bool layout_args_ok(int64_t n, int64_t n_seg, const int64_t* off) {
+  if (n < 0 || n_seg < 0 || !off) return false;
+  if (n > 0 && n_seg < 1) return false;
+  if (n == 0 && n_seg != 0) return false;
+  if (n_seg > (int64_t)INT32_MAX - 1) return false;
+  if (off[0] != 0 || off[n_seg] != n) return false;
+  for (int64_t s = 0; s < n_seg; ++s)
+    if (off[s + 1] <= off[s]) return false;
+  return true;
+}
+
+uint64_t fingerprint_of(int64_t n, int64_t n_seg, const int64_t* off, const uint8_t* decay) {
+  uint64_t h = kFnvOffset;
+  h = fnv_bytes(h, &n, sizeof n);
+  h = fnv_bytes(h, &n_seg, sizeof n_seg);
+  h = fnv_bytes(h, off, sizeof(int64_t) * (size_t)(n_seg + 1));
+  for (int64_t s = 0; s < n_seg; ++s) {
+    const unsigned char f = (decay == nullptr || decay[s] != 0) ? 1 : 0;
+    h = fnv_bytes(h, &f, 1);
+  }
+  return h;
+}
+
+bool finite(float x) { return std::isfinite(x); }
+
+bool hparams_ok(const fl_adamw_hparams* h) {
+  if (!h) return false;
+  if (!finite(h->lr) || !finite(h->beta1) || !finite(h->beta2) || !finite(h->eps) ||
+      !finite(h->weight_decay))
+    return false;
+  if (!(h->lr >= 0.f)) return false;
+  if (!(h->beta1 >= 0.f && h->beta1 < 1.f)) return false;
+  if (!(h->beta2 >= 0.f && h->beta2 < 1.f)) return false;
+  if (!(h->eps > 0.f)) return false;
+  if (!(h->weight_decay >= 0.f)) return false;
+  return true;
+}
+
+// Per-step scalars: double on the host, each rounded once to float.
+flr::AdamScalars adam_scalars(const fl_adamw_hparams& h, int64_t step) {
+  const double lr = (double)h.lr;
+  const double t = (double)step;
+  flr::AdamScalars s;
+  s.b1 = h.beta1;
+  s.b2 = h.beta2;
+  s.omb1 = (float)(1.0 - (double)h.beta1);
+  s.omb2 = (float)(1.0 - (double)h.beta2);
+  s.step_size = (float)(lr / (1.0 - std::pow((double)h.beta1, t)));
+  s.bc2_sqrt = (float)std::sqrt(1.0 - std::pow((double)h.beta2, t));
+  s.eps = h.eps;
+  s.decay = (float)(1.0 - lr * (double)h.weight_decay);
+  return s;
+}
+
+// FedAvg weights w / sum(w): sum in double in index order.
+int normalise_weights(int G, const float* w, float* out) {
+  if (!w) return FL_ERR_INVALID;
+  double sum = 0.0;
+  for (int g = 0; g < G; ++g) {
+    if (!finite(w[g]) || !(w[g] >= 0.f)) return FL_ERR_INVALID;
+    sum += (double)w[g];
+  }
+  if (!(sum > 0.0) || !std::isfinite(sum)) return FL_ERR_INVALID;
+  for (int g = 0; g < G; ++g) out[g] = (float)((double)w[g] / sum);
+  return FL_OK;
+}
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+// A device pointer argument: must be non-null and 16-byte aligned when n > 0.
+int dev_ptr(const void* p, int64_t n) {
+  if (n == 0) return FL_OK;
+  if (!p) return FL_ERR_INVALID;
+  return aligned16(p) ? FL_OK : FL_ERR_ALIGN;
+}
+
+int check_device(const fl_layout* lay) {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess) return FL_ERR_HIP;
+  return dev == lay->device ? FL_OK : FL_ERR_DEVICE;
+}
+
+int grid_for(const fl_layout* lay, int64_t units) {
+  const int bpc = g_blocks_per_cu > 0 ? g_blocks_per_cu : kDefaultBlocksPerCu;
+  int64_t cap = (int64_t)bpc * (int64_t)lay->num_cus;
+  if (cap < 1) cap = 1;
+  int64_t g = units < cap ? units : cap;
+  return (int)(g < 1 ? 1 : g);
+}
+
+int fedavg_grid(const fl_layout* lay) {
+  const int64_t nvec = (lay->L.n + flr::kVec - 1) / flr::kVec;
+  return grid_for(lay, (nvec + flr::kBlock - 1) / flr::kBlock);
+}
+
+int status_of(hipError_t e) {
+  if (e == hipSuccess) return FL_OK;
+  if (e == hipErrorOutOfMemory) return FL_ERR_NOMEM;
+  return FL_ERR_HIP;
+}
+
+int check_peers(int R, const uint16_t* const* peers, int64_t n) {
+  if (R < 1 || R > FL_MAX_PEERS || !peers) return FL_ERR_INVALID;
+  for (int r = 0; r < R; ++r) {
+    const int rc = dev_ptr(peers[r], n);
+    if (rc != FL_OK) return rc;
+  }
+  return FL_OK;
+}
+
+// Stream-ordered temporary for the per-piece partial sums.
+struct Workspace {
+  float* p = nullptr;
+  hipStream_t st = nullptr;
+  int alloc(int64_t n_pieces, hipStream_t stream) {
+    st = stream;
+    void* q = nullptr;
+    const hipError_t e = hipMallocAsync(&q, (size_t)(n_pieces > 0 ? n_pieces : 1) * sizeof(float), st);
+    if (e != hipSuccess) return status_of(e);
+    p = static_cast<float*>(q);
+    return FL_OK;
+  }
+  int release() {
+    if (!p) return FL_OK;
+    const hipError_t e = hipFreeAsync(p, st);
+    p = nullptr;
+    return status_of(e);
+  }
+};
+
+flr::StepArgs step_args(const fl_layout* lay) {
+  flr::StepArgs a;
+  std::memset(&a, 0, sizeof a);
+  a.L = lay->L;
+  return a;
+}
+
+// Enqueue one fused local step (and, with seg_sumsq, its per-segment sums).
+int enqueue_local_step(const fl_layout* lay, const fl_adamw_hparams& h, int64_t step, int R,
+                       const uint16_t* const* peers, float grad_scale, float* master, float* m,
+                       float* v, uint16_t* working, float* partials, float* seg_sumsq,
+                       hipStream_t st) {
+  flr::StepArgs a = step_args(lay);
+  for (int r = 0; r < R; ++r) a.grads[r] = peers[r];
+  a.R = R;
+  a.grad_scale = grad_scale;
+  a.s = adam_scalars(h, step);
+  a.master = master;
+  a.m = m;
+  a.v = v;
+  a.working = working;
+  a.partials = seg_sumsq ? partials : nullptr;
+  int rc = status_of(flr::launch_local_step(a, grid_for(lay, lay->L.n_tiles), st));
+  if (rc == FL_OK && seg_sumsq) rc = status_of(flr::launch_seg_finalize(lay->L, partials, seg_sumsq, st));
+  return rc;
+}
+
+int enqueue_fedavg(const fl_layout* lay, int G, const uint16_t* const* reps, const float* wn,
+                   float* master, uint16_t* working, hipStream_t st) {
+  flr::FedArgs f;
+  std::memset(&f, 0, sizeof f);
+  f.n = lay->L.n;
+  f.G = G;
+  for (int g = 0; g < G; ++g) {
+    f.reps[g] = reps[g];
+    f.w[g] = wn[g];
+  }
+  f.master = master;
+  f.working = working;
+  return status_of(flr::launch_fedavg(f, fedavg_grid(lay), st));
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* fl_status_string(int status) {
+  switch (status) {
+    case FL_OK: return "FL_OK";
+    case FL_ERR_INVALID: return "FL_ERR_INVALID: invalid argument";
+    case FL_ERR_ALIGN: return "FL_ERR_ALIGN: device pointer not 16-byte aligned";
+    case FL_ERR_LAYOUT: return "FL_ERR_LAYOUT: replica layout fingerprint mismatch";
+    case FL_ERR_DEVICE: return "FL_ERR_DEVICE: current device is not the layout's device";
+    case FL_ERR_HIP: return "FL_ERR_HIP: HIP runtime or launch failure";
+    case FL_ERR_NOMEM: return "FL_ERR_NOMEM: allocation failed";
+    default: return "unknown fl_status";
+  }
+}
+
+int fl_version(void) { return (1 << 16) | 0; }
+
+int fl_set_blocks_per_cu(int blocks_per_cu) {
+  const int prev = g_blocks_per_cu;
+  g_blocks_per_cu = blocks_per_cu > 0 ? blocks_per_cu : 0;
+  return prev;
+}
+
+uint64_t fl_fingerprint(int64_t n, int64_t n_seg, const int64_t* seg_offsets,
+                        const uint8_t* seg_decay) {
+  if (!layout_args_ok(n, n_seg, seg_offsets)) return 0;
+  return fingerprint_of(n, n_seg, seg_offsets, seg_decay);
+}
+
+int fl_layout_create(int64_t n, int64_t n_seg, const int64_t* seg_offsets,
+                     const uint8_t* seg_decay, fl_layout** out) {
+  if (!out) return FL_ERR_INVALID;
+  *out = nullptr;
+  if (!layout_args_ok(n, n_seg, seg_offsets)) return FL_ERR_INVALID;
+  const int64_t n_tiles = (n + kTile - 1) / kTile;
+  if (n_tiles > (int64_t)INT32_MAX / 2) return FL_ERR_INVALID;
+
+  // Per-tile segment tables.
+  std::vector<flr::TileInfo> tiles((size_t)n_tiles);
+  std::vector<int64_t> seg_piece0((size_t)n_seg + 1, 0);
+  int64_t s = 0;
+  int64_t pieces = 0;
+  for (int64_t t = 0; t < n_tiles; ++t) {
+    const int64_t lo = t * kTile;
+    const int64_t hi = (lo + kTile < n ? lo + kTile : n) - 1;
+    while (seg_offsets[s + 1] <= lo) ++s;
+    int64_t s1 = s;
+    while (seg_offsets[s1 + 1] <= hi) ++s1;
+    flr::TileInfo ti;
+    ti.seg0 = (int32_t)s;
+    ti.nseg = (int32_t)(s1 - s + 1);
+    if (pieces > (int64_t)INT32_MAX - ti.nseg) return FL_ERR_INVALID;
+    ti.piece0 = (int32_t)pieces;
+    ti.decay = (ti.nseg == 1 && (seg_decay == nullptr || seg_decay[s] != 0)) ? 1 : 0;
+    tiles[(size_t)t] = ti;
+    for (int64_t k = s; k <= s1; ++k)
+      if (seg_offsets[k] >= lo) seg_piece0[(size_t)k] = pieces + (k - s);
+    pieces += ti.nseg;
+  }
+  seg_piece0[(size_t)n_seg] = pieces;
+  std::vector<uint8_t> decay((size_t)n_seg);
+  for (int64_t k = 0; k < n_seg; ++k) decay[(size_t)k] = (seg_decay == nullptr || seg_decay[k]) ? 1 : 0;
+
+  fl_layout* lay = new (std::nothrow) fl_layout;
+  if (!lay) return FL_ERR_NOMEM;
+  std::memset(lay, 0, sizeof *lay);
+  if (hipGetDevice(&lay->device) != hipSuccess) {
+    delete lay;
+    return FL_ERR_HIP;
+  }
+  int cus = 0;
+  if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, lay->device) !=
+          hipSuccess || cus < 1) {
+    delete lay;
+    return FL_ERR_HIP;
+  }
+  lay->num_cus = cus;
+  lay->fingerprint = fingerprint_of(n, n_seg, seg_offsets, seg_decay);
+  lay->L.n = n;
+  lay->L.n_seg = n_seg;
+  lay->L.n_tiles = n_tiles;
+  lay->L.n_pieces = pieces;
+
+  // One device allocation: [seg_off | seg_piece0 | tiles | seg_decay].
+  const size_t b_off = sizeof(int64_t) * (size_t)(n_seg + 1);
+  const size_t b_pp = sizeof(int64_t) * (size_t)(n_seg + 1);
+  const size_t b_tiles = sizeof(flr::TileInfo) * (size_t)n_tiles;
+  const size_t b_dec = (size_t)n_seg;
+  const size_t total = b_off + b_pp + b_tiles + b_dec + 64;
+  void* mem = nullptr;
+  hipError_t e = hipMalloc(&mem, total);
+  if (e != hipSuccess) {
+    delete lay;
+    return status_of(e);
+  }
+  char* base = static_cast<char*>(mem);
+  e = hipMemcpy(base, seg_offsets, b_off, hipMemcpyHostToDevice);
+  if (e == hipSuccess) e = hipMemcpy(base + b_off, seg_piece0.data(), b_pp, hipMemcpyHostToDevice);
+  if (e == hipSuccess && b_tiles)
+    e = hipMemcpy(base + b_off + b_pp, tiles.data(), b_tiles, hipMemcpyHostToDevice);
+  if (e == hipSuccess && b_dec)
+    e = hipMemcpy(base + b_off + b_pp + b_tiles, decay.data(), b_dec, hipMemcpyHostToDevice);
+  if (e != hipSuccess) {
+    (void)hipFree(mem);
+    delete lay;
+    return status_of(e);
+  }
+  lay->dev_mem = mem;
+  lay->L.seg_off = reinterpret_cast<const int64_t*>(base);
+  lay->L.seg_piece0 = reinterpret_cast<const int64_t*>(base + b_off);
+  lay->L.tiles = reinterpret_cast<const flr::TileInfo*>(base + b_off + b_pp);
+  lay->L.seg_decay = reinterpret_cast<const uint8_t*>(base + b_off + b_pp + b_tiles);
+  *out = lay;
+  return FL_OK;
+}
+
+int fl_layout_destroy(fl_layout* layout) {
+  if (!layout) return FL_OK;
+  int rc = FL_OK;
+  if (layout->dev_mem) {
+    int cur = -1;
+    (void)hipGetDevice(&cur);
+    if (cur != layout->device) (void)hipSetDevice(layout->device);
+    if (hipFree(layout->dev_mem) != hipSuccess) rc = FL_ERR_HIP;
+    if (cur >= 0 && cur != layout->device) (void)hipSetDevice(cur);
+  }
+  delete layout;
+  return rc;
+}
+
+int64_t fl_layout_numel(const fl_layout* layout) { return layout ? layout->L.n : -1; }
+
+int64_t fl_layout_num_segments(const fl_layout* layout) { return layout ? layout->L.n_seg : -1; }
+
+uint64_t fl_layout_fingerprint(const fl_layout* layout) {
+  return layout ? layout->fingerprint : 0;
+}
+
+int fl_shard_reduce(const fl_layout* layout, int R, const uint16_t* const* peer_grads,
+                    float grad_scale, float* grad_out, float* seg_sumsq, void* stream) {
+  if (!layout) return FL_ERR_INVALID;
+  const int64_t n = layout->L.n;
+  int rc = check_peers(R, peer_grads, n);
+  if (rc != FL_OK) return rc;
+  if (!finite(grad_scale)) return FL_ERR_INVALID;
+  if ((rc = dev_ptr(grad_out, n)) != FL_OK) return rc;
+  if (seg_sumsq && (reinterpret_cast<uintptr_t>(seg_sumsq) & 3u)) return FL_ERR_ALIGN;
+  if ((rc = check_device(layout)) != FL_OK) return rc;
+  if (n == 0) return FL_OK;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  Workspace ws;
+  if (seg_sumsq && (rc = ws.alloc(layout->L.n_pieces, st)) != FL_OK) return rc;
+  flr::StepArgs a = step_args(layout);
+  for (int r = 0; r < R; ++r) a.grads[r] = peer_grads[r];
+  a.R = R;
+  a.grad_scale = grad_scale;
+  a.g_out = grad_out;
+  a.partials = ws.p;
+  rc = status_of(flr::launch_reduce(a, grid_for(layout, layout->L.n_tiles), st));
+  if (rc == FL_OK && seg_sumsq) rc = status_of(flr::launch_seg_finalize(layout->L, ws.p, seg_sumsq, st));
+  const int rc2 = ws.release();
+  return rc != FL_OK ? rc : rc2;
+}
+
+int fl_adamw_step(const fl_layout* layout, const fl_adamw_hparams* h, int64_t step,
+                  const float* grad, float* master, float* m, float* v, uint16_t* working,
+                  void* stream) {
+  if (!layout || !hparams_ok(h) || step < 1) return FL_ERR_INVALID;
+  const int64_t n = layout->L.n;
+  int rc;
+  if ((rc = dev_ptr(grad, n)) != FL_OK) return rc;
+  if ((rc = dev_ptr(master, n)) != FL_OK) return rc;
+  if ((rc = dev_ptr(m, n)) != FL_OK) return rc;
+  if ((rc = dev_ptr(v, n)) != FL_OK) return rc;
+  if (working && (rc = dev_ptr(working, n)) != FL_OK) return rc;
+  if (n > 0 && (master == m || master == v || m == v)) return FL_ERR_INVALID;
+  if ((rc = check_device(layout)) != FL_OK) return rc;
+  if (n == 0) return FL_OK;
+  flr::StepArgs a = step_args(layout);
+  a.s = adam_scalars(*h, step);
+  a.g_in = grad;
+  a.master = master;
+  a.m = m;
+  a.v = v;
+  a.working = working;
+  return status_of(flr::launch_adamw(a, grid_for(layout, layout->L.n_tiles),
+                                     static_cast<hipStream_t>(stream)));
+}
+
+int fl_local_step(const fl_layout* layout, const fl_adamw_hparams* h, int64_t step, int R,
+                  const uint16_t* const* peer_grads, float grad_scale, float* master, float* m,
+                  float* v, uint16_t* working, float* seg_sumsq, void* stream) {
+  if (!layout || !hparams_ok(h) || step < 1 || !finite(grad_scale)) return FL_ERR_INVALID;
+  const int64_t n = layout->L.n;
+  int rc = check_peers(R, peer_grads, n);
+  if (rc != FL_OK) return rc;
+  if ((rc = dev_ptr(master, n)) != FL_OK) return rc;
+  if ((rc = dev_ptr(m, n)) != FL_OK) return rc;
+  if ((rc = dev_ptr(v, n)) != FL_OK) return rc;
+  if ((rc = dev_ptr(working, n)) != FL_OK) return rc;
+  if (n > 0 && (master == m || master == v || m == v)) return FL_ERR_INVALID;
+  if (seg_sumsq && (reinterpret_cast<uintptr_t>(seg_sumsq) & 3u)) return FL_ERR_ALIGN;
+  if ((rc = check_device(layout)) != FL_OK) return rc;
+  if (n == 0) return FL_OK;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  Workspace ws;
+  if (seg_sumsq && (rc = ws.alloc(layout->L.n_pieces, st)) != FL_OK) return rc;
+  rc = enqueue_local_step(layout, *h, step, R, peer_grads, grad_scale, master, m, v, working,
+                          ws.p, seg_sumsq, st);
+  const int rc2 = ws.release();
+  return rc != FL_OK ? rc : rc2;
+}
+
+int fl_fedavg(const fl_layout* layout, int G, const uint16_t* const* replicas,
+              const float* weights, const uint64_t* replica_fp, float* master_out,
+              uint16_t* working_out, void* stream) {
+  if (!layout || G < 1 || G > FL_MAX_GROUPS || !replicas) return FL_ERR_INVALID;
+  const int64_t n = layout->L.n;
+  float wn[FL_MAX_GROUPS];
+  int rc = normalise_weights(G, weights, wn);
+  if (rc != FL_OK) return rc;
+  for (int g = 0; g < G; ++g)
+    if ((rc = dev_ptr(replicas[g], n)) != FL_OK) return rc;
+  if ((rc = dev_ptr(master_out, n)) != FL_OK) return rc;
+  if ((rc = dev_ptr(working_out, n)) != FL_OK) return rc;
+  if (replica_fp)
+    for (int g = 0; g < G; ++g)
+      if (replica_fp[g] != layout->fingerprint) return FL_ERR_LAYOUT;
+  if ((rc = check_device(layout)) != FL_OK) return rc;
+  if (n == 0) return FL_OK;
+  return enqueue_fedavg(layout, G, replicas, wn, master_out, working_out,
+                        static_cast<hipStream_t>(stream));
+}
+
+int fl_round(const fl_layout* layout, const fl_round_cfg* cfg, const uint16_t* const* grads,
+             const uint16_t* const* replicas, float* master, float* m, float* v,
+             uint16_t* working, float* seg_sumsq, void* stream) {
+  if (!layout || !cfg || !grads || !replicas) return FL_ERR_INVALID;
+  const fl_round_cfg& c = *cfg;
+  const int64_t n = layout->L.n;
+  if (c.R < 1 || c.R > FL_MAX_PEERS || c.G < 1 || c.G > FL_MAX_GROUPS || c.A < 1 ||
+      c.self_group < 0 || c.self_group >= c.G || c.step0 < 1 || !finite(c.grad_scale) ||
+      !hparams_ok(&c.h))
+    return FL_ERR_INVALID;
+  if (c.step0 > INT64_MAX - c.A) return FL_ERR_INVALID;
+  if ((int64_t)c.A * c.R > (int64_t)INT32_MAX) return FL_ERR_INVALID;
+  float wn[FL_MAX_GROUPS];
+  int rc = normalise_weights(c.G, c.weights, wn);
+  if (rc != FL_OK) return rc;
+  for (int64_t k = 0; k < (int64_t)c.A * c.R; ++k)
+    if ((rc = dev_ptr(grads[k], n)) != FL_OK) return rc;
+  const uint16_t* reps[FL_MAX_GROUPS];
+  for (int g = 0; g < c.G; ++g) {
+    if (g == c.self_group) {
+      reps[g] = working;
+      continue;
+    }
+    if ((rc = dev_ptr(replicas[g], n)) != FL_OK) return rc;
+    reps[g] = replicas[g];
+  }
+  if ((rc = dev_ptr(master, n)) != FL_OK) return rc;
+  if ((rc = dev_ptr(m, n)) != FL_OK) return rc;
+  if ((rc = dev_ptr(v, n)) != FL_OK) return rc;
+  if ((rc = dev_ptr(working, n)) != FL_OK) return rc;
+  if (n > 0 && (master == m || master == v || m == v)) return FL_ERR_INVALID;
+  if (seg_sumsq && (reinterpret_cast<uintptr_t>(seg_sumsq) & 3u)) return FL_ERR_ALIGN;
+  if (c.replica_fp)
+    for (int g = 0; g < c.G; ++g)
+      if (g != c.self_group && c.replica_fp[g] != layout->fingerprint) return FL_ERR_LAYOUT;
+  if (c.phase_events)
+    for (int k = 0; k < c.A + 2; ++k)
+      if (!c.phase_events[k]) return FL_ERR_INVALID;
+  if ((rc = check_device(layout)) != FL_OK) return rc;
+
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  auto record = [&](int k) -> int {
+    if (!c.phase_events) return FL_OK;
+    return status_of(hipEventRecord(static_cast<hipEvent_t>(c.phase_events[k]), st));
+  };
+  Workspace ws;
+  if (n > 0 && seg_sumsq && (rc = ws.alloc(layout->L.n_pieces, st)) != FL_OK) return rc;
+  for (int a = 0; a < c.A && rc == FL_OK; ++a) {
+    rc = record(a);
+    if (rc == FL_OK && n > 0)
+      rc = enqueue_local_step(layout, c.h, c.step0 + a, c.R, grads + (size_t)a * (size_t)c.R,
+                              c.grad_scale, master, m, v, working, ws.p,
+                              seg_sumsq ? seg_sumsq + (size_t)a * (size_t)layout->L.n_seg : nullptr,
+                              st);
+  }
+  if (rc == FL_OK) rc = record(c.A);
+  if (rc == FL_OK && n > 0) rc = enqueue_fedavg(layout, c.G, reps, wn, master, working, st);
+  if (rc == FL_OK) rc = record(c.A + 1);
+  const int rc2 = ws.release();
+  return rc != FL_OK ? rc : rc2;
+}
+
+}  // extern "C"

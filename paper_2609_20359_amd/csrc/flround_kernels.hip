@@ -1,0 +1,399 @@
+// flround_kernels.hip -- gfx950 kernels of the parameter-sync path.
+//
+// Every kernel here is a bandwidth-bound stream over the flat shard: an
+// element is read once, updated with a few dozen fp32 operations and written
+// once, so the kernels are built for HBM, not for the matrix cores:
+//   * a workgroup of 256 threads (4 wave64) owns one 2048-element tile per
+//     iteration of a grid-stride loop; each thread owns 8 consecutive
+//     elements, i.e. one 16-byte load per bf16 stream and two per fp32 stream
+//     (global_load_dwordx4), so every wave touches whole 128-byte lines;
+//   * all loads of a tile are issued before its arithmetic (memory-level
+//     parallelism), with compile-time peer / group counts where common;
+//   * sums over peers and replicas run in ascending index order in fp32, one
+//     correctly rounded operation at a time (the file is built with
+//     -ffp-contract=off), so results are bitwise those of the definition and
+//     do not depend on the grid;
+//   * per-segment sums of squares use wave64 butterfly reductions and a
+//     4-entry LDS exchange per workgroup; only tiles that straddle a segment
+//     boundary (rare) resolve segments per element.
+#include "flr_internal.h"
+
+namespace flr {
+namespace {
+
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+// Streaming access: data read or written exactly once per pass.
+#ifndef FLR_NT_LOADS
+#define FLR_NT_LOADS 1
+#endif
+#ifndef FLR_NT_STORES
+#define FLR_NT_STORES 1
+#endif
+
+template <typename T>
+__device__ __forceinline__ T ld(const T* p) {
+#if FLR_NT_LOADS
+  return __builtin_nontemporal_load(p);
+#else
+  return *p;
+#endif
+}
+
+template <typename T>
+__device__ __forceinline__ void st(T* p, T v) {
+#if FLR_NT_STORES
+  __builtin_nontemporal_store(v, p);
+#else
+  *p = v;
+#endif
+}
+
+__device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
+__device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xFFFF0000u); }
+
+// fp32 -> bf16 bits, round to nearest even; NaN -> quiet NaN, sign kept.
+__device__ __forceinline__ uint32_t to_bf16(float x) {
+  const uint32_t u = __float_as_uint(x);
+  const uint32_t r = (u + 0x7FFFu + ((u >> 16) & 1u)) >> 16;
+  return ((u & 0x7FFFFFFFu) > 0x7F800000u) ? ((u >> 16) | 0x40u) : r;
+}
+
+__device__ __forceinline__ u32x4 pack_bf16x8(const float x[8]) {
+  u32x4 o;
+  o.x = to_bf16(x[0]) | (to_bf16(x[1]) << 16);
+  o.y = to_bf16(x[2]) | (to_bf16(x[3]) << 16);
+  o.z = to_bf16(x[4]) | (to_bf16(x[5]) << 16);
+  o.w = to_bf16(x[6]) | (to_bf16(x[7]) << 16);
+  return o;
+}
+
+// acc[e] = acc[e] + bf16 element e of w (ascending e).
+__device__ __forceinline__ void add_bf16x8(float acc[8], u32x4 w) {
+  acc[0] = acc[0] + bf16_lo(w.x);
+  acc[1] = acc[1] + bf16_hi(w.x);
+  acc[2] = acc[2] + bf16_lo(w.y);
+  acc[3] = acc[3] + bf16_hi(w.y);
+  acc[4] = acc[4] + bf16_lo(w.z);
+  acc[5] = acc[5] + bf16_hi(w.z);
+  acc[6] = acc[6] + bf16_lo(w.w);
+  acc[7] = acc[7] + bf16_hi(w.w);
+}
+
+// acc[e] = acc[e] + wt * bf16 element e of w.
+__device__ __forceinline__ void fma_free_bf16x8(float acc[8], float wt, u32x4 w) {
+  acc[0] = acc[0] + (wt * bf16_lo(w.x));
+  acc[1] = acc[1] + (wt * bf16_hi(w.x));
+  acc[2] = acc[2] + (wt * bf16_lo(w.y));
+  acc[3] = acc[3] + (wt * bf16_hi(w.y));
+  acc[4] = acc[4] + (wt * bf16_lo(w.z));
+  acc[5] = acc[5] + (wt * bf16_hi(w.z));
+  acc[6] = acc[6] + (wt * bf16_lo(w.w));
+  acc[7] = acc[7] + (wt * bf16_hi(w.w));
+}
+
+__device__ __forceinline__ void load_f32x8(const float* p, float x[8]) {
+  const f32x4 a = ld(reinterpret_cast<const f32x4*>(p));
+  const f32x4 b = ld(reinterpret_cast<const f32x4*>(p + 4));
+  x[0] = a.x; x[1] = a.y; x[2] = a.z; x[3] = a.w;
+  x[4] = b.x; x[5] = b.y; x[6] = b.z; x[7] = b.w;
+}
+
+__device__ __forceinline__ void store_f32x8(float* p, const float x[8]) {
+  st(reinterpret_cast<f32x4*>(p), f32x4{x[0], x[1], x[2], x[3]});
+  st(reinterpret_cast<f32x4*>(p + 4), f32x4{x[4], x[5], x[6], x[7]});
+}
+
+// Reduced gradient of 8 elements (full vector): peers in ascending order.
+template <int RT>
+__device__ __forceinline__ void reduce_vec(const StepArgs& a, int64_t base, float g[8]) {
+  float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+  if constexpr (RT > 0) {
+    u32x4 w[RT];
+#pragma unroll
+    for (int r = 0; r < RT; ++r) w[r] = ld(reinterpret_cast<const u32x4*>(a.grads[r] + base));
+#pragma unroll
+    for (int r = 0; r < RT; ++r) add_bf16x8(acc, w[r]);
+  } else {
+    constexpr int kChunk = 4;
+    for (int r0 = 0; r0 < a.R; r0 += kChunk) {
+      u32x4 w[kChunk];
+#pragma unroll
+      for (int k = 0; k < kChunk; ++k)
+        if (r0 + k < a.R) w[k] = ld(reinterpret_cast<const u32x4*>(a.grads[r0 + k] + base));
+#pragma unroll
+      for (int k = 0; k < kChunk; ++k)
+        if (r0 + k < a.R) add_bf16x8(acc, w[k]);
+    }
+  }
+#pragma unroll
+  for (int e = 0; e < 8; ++e) g[e] = acc[e] * a.grad_scale;
+}
+
+// Same for the last, partial vector: elements base .. base + cnt - 1.
+__device__ __forceinline__ void reduce_tail(const StepArgs& a, int64_t base, int cnt,
+                                            float g[8]) {
+  for (int e = 0; e < 8; ++e) {
+    float acc = 0.f;
+    if (e < cnt) {
+      for (int r = 0; r < a.R; ++r)
+        acc = acc + __uint_as_float((uint32_t)a.grads[r][base + e] << 16);
+    }
+    g[e] = acc * a.grad_scale;
+  }
+}
+
+// Fixed-tree sum over the workgroup: wave64 butterfly (every lane ends with
+// the same bits), then the four wave totals in order.
+__device__ __forceinline__ float block_sum(float v, float* red) {
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) v = v + __shfl_xor(v, off, 64);
+  const int lane = threadIdx.x & 63;
+  const int wid = threadIdx.x >> 6;
+  if (lane == 0) red[wid] = v;
+  __syncthreads();
+  const float r = ((red[0] + red[1]) + red[2]) + red[3];
+  __syncthreads();
+  return r;
+}
+
+// Segment of element `i`, searching [lo, hi] (segments overlapping the tile).
+__device__ __forceinline__ int find_seg(const int64_t* off, int lo, int hi, int64_t i) {
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) >> 1;
+    if (off[mid] <= i) lo = mid; else hi = mid - 1;
+  }
+  return lo;
+}
+
+// MODE 0: fused reduce + AdamW + working copy; 1: reduce only (g_out);
+// 2: AdamW only (g_in).  SUMSQ: per-piece sums of squares of g.
+template <int RT, int MODE, bool SUMSQ>
+__global__ void __launch_bounds__(kBlock) k_step(const StepArgs a) {
+  __shared__ float red[4];
+  const int tid = threadIdx.x;
+  for (int64_t t = blockIdx.x; t < a.L.n_tiles; t += gridDim.x) {
+    const TileInfo ti = a.L.tiles[t];
+    const int64_t base = t * kTile + (int64_t)tid * kVec;
+    const int64_t left = a.L.n - base;
+    const int cnt = left >= kVec ? kVec : (left > 0 ? (int)left : 0);
+
+    // segment of each element (only needed where the tile straddles segments)
+    int seg[8];
+    if (ti.nseg > 1 && (SUMSQ || MODE != 1)) {
+      int s = cnt > 0 ? find_seg(a.L.seg_off, ti.seg0, ti.seg0 + ti.nseg - 1, base) : ti.seg0;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        if (e < cnt)
+          while (base + e >= a.L.seg_off[s + 1]) ++s;
+        seg[e] = s;
+      }
+    }
+
+    float g[8];
+    float p[8], m[8], v[8];
+    if (cnt == kVec) {
+      if constexpr (MODE != 1) {
+        load_f32x8(a.master + base, p);
+        load_f32x8(a.m + base, m);
+        load_f32x8(a.v + base, v);
+      }
+      if constexpr (MODE == 2) load_f32x8(a.g_in + base, g);
+      else reduce_vec<RT>(a, base, g);
+    } else {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        p[e] = 0.f; m[e] = 0.f; v[e] = 0.f; g[e] = 0.f;
+        if constexpr (MODE != 1) {
+          if (e < cnt) { p[e] = a.master[base + e]; m[e] = a.m[base + e]; v[e] = a.v[base + e]; }
+        }
+        if constexpr (MODE == 2) {
+          if (e < cnt) g[e] = a.g_in[base + e];
+        }
+      }
+      if constexpr (MODE != 2) {
+        if (cnt > 0) reduce_tail(a, base, cnt, g);
+      }
+    }
+
+    if constexpr (MODE == 1) {
+      if (cnt == kVec) {
+        store_f32x8(a.g_out + base, g);
+      } else {
+        for (int e = 0; e < cnt; ++e) a.g_out[base + e] = g[e];
+      }
+    } else {
+      const AdamScalars& s = a.s;
+      float d[8];
+      if (ti.nseg == 1) {
+        const float du = ti.decay ? s.decay : 1.0f;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) d[e] = du;
+      } else {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) d[e] = a.L.seg_decay[seg[e]] ? s.decay : 1.0f;
+      }
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        float pe = p[e] * d[e];
+        const float mn = (s.b1 * m[e]) + (s.omb1 * g[e]);
+        const float vn = (s.b2 * v[e]) + (s.omb2 * (g[e] * g[e]));
+        const float den = (__builtin_sqrtf(vn) / s.bc2_sqrt) + s.eps;
+        pe = pe - (s.step_size * (mn / den));
+        p[e] = pe; m[e] = mn; v[e] = vn;
+      }
+      if (cnt == kVec) {
+        store_f32x8(a.master + base, p);
+        store_f32x8(a.m + base, m);
+        store_f32x8(a.v + base, v);
+        if (MODE == 0 || a.working) st(reinterpret_cast<u32x4*>(a.working + base), pack_bf16x8(p));
+      } else {
+        for (int e = 0; e < cnt; ++e) {
+          a.master[base + e] = p[e];
+          a.m[base + e] = m[e];
+          a.v[base + e] = v[e];
+          if (MODE == 0 || a.working) a.working[base + e] = (uint16_t)to_bf16(p[e]);
+        }
+      }
+    }
+
+    if constexpr (SUMSQ) {
+      if (ti.nseg == 1) {
+        float acc = 0.f;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) if (e < cnt) acc = acc + g[e] * g[e];
+        const float tot = block_sum(acc, red);
+        if (tid == 0) a.partials[ti.piece0] = tot;
+      } else {
+        for (int j = 0; j < ti.nseg; ++j) {
+          const int sj = ti.seg0 + j;
+          float acc = 0.f;
+#pragma unroll
+          for (int e = 0; e < 8; ++e) if (e < cnt && seg[e] == sj) acc = acc + g[e] * g[e];
+          const float tot = block_sum(acc, red);
+          if (tid == 0) a.partials[ti.piece0 + j] = tot;
+        }
+      }
+    }
+  }
+}
+
+// FedAvg: master = sum_g w_g * f32(rep_g), ascending g; working = bf16(master).
+template <int GT>
+__global__ void __launch_bounds__(kBlock) k_fedavg(const FedArgs a) {
+  const int64_t nvec = (a.n + kVec - 1) / kVec;
+  const int64_t stride = (int64_t)gridDim.x * kBlock;
+  for (int64_t vi = (int64_t)blockIdx.x * kBlock + threadIdx.x; vi < nvec; vi += stride) {
+    const int64_t base = vi * kVec;
+    const int64_t left = a.n - base;
+    float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+    if (left >= kVec) {
+      if constexpr (GT > 0) {
+        u32x4 w[GT];
+#pragma unroll
+        for (int k = 0; k < GT; ++k) w[k] = ld(reinterpret_cast<const u32x4*>(a.reps[k] + base));
+#pragma unroll
+        for (int k = 0; k < GT; ++k) fma_free_bf16x8(acc, a.w[k], w[k]);
+      } else {
+        constexpr int kChunk = 4;
+        for (int k0 = 0; k0 < a.G; k0 += kChunk) {
+          u32x4 w[kChunk];
+#pragma unroll
+          for (int k = 0; k < kChunk; ++k)
+            if (k0 + k < a.G) w[k] = ld(reinterpret_cast<const u32x4*>(a.reps[k0 + k] + base));
+#pragma unroll
+          for (int k = 0; k < kChunk; ++k)
+            if (k0 + k < a.G) fma_free_bf16x8(acc, a.w[k0 + k], w[k]);
+        }
+      }
+      store_f32x8(a.master + base, acc);
+      st(reinterpret_cast<u32x4*>(a.working + base), pack_bf16x8(acc));
+    } else {
+      const int cnt = (int)left;
+      for (int e = 0; e < cnt; ++e) {
+        float s = 0.f;
+        for (int k = 0; k < a.G; ++k)
+          s = s + (a.w[k] * __uint_as_float((uint32_t)a.reps[k][base + e] << 16));
+        acc[e] = s;
+      }
+      for (int e = 0; e < cnt; ++e) {
+        a.master[base + e] = acc[e];
+        a.working[base + e] = (uint16_t)to_bf16(acc[e]);
+      }
+    }
+  }
+}
+
+// Per-segment total of the piece partials, in double, fixed order: thread j
+// sums pieces j, j+256, ...; then a wave64 butterfly and the 4 wave totals.
+__global__ void __launch_bounds__(kBlock) k_seg_finalize(const LayoutDev L, const float* partials,
+                                                         float* out) {
+  __shared__ double red[4];
+  for (int64_t s = blockIdx.x; s < L.n_seg; s += gridDim.x) {
+    const int64_t p0 = L.seg_piece0[s];
+    const int64_t p1 = L.seg_piece0[s + 1];
+    double acc = 0.0;
+    for (int64_t p = p0 + threadIdx.x; p < p1; p += kBlock) acc = acc + (double)partials[p];
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) acc = acc + __shfl_xor(acc, off, 64);
+    if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = acc;
+    __syncthreads();
+    if (threadIdx.x == 0) out[s] = (float)(((red[0] + red[1]) + red[2]) + red[3]);
+    __syncthreads();
+  }
+}
+
+template <typename Args>
+hipError_t launch(const void* fn, const Args& a, int grid, hipStream_t st) {
+  void* args[] = {const_cast<Args*>(&a)};
+  return hipLaunchKernel(fn, dim3((unsigned)grid), dim3(kBlock), args, 0, st);
+}
+
+template <int MODE, bool SUMSQ>
+hipError_t dispatch_step(const StepArgs& a, int grid, hipStream_t st) {
+  switch (a.R) {
+    case 1: return launch((const void*)k_step<1, MODE, SUMSQ>, a, grid, st);
+    case 2: return launch((const void*)k_step<2, MODE, SUMSQ>, a, grid, st);
+    case 4: return launch((const void*)k_step<4, MODE, SUMSQ>, a, grid, st);
+    case 8: return launch((const void*)k_step<8, MODE, SUMSQ>, a, grid, st);
+    case 16: return launch((const void*)k_step<16, MODE, SUMSQ>, a, grid, st);
+    default: return launch((const void*)k_step<0, MODE, SUMSQ>, a, grid, st);
+  }
+}
+
+}  // namespace
+
+hipError_t launch_local_step(const StepArgs& a, int grid, hipStream_t st) {
+  return a.partials ? dispatch_step<0, true>(a, grid, st) : dispatch_step<0, false>(a, grid, st);
+}
+
+hipError_t launch_reduce(const StepArgs& a, int grid, hipStream_t st) {
+  return a.partials ? dispatch_step<1, true>(a, grid, st) : dispatch_step<1, false>(a, grid, st);
+}
+
+hipError_t launch_adamw(const StepArgs& a, int grid, hipStream_t st) {
+  return launch((const void*)k_step<1, 2, false>, a, grid, st);
+}
+
+hipError_t launch_fedavg(const FedArgs& a, int grid, hipStream_t st) {
+  switch (a.G) {
+    case 1: return launch((const void*)k_fedavg<1>, a, grid, st);
+    case 2: return launch((const void*)k_fedavg<2>, a, grid, st);
+    case 4: return launch((const void*)k_fedavg<4>, a, grid, st);
+    case 8: return launch((const void*)k_fedavg<8>, a, grid, st);
+    case 16: return launch((const void*)k_fedavg<16>, a, grid, st);
+    default: return launch((const void*)k_fedavg<0>, a, grid, st);
+  }
+}
+
+hipError_t launch_seg_finalize(const LayoutDev& L, const float* partials, float* out,
+                               hipStream_t st) {
+  if (L.n_seg == 0) return hipSuccess;
+  const int grid = (int)(L.n_seg < 65535 ? L.n_seg : 65535);
+  void* args[] = {const_cast<LayoutDev*>(&L), &partials, &out};
+  return hipLaunchKernel((const void*)k_seg_finalize, dim3((unsigned)grid), dim3(kBlock), args, 0,
+                         st);
+}
+
+}  // namespace flr

@@ -1,0 +1,289 @@
+"""ctypes binding of libflround (include/flround.h).
+
+Argument marshalling only: every step of the path runs in the library's
+gfx950 kernels.  Tensors are torch CUDA tensors (bf16 buffers may be
+torch.bfloat16 or any 2-byte dtype holding bf16 bits); work is enqueued on
+the current torch stream unless `stream` is given.  Every non-OK status
+raises FlError.  If the library is missing, importing the symbols raises:
+there is no fallback.
+"""
+import ctypes
+import os
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libflround.so")
+
+FL_OK = 0
+FL_ERR_INVALID = -1
+FL_ERR_ALIGN = -2
+FL_ERR_LAYOUT = -3
+FL_ERR_DEVICE = -4
+FL_ERR_HIP = -5
+FL_ERR_NOMEM = -6
+
+FL_MAX_PEERS = 64
+FL_MAX_GROUPS = 64
+
+# Every symbol include/flround.h declares.
+EXPORTS = ("fl_status_string", "fl_version", "fl_layout_create", "fl_layout_destroy",
+           "fl_layout_numel", "fl_layout_num_segments", "fl_fingerprint",
+           "fl_layout_fingerprint", "fl_shard_reduce", "fl_adamw_step", "fl_local_step",
+           "fl_fedavg", "fl_round", "fl_set_blocks_per_cu")
+
+_P = ctypes.c_void_p
+
+
+class FlError(RuntimeError):
+    def __init__(self, status, where):
+        self.status = status
+        super().__init__("%s: %s" % (where, status_string(status)))
+
+
+class AdamwHparams(ctypes.Structure):
+    _fields_ = [("lr", ctypes.c_float), ("beta1", ctypes.c_float), ("beta2", ctypes.c_float),
+                ("eps", ctypes.c_float), ("weight_decay", ctypes.c_float)]
+
+
+class RoundCfg(ctypes.Structure):
+    _fields_ = [("R", ctypes.c_int), ("G", ctypes.c_int), ("A", ctypes.c_int),
+                ("self_group", ctypes.c_int), ("grad_scale", ctypes.c_float),
+                ("h", AdamwHparams), ("step0", ctypes.c_int64),
+                ("weights", ctypes.POINTER(ctypes.c_float)),
+                ("replica_fp", ctypes.POINTER(ctypes.c_uint64)),
+                ("phase_events", ctypes.POINTER(ctypes.c_void_p))]
+
+
+_lib = None
+
+
+def lib():
+    """The loaded library (raises if it has not been built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError("libflround.so is not built (%s); run "
+                               "`python -m paper_2609_20359_amd.build`" % LIB_PATH)
+        L = ctypes.CDLL(LIB_PATH)
+        L.fl_status_string.argtypes = [ctypes.c_int]
+        L.fl_status_string.restype = ctypes.c_char_p
+        L.fl_version.restype = ctypes.c_int
+        L.fl_layout_create.argtypes = [ctypes.c_int64, ctypes.c_int64, _P, _P,
+                                       ctypes.POINTER(_P)]
+        L.fl_layout_destroy.argtypes = [_P]
+        L.fl_layout_numel.argtypes = [_P]
+        L.fl_layout_numel.restype = ctypes.c_int64
+        L.fl_layout_num_segments.argtypes = [_P]
+        L.fl_layout_num_segments.restype = ctypes.c_int64
+        L.fl_fingerprint.argtypes = [ctypes.c_int64, ctypes.c_int64, _P, _P]
+        L.fl_fingerprint.restype = ctypes.c_uint64
+        L.fl_layout_fingerprint.argtypes = [_P]
+        L.fl_layout_fingerprint.restype = ctypes.c_uint64
+        L.fl_shard_reduce.argtypes = [_P, ctypes.c_int, _P, ctypes.c_float, _P, _P, _P]
+        L.fl_adamw_step.argtypes = [_P, ctypes.POINTER(AdamwHparams), ctypes.c_int64, _P, _P,
+                                    _P, _P, _P, _P]
+        L.fl_local_step.argtypes = [_P, ctypes.POINTER(AdamwHparams), ctypes.c_int64,
+                                    ctypes.c_int, _P, ctypes.c_float, _P, _P, _P, _P, _P, _P]
+        L.fl_fedavg.argtypes = [_P, ctypes.c_int, _P, _P, _P, _P, _P, _P]
+        L.fl_round.argtypes = [_P, ctypes.POINTER(RoundCfg), _P, _P, _P, _P, _P, _P, _P, _P]
+        L.fl_set_blocks_per_cu.argtypes = [ctypes.c_int]
+        L.fl_set_blocks_per_cu.restype = ctypes.c_int
+        _lib = L
+    return _lib
+
+
+def status_string(status):
+    return lib().fl_status_string(status).decode()
+
+
+def _check(rc, where):
+    if rc != FL_OK:
+        raise FlError(rc, where)
+
+
+def _ptr(t):
+    """Device address of a tensor, or 0 for None."""
+    if t is None:
+        return None
+    if isinstance(t, int):
+        return t
+    if not t.is_contiguous():
+        raise ValueError("tensors passed to libflround must be contiguous")
+    return t.data_ptr()
+
+
+def _ptr_array(ts):
+    return (ctypes.c_void_p * len(ts))(*[_ptr(t) for t in ts])
+
+
+def _stream(stream):
+    if stream is not None:
+        return ctypes.c_void_p(stream if isinstance(stream, int) else stream.cuda_stream)
+    import torch
+
+    return ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+
+
+def hparams(hp):
+    if isinstance(hp, AdamwHparams):
+        return hp
+    return AdamwHparams(hp["lr"], hp["beta1"], hp["beta2"], hp["eps"], hp["weight_decay"])
+
+
+def set_blocks_per_cu(n):
+    """Cap the streaming kernels' grid at n * CUs (0 = default); returns the
+    previous value."""
+    return lib().fl_set_blocks_per_cu(int(n))
+
+
+def fingerprint(seg_offsets, seg_decay=None):
+    import numpy as np
+
+    off = np.ascontiguousarray(seg_offsets, dtype=np.int64)
+    dec = None if seg_decay is None else np.ascontiguousarray(seg_decay, dtype=np.uint8)
+    return lib().fl_fingerprint(int(off[-1]), off.size - 1, off.ctypes.data,
+                                None if dec is None else dec.ctypes.data)
+
+
+class Layout:
+    """fl_layout handle: the flat shard's segments and decay flags."""
+
+    def __init__(self, seg_offsets, seg_decay=None):
+        import numpy as np
+
+        off = np.ascontiguousarray(seg_offsets, dtype=np.int64)
+        dec = None if seg_decay is None else np.ascontiguousarray(seg_decay, dtype=np.uint8)
+        h = ctypes.c_void_p()
+        rc = lib().fl_layout_create(int(off[-1]), off.size - 1, off.ctypes.data,
+                                    None if dec is None else dec.ctypes.data, ctypes.byref(h))
+        _check(rc, "fl_layout_create")
+        self.handle = h
+        self.n = int(off[-1])
+        self.n_seg = off.size - 1
+
+    @property
+    def fingerprint(self):
+        return lib().fl_layout_fingerprint(self.handle)
+
+    def close(self):
+        if self.handle:
+            lib().fl_layout_destroy(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+def fl_shard_reduce(layout, peer_grads, grad_scale, grad_out, seg_sumsq=None, stream=None):
+    rc = lib().fl_shard_reduce(layout.handle, len(peer_grads), _ptr_array(peer_grads),
+                               float(grad_scale), _ptr(grad_out), _ptr(seg_sumsq), _stream(stream))
+    _check(rc, "fl_shard_reduce")
+
+
+def fl_adamw_step(layout, hp, step, grad, master, m, v, working=None, stream=None):
+    h = hparams(hp)
+    rc = lib().fl_adamw_step(layout.handle, ctypes.byref(h), int(step), _ptr(grad), _ptr(master),
+                             _ptr(m), _ptr(v), _ptr(working), _stream(stream))
+    _check(rc, "fl_adamw_step")
+
+
+def fl_local_step(layout, hp, step, peer_grads, grad_scale, master, m, v, working,
+                  seg_sumsq=None, stream=None):
+    h = hparams(hp)
+    rc = lib().fl_local_step(layout.handle, ctypes.byref(h), int(step), len(peer_grads),
+                             _ptr_array(peer_grads), float(grad_scale), _ptr(master), _ptr(m),
+                             _ptr(v), _ptr(working), _ptr(seg_sumsq), _stream(stream))
+    _check(rc, "fl_local_step")
+
+
+def fl_fedavg(layout, replicas, weights, master_out, working_out, replica_fp=None, stream=None):
+    G = len(replicas)
+    w = (ctypes.c_float * G)(*[float(x) for x in weights])
+    fp = None if replica_fp is None else (ctypes.c_uint64 * G)(*[int(x) for x in replica_fp])
+    rc = lib().fl_fedavg(layout.handle, G, _ptr_array(replicas), w, fp, _ptr(master_out),
+                         _ptr(working_out), _stream(stream))
+    _check(rc, "fl_fedavg")
+
+
+def make_round_cfg(R, G, A, weights, hp, *, self_group=0, grad_scale=None, step0=1,
+                   replica_fp=None, phase_events=None):
+    """Build an fl_round_cfg; the returned object keeps its arrays alive."""
+    w = (ctypes.c_float * G)(*[float(x) for x in weights])
+    fp = None if replica_fp is None else (ctypes.c_uint64 * G)(*[int(x) for x in replica_fp])
+    ev = None if phase_events is None else (ctypes.c_void_p * len(phase_events))(*phase_events)
+    cfg = RoundCfg(R, G, A, self_group, float(1.0 / R if grad_scale is None else grad_scale),
+                   hparams(hp), int(step0), w, fp, ev)
+    cfg._keep = (w, fp, ev)
+    return cfg
+
+
+def fl_round(layout, cfg, grads, replicas, master, m, v, working, seg_sumsq=None, stream=None):
+    """grads: A*R tensors (step-major); replicas: G tensors or None (entry
+    self_group is ignored)."""
+    rc = lib().fl_round(layout.handle, ctypes.byref(cfg), _ptr_array(grads),
+                        _ptr_array(replicas), _ptr(master), _ptr(m), _ptr(v), _ptr(working),
+                        _ptr(seg_sumsq), _stream(stream))
+    _check(rc, "fl_round")
+
+
+# ---- HIP events (for fl_round's per-phase timing) -------------------------
+
+_hip = None
+
+
+def hip_runtime():
+    global _hip
+    if _hip is None:
+        h = None
+        for name in ("libamdhip64.so", "libamdhip64.so.7", "/opt/rocm/lib/libamdhip64.so"):
+            try:
+                h = ctypes.CDLL(name)
+                break
+            except OSError:
+                continue
+        if h is None:
+            raise RuntimeError("HIP runtime library not found")
+        h.hipEventCreate.argtypes = [ctypes.POINTER(ctypes.c_void_p)]
+        h.hipEventDestroy.argtypes = [ctypes.c_void_p]
+        h.hipEventRecord.argtypes = [ctypes.c_void_p, ctypes.c_void_p]
+        h.hipEventSynchronize.argtypes = [ctypes.c_void_p]
+        h.hipEventElapsedTime.argtypes = [ctypes.POINTER(ctypes.c_float), ctypes.c_void_p,
+                                          ctypes.c_void_p]
+        _hip = h
+    return _hip
+
+
+class HipEvents:
+    """k raw hipEvent_t handles, for fl_round's phase_events."""
+
+    def __init__(self, k):
+        h = hip_runtime()
+        self.handles = []
+        for _ in range(k):
+            e = ctypes.c_void_p()
+            if h.hipEventCreate(ctypes.byref(e)) != 0:
+                raise RuntimeError("hipEventCreate failed")
+            self.handles.append(e.value)
+
+    def elapsed_ms(self, i, j):
+        h = hip_runtime()
+        out = ctypes.c_float()
+        if h.hipEventElapsedTime(ctypes.byref(out), self.handles[i], self.handles[j]) != 0:
+            raise RuntimeError("hipEventElapsedTime failed")
+        return out.value
+
+    def record(self, i, stream):
+        if hip_runtime().hipEventRecord(self.handles[i], stream) != 0:
+            raise RuntimeError("hipEventRecord failed")
+
+    def synchronize(self, i):
+        if hip_runtime().hipEventSynchronize(self.handles[i]) != 0:
+            raise RuntimeError("hipEventSynchronize failed")
+
+    def close(self):
+        h = hip_runtime()
+        for e in self.handles:
+            h.hipEventDestroy(e)
+        self.handles = []

@@ -73,6 +73,8 @@ def host_lib():
         lib = _load(os.path.join(HERE, "libsynth_host.so"), "host generator")
         P = ctypes.POINTER(SynthSpec)
         lib.synth_host_fill.argtypes = [P, ctypes.c_int64, ctypes.c_int64, ctypes.c_void_p]
+        lib.synth_host_fill_mt.argtypes = [P, ctypes.c_int64, ctypes.c_int64, ctypes.c_void_p,
+                                           ctypes.c_int]
         lib.synth_host_gather.argtypes = [P, ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p]
         lib.synth_host_draws.argtypes = [ctypes.c_uint64, ctypes.c_uint64, ctypes.c_uint32,
                                          ctypes.c_int64, ctypes.c_int64, ctypes.c_void_p]
@@ -99,10 +101,18 @@ def _out_array(sp, n):
     return np.empty(n, dtype=np.uint16 if sp.is_bf16 else np.float32)
 
 
-def host_fill(sp, i0, n):
+def host_threads():
+    try:
+        return max(1, min(16, len(os.sched_getaffinity(0))))
+    except AttributeError:
+        return 1
+
+
+def host_fill(sp, i0, n, threads=None):
     """Values at indices i0..i0+n-1 (uint16 bf16 bits, or float32)."""
     out = _out_array(sp, n)
-    rc = host_lib().synth_host_fill(ctypes.byref(sp), i0, n, out.ctypes.data)
+    threads = host_threads() if threads is None else threads
+    rc = host_lib().synth_host_fill_mt(ctypes.byref(sp), i0, n, out.ctypes.data, threads)
     if rc != 0:
         raise ValueError("synth_host_fill failed (%d) for %r" % (rc, sp))
     return out

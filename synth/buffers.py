@@ -1,0 +1,70 @@
+"""Input buffers of a workload, filled by the synth generator.
+
+DeviceInputs: torch CUDA tensors filled in HBM by the device build;
+HostInputs: numpy arrays from the host build, for all elements or at chosen
+indices (bit-identical to the device values).
+"""
+import numpy as np
+
+from . import dev_fill, host_fill, host_gather
+from .workloads import Workload
+
+
+class DeviceInputs:
+    def __init__(self, w: Workload, device="cuda:0"):
+        import torch
+
+        n = w.n
+        self.w = w
+        f32 = dict(dtype=torch.float32, device=device)
+        bf = dict(dtype=torch.bfloat16, device=device)
+        self.master = dev_fill(torch.empty(n, **f32), w.master_spec)
+        self.m = torch.zeros(n, **f32)
+        self.v = torch.zeros(n, **f32)
+        self.working = dev_fill(torch.empty(n, **bf), w.working_spec)
+        self.grad_arrays = [dev_fill(torch.empty(n, **bf), sp) for sp in w.grad_specs]
+        self.grads = [self.grad_arrays[k] for k in w.grad_index]
+        self.replicas = [None if sp is None else dev_fill(torch.empty(n, **bf), sp)
+                         for sp in w.replica_specs]
+
+    def bytes(self):
+        t = [self.master, self.m, self.v, self.working] + self.grad_arrays + \
+            [r for r in self.replicas if r is not None]
+        return sum(x.numel() * x.element_size() for x in t)
+
+
+def to_u16(t):
+    import torch
+
+    return t.contiguous().view(torch.int16).cpu().numpy().view(np.uint16)
+
+
+def gather_u16(t, idx_dev):
+    import torch
+
+    return to_u16(torch.index_select(t.view(torch.int16), 0, idx_dev))
+
+
+def gather_f32(t, idx_dev):
+    import torch
+
+    return torch.index_select(t, 0, idx_dev).cpu().numpy()
+
+
+class HostInputs:
+    """The same inputs on the host, for all elements or at given indices."""
+
+    def __init__(self, w: Workload, idx=None):
+        self.w = w
+        if idx is None:
+            fill = lambda sp: host_fill(sp, 0, w.n)  # noqa: E731
+        else:
+            fill = lambda sp: host_gather(sp, idx)  # noqa: E731
+        self.master = fill(w.master_spec)
+        n = self.master.size
+        self.m = np.zeros(n, np.float32)
+        self.v = np.zeros(n, np.float32)
+        self.working = fill(w.working_spec)
+        self.grad_arrays = [fill(sp) for sp in w.grad_specs]
+        self.grads = [self.grad_arrays[k] for k in w.grad_index]
+        self.replicas = [None if sp is None else fill(sp) for sp in w.replica_specs]

@@ -22,7 +22,7 @@ def _run(cmd):
 
 def build_host():
     _run(["gcc", "-std=c11", "-O2", "-fPIC", "-shared", "-ffp-contract=off",
-          "-fno-fast-math", "-Wall", "-Wextra", "-o", HOST_LIB, "synth_host.c"])
+          "-fno-fast-math", "-Wall", "-Wextra", "-o", HOST_LIB, "synth_host.c", "-lpthread"])
 
 
 def build_dev():

@@ -6,6 +6,7 @@
  * inputs of sampled elements for the oracle).  Must be compiled with
  * -ffp-contract=off so that its bits equal the device build's.
  */
+#include <pthread.h>
 #include <stddef.h>
 #include <stdint.h>
 
@@ -104,3 +105,49 @@ int synth_host_normals(uint64_t seed, uint64_t stream, int64_t i0, int64_t n,
 double synth_host_log(double x) { return synth_log(x); }
 double synth_host_cos2pi(double u) { return synth_cos2pi(u); }
 double synth_host_sqrt(double x) { return synth_sqrt(x); }
+
+/* synth_host_fill split over `threads` POSIX threads (same values). */
+typedef struct {
+  const synth_spec* sp;
+  int64_t i0, n;
+  void* out;
+  int rc;
+} synth_job;
+
+static void* synth_job_run(void* p) {
+  synth_job* j = (synth_job*)p;
+  j->rc = synth_host_fill(j->sp, j->i0, j->n, j->out);
+  return NULL;
+}
+
+int synth_host_fill_mt(const synth_spec* sp, int64_t i0, int64_t n, void* out, int threads) {
+  if (threads <= 1 || n < 65536) return synth_host_fill(sp, i0, n, out);
+  if (threads > 64) threads = 64;
+  if (!sp || !synth_kind_ok(sp->kind) || n < 0 || i0 < 0 || !out) return -1;
+  const size_t esz = synth_is_bf16(sp->kind) ? 2 : 4;
+  pthread_t tid[64];
+  synth_job job[64];
+  const int64_t chunk = (n + threads - 1) / threads;
+  int started = 0;
+  int rc = 0;
+  for (int t = 0; t < threads; ++t) {
+    const int64_t lo = (int64_t)t * chunk;
+    if (lo >= n) break;
+    const int64_t cnt = (lo + chunk <= n) ? chunk : n - lo;
+    job[t].sp = sp;
+    job[t].i0 = i0 + lo;
+    job[t].n = cnt;
+    job[t].out = (char*)out + (size_t)lo * esz;
+    job[t].rc = 0;
+    if (pthread_create(&tid[t], NULL, synth_job_run, &job[t]) != 0) {
+      job[t].rc = synth_host_fill(sp, i0 + lo, cnt, job[t].out);
+      tid[t] = 0;
+    }
+    started = t + 1;
+  }
+  for (int t = 0; t < started; ++t) {
+    if (tid[t]) pthread_join(tid[t], NULL);
+    if (job[t].rc) rc = job[t].rc;
+  }
+  return rc;
+}

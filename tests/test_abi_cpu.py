@@ -1,0 +1,93 @@
+"""The C ABI without a GPU: the library loads, exports every symbol the
+header declares, and its host-side logic (status strings, fingerprints,
+argument validation that happens before any HIP call) behaves."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+import paper_2609_20359_amd as P
+from paper_2609_20359_amd import flround as F
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "flround.h")
+
+
+def header_functions():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(fl_[a-z0-9_]+)\s*\(", src)))
+
+
+def test_header_declares_the_binding_exports():
+    assert header_functions() == sorted(F.EXPORTS)
+
+
+def test_library_exports_every_declared_symbol():
+    lib = ctypes.CDLL(F.LIB_PATH)
+    missing = [f for f in header_functions() if not hasattr(lib, f)]
+    assert not missing, missing
+
+
+def test_status_strings_and_version():
+    assert P.status_string(0) == "FL_OK"
+    for code in range(-6, 0):
+        assert P.status_string(code).startswith("FL_ERR_")
+    assert "unknown" in P.status_string(7)
+    assert P.lib().fl_version() >> 16 == 1
+
+
+def test_fingerprint_host():
+    off = np.array([0, 512, 4096, 10000], np.int64)
+    dec = np.array([1, 0, 1], np.uint8)
+    a = P.fingerprint(off, dec)
+    assert a != 0
+    assert a == P.fingerprint(off.copy(), dec.copy())
+    assert a == P.fingerprint(off, np.array([7, 0, 1], np.uint8))     # flags are 0/1
+    assert a != P.fingerprint(off, np.array([1, 1, 1], np.uint8))     # decay differs
+    assert a != P.fingerprint(np.array([0, 513, 4096, 10000]), dec)   # boundary differs
+    assert P.fingerprint(off) == P.fingerprint(off, np.ones(3, np.uint8))
+    # invalid layouts hash to 0
+    L = P.lib()
+    bad = np.array([0, 10, 10, 20], np.int64)
+    assert L.fl_fingerprint(20, 3, bad.ctypes.data, None) == 0
+    assert L.fl_fingerprint(21, 3, off.ctypes.data, None) == 0
+    assert L.fl_fingerprint(-1, 0, off.ctypes.data, None) == 0
+
+
+def test_layout_create_rejects_bad_layouts_without_a_gpu():
+    L = P.lib()
+    h = ctypes.c_void_p()
+    cases = [
+        (10, 2, np.array([0, 5, 5], np.int64)),      # empty segment
+        (10, 2, np.array([1, 5, 10], np.int64)),     # does not start at 0
+        (10, 2, np.array([0, 5, 9], np.int64)),      # does not end at n
+        (10, 0, np.array([0], np.int64)),            # n > 0 needs a segment
+        (-5, 1, np.array([0, -5], np.int64)),        # negative n
+    ]
+    for n, ns, off in cases:
+        assert L.fl_layout_create(n, ns, off.ctypes.data, None, ctypes.byref(h)) == -1
+    assert L.fl_layout_create(10, 1, None, None, ctypes.byref(h)) == -1
+    assert L.fl_layout_create(10, 1, np.array([0, 10]).ctypes.data, None, None) == -1
+
+
+def test_calls_reject_null_handles_without_a_gpu():
+    L = P.lib()
+    cfg = F.make_round_cfg(2, 2, 1, [1.0, 1.0], dict(lr=3e-4, beta1=0.9, beta2=0.95, eps=1e-8,
+                                                   weight_decay=0.1))
+    arr = (ctypes.c_void_p * 4)()
+    assert L.fl_round(None, ctypes.byref(cfg), arr, arr, None, None, None, None, None, None) == -1
+    assert L.fl_fedavg(None, 2, arr, None, None, None, None, None) == -1
+    assert L.fl_shard_reduce(None, 1, arr, ctypes.c_float(1.0), None, None, None) == -1
+    h = F.hparams(dict(lr=3e-4, beta1=0.9, beta2=0.95, eps=1e-8, weight_decay=0.1))
+    assert L.fl_adamw_step(None, ctypes.byref(h), 1, None, None, None, None, None, None) == -1
+    assert L.fl_layout_numel(None) == -1
+    assert L.fl_layout_fingerprint(None) == 0
+    assert L.fl_layout_destroy(None) == 0
+
+
+def test_blocks_per_cu_setting_round_trips():
+    prev = P.set_blocks_per_cu(5)
+    assert P.set_blocks_per_cu(prev) == 5
