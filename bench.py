@@ -54,6 +54,91 @@ def read_traffic(current_hash):
         return None
 
 
+LOCAL_STEP_KERNEL = "k_step<8, 0, false>"
+FEDAVG_KERNEL = "k_fedavg<4>"
+COPY_KERNEL = "__amd_rocclr_copyBuffer"
+
+
+def _pmc_means(path):
+    """Per-kernel mean and count of a rocprofv3 --pmc counter_collection CSV."""
+    import csv
+
+    acc = {}
+    for r in csv.DictReader(open(path)):
+        key = (r["Kernel_Name"], int(r["Grid_Size"]))
+        acc.setdefault(key, []).append(float(r["Counter_Value"]))
+    return {k: (sum(v) / len(v), len(v)) for k, v in acc.items()}
+
+
+def summarize_pmc(fetch_csv, write_csv, copy_mib, cmd_fetch, cmd_write):
+    """Markdown summary of two counter passes (FETCH_SIZE, WRITE_SIZE, KiB per
+    dispatch), scaled by what each counter reads for the plain copy of
+    copy_mib MiB that the same runs performed."""
+    w = W_ALL()["llama8b_s8"]()
+    fetch, write = _pmc_means(fetch_csv), _pmc_means(write_csv)
+
+    def pick(table, name, grid=None):
+        for (k, g), v in table.items():
+            if name in k and (grid is None or g == grid):
+                return v
+        raise KeyError(name)
+
+    copy_kib = copy_mib * 1024.0
+    cands = [(k, g) for (k, g) in fetch if COPY_KERNEL in k]
+    big = max(cands, key=lambda kg: fetch[kg][0])
+    f_copy, w_copy = fetch[big][0], write[big][0]
+    f_scale, w_scale = copy_kib / f_copy, copy_kib / w_copy
+    lines = ["# HBM traffic of the local-step and FedAvg kernels, Llama-3.1-8B shard (S=8)", "",
+             "Counter passes (one counter per run, KiB per dispatch):", "",
+             "    " + cmd_fetch, "    " + cmd_write, "",
+             "Calibration: the same runs copy %d MiB with %s (reads and writes %d KiB)." % (
+                 copy_mib, COPY_KERNEL, copy_kib),
+             "FETCH_SIZE reads %.1f KiB for it -> scale %.5f; WRITE_SIZE reads %.1f KiB -> "
+             "scale %.5f." % (f_copy, f_scale, w_copy, w_scale), "",
+             "| kernel | dispatches | FETCH_SIZE KiB | WRITE_SIZE KiB | scaled read GB | "
+             "scaled write GB | algorithmic read GB | algorithmic write GB | traffic / algorithmic |",
+             "|---|---|---|---|---|---|---|---|---|"]
+    n = w.n
+    specs = [(LOCAL_STEP_KERNEL, (2 * w.R + 12) * n, 14 * n),
+             (FEDAVG_KERNEL, 2 * w.G * n, 6 * n)]
+    out = {}
+    for name, alg_r, alg_w in specs:
+        f, cnt = pick(fetch, name)
+        wr, _ = pick(write, name)
+        rb, wb = f * f_scale * 1024, wr * w_scale * 1024
+        out[name] = rb + wb
+        lines.append("| %s | %d | %.1f | %.1f | %.4f | %.4f | %.4f | %.4f | %.4f |" % (
+            name, cnt, f, wr, rb / 1e9, wb / 1e9, alg_r / 1e9, alg_w / 1e9,
+            (rb + wb) / (alg_r + alg_w)))
+    lines += ["", "Values read by bench.py (roofline.traffic of the local-step kernel):", "",
+              "- kernel_source_hash: %s" % kernel_source_hash(),
+              "- hbm_bytes_per_launch: %.0f" % out[LOCAL_STEP_KERNEL],
+              "- fedavg_hbm_bytes_per_launch: %.0f" % out[FEDAVG_KERNEL], ""]
+    return "\n".join(lines)
+
+
+def summarize_trace(stats_csv, cmd):
+    import csv
+
+    rows = list(csv.DictReader(open(stats_csv)))
+    lines = ["# Kernel trace, fl_round on the Llama-3.1-8B shard (S=8, R=8, G=4, A=8)", "",
+             "    " + cmd, "",
+             "| kernel | calls | average us | min us | max us | share of GPU time |",
+             "|---|---|---|---|---|---|"]
+    for r in rows:
+        lines.append("| %s | %s | %.1f | %.1f | %.1f | %.2f %% |" % (
+            r["Name"].replace("|", "/"), r["Calls"], float(r["AverageNs"]) / 1e3,
+            float(r["MinNs"]) / 1e3, float(r["MaxNs"]) / 1e3, float(r["Percentage"])))
+    lines.append("")
+    return "\n".join(lines)
+
+
+def W_ALL():
+    from synth import workloads as W
+
+    return W.ALL
+
+
 def cpu_baseline(w, n_sample):
     """The oracle as it stands, one thread, one full round on the first
     n_sample elements of the same shard (same generator, same segments)."""
@@ -88,7 +173,23 @@ def main():
     ap.add_argument("--workload", default="llama8b_s8")
     ap.add_argument("--cpu-sample", type=int, default=32 << 20)
     ap.add_argument("--no-cpu", action="store_true")
+    ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
+                    help="first run one plain torch copy of MIB MiB (reference kernel of "
+                         "known traffic for counter runs)")
+    ap.add_argument("--summarize-pmc", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
+                    help="print the traffic summary of two rocprofv3 --pmc runs and exit")
+    ap.add_argument("--summarize-trace", metavar="KERNEL_STATS_CSV",
+                    help="print the summary of a rocprofv3 --kernel-trace --stats run and exit")
+    ap.add_argument("--cmd", nargs="*", default=[], help="command line(s) quoted in a summary")
     args = ap.parse_args()
+    if args.summarize_pmc:
+        cmds = args.cmd + ["", ""]
+        print(summarize_pmc(args.summarize_pmc[0], args.summarize_pmc[1],
+                            args.copy_calibration or 1024, cmds[0], cmds[1]))
+        return
+    if args.summarize_trace:
+        print(summarize_trace(args.summarize_trace, (args.cmd + [""])[0]))
+        return
     if args.gpus != 1:
         print("bench.py measures one GPU's share of the path; the multi-GPU collectives are "
               "not part of this build, so --gpus %d is not supported (use --gpus 1)"
@@ -113,6 +214,16 @@ def main():
     dev = B.DeviceInputs(w)
     torch.cuda.synchronize()
     log("inputs resident: %.1f GB in %.1f s" % (dev.bytes() / 1e9, time.perf_counter() - t0))
+
+    if args.copy_calibration:
+        src = torch.empty(args.copy_calibration << 18, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        src.fill_(1.0)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        log("copy calibration: %d MiB copied" % args.copy_calibration)
+        del src, dst
 
     stream = torch.cuda.current_stream()
     K, Wm = args.steps, args.warmup

@@ -1,0 +1,161 @@
+// hbm_probe -- attainable HBM bandwidth on this GPU for the access patterns of
+// the parameter-sync kernels, with no arithmetic: the ceiling that the local
+// step and FedAvg kernels are compared with, besides the 8 TB/s datasheet
+// peak.  Not part of the library.
+//
+// Patterns (every stream a separate buffer; each thread moves 16 B of every
+// stream per grid-stride iteration, 256-thread workgroups):
+//   read1      1 stream read
+//   write1     1 stream written
+//   copy       1 read, 1 written
+//   step_R8    8 bf16 streams read, 3 fp32 streams read and written, 1 bf16
+//              stream written: the traffic of one fused local step (R = 8)
+//   fedavg_G4  4 bf16 streams read, 1 fp32 and 1 bf16 stream written
+// each with plain and nontemporal stores, for 1..8 workgroups per CU.
+// Buffers are sized for the 1,003,782,144-element shard.
+//
+// usage: hbm_probe [elements]
+#include <hip/hip_runtime.h>
+
+#include <cstdio>
+#include <cstdlib>
+#include <vector>
+
+typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
+
+#define CK(x)                                                                         \
+  do {                                                                                \
+    hipError_t e_ = (x);                                                              \
+    if (e_ != hipSuccess) {                                                           \
+      std::printf("HIP error %s at line %d\n", hipGetErrorString(e_), __LINE__);      \
+      std::exit(1);                                                                   \
+    }                                                                                 \
+  } while (0)
+
+struct Streams {
+  const u32x4* rd[12];  // read-only 16-byte streams, in units of u32x4
+  u32x4* rmw[4];        // read-modify-write streams (fp32, 2 x 16 B per thread)
+  u32x4* wr[2];         // write-only streams
+  long nvec;            // 16-byte vectors per bf16 stream
+};
+
+// NRD bf16 streams read, NRMW fp32 streams read+written, NWH bf16 streams
+// written, NWF fp32 streams written.  fp32 streams hold 2 vectors per bf16
+// vector.  All indices < nvec (bf16) or < 2 * nvec (fp32).
+template <int NRD, int NRMW, int NWH, int NWF, bool NTS>
+__global__ void __launch_bounds__(256) k_pattern(Streams s) {
+  const long stride = (long)gridDim.x * 256;
+  for (long i = (long)blockIdx.x * 256 + threadIdx.x; i < s.nvec; i += stride) {
+    u32x4 x = {(unsigned)i, 0u, 0u, 0u};
+#pragma unroll
+    for (int k = 0; k < NRD; ++k) x += __builtin_nontemporal_load(s.rd[k] + i);
+    u32x4 a[NRMW > 0 ? NRMW : 1], b[NRMW > 0 ? NRMW : 1];
+#pragma unroll
+    for (int k = 0; k < NRMW; ++k) {
+      a[k] = s.rmw[k][2 * i];
+      b[k] = s.rmw[k][2 * i + 1];
+    }
+#pragma unroll
+    for (int k = 0; k < NRMW; ++k) {
+      if (NTS) {
+        __builtin_nontemporal_store(a[k] + x, s.rmw[k] + 2 * i);
+        __builtin_nontemporal_store(b[k] + x, s.rmw[k] + 2 * i + 1);
+      } else {
+        s.rmw[k][2 * i] = a[k] + x;
+        s.rmw[k][2 * i + 1] = b[k] + x;
+      }
+    }
+#pragma unroll
+    for (int k = 0; k < NWH; ++k) {
+      if (NTS) __builtin_nontemporal_store(x, s.wr[k] + i); else s.wr[k][i] = x;
+    }
+#pragma unroll
+    for (int k = 0; k < NWF; ++k) {
+      if (NTS) {
+        __builtin_nontemporal_store(x, s.wr[1 - k] + 2 * i);
+        __builtin_nontemporal_store(x, s.wr[1 - k] + 2 * i + 1);
+      } else {
+        s.wr[1 - k][2 * i] = x;
+        s.wr[1 - k][2 * i + 1] = x;
+      }
+    }
+    if (NRD + NRMW + NWH + NWF == NRD && x.y == 0xFFFFFFFFu && x.z == 0x12345u)
+      s.wr[0][0] = x;  // keep read-only loads alive
+  }
+}
+
+template <typename F>
+float time_ms(F launch, int reps) {
+  hipEvent_t a, b;
+  CK(hipEventCreate(&a));
+  CK(hipEventCreate(&b));
+  launch();
+  CK(hipDeviceSynchronize());
+  CK(hipEventRecord(a));
+  for (int r = 0; r < reps; ++r) launch();
+  CK(hipEventRecord(b));
+  CK(hipEventSynchronize(b));
+  float ms = 0.f;
+  CK(hipEventElapsedTime(&ms, a, b));
+  CK(hipEventDestroy(a));
+  CK(hipEventDestroy(b));
+  return ms / reps;
+}
+
+template <int NRD, int NRMW, int NWH, int NWF>
+void run(const char* name, Streams s, int cus, long elems) {
+  const double bytes = (double)elems * (2.0 * NRD + 8.0 * NRMW + 2.0 * NWH + 4.0 * NWF);
+  for (int nts = 0; nts < 2; ++nts) {
+    double best = 0.0;
+    int best_bpc = 0;
+    std::printf("| %-9s | %-5s |", name, nts ? "nt" : "plain");
+    for (int bpc : {1, 2, 4, 8}) {
+      const int grid = bpc * cus;
+      float ms = nts ? time_ms([&] { k_pattern<NRD, NRMW, NWH, NWF, true><<<grid, 256>>>(s); }, 5)
+                     : time_ms([&] { k_pattern<NRD, NRMW, NWH, NWF, false><<<grid, 256>>>(s); }, 5);
+      CK(hipGetLastError());
+      const double gbs = bytes / (ms * 1e-3) / 1e9;
+      std::printf(" %7.1f |", gbs);
+      if (gbs > best) {
+        best = gbs;
+        best_bpc = bpc;
+      }
+    }
+    std::printf(" %7.1f (%d/CU) | %5.1f %% |\n", best, best_bpc, 100.0 * best / 8000.0);
+    std::fflush(stdout);
+  }
+}
+
+int main(int argc, char** argv) {
+  long elems = argc > 1 ? std::atol(argv[1]) : 1003782144L;
+  elems -= elems % 8;
+  int cus = 0;
+  CK(hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, 0));
+  hipDeviceProp_t prop;
+  CK(hipGetDeviceProperties(&prop, 0));
+  Streams s;
+  s.nvec = elems / 8;
+  std::vector<void*> bufs;
+  auto alloc = [&](size_t b) {
+    void* p = nullptr;
+    CK(hipMalloc(&p, b));
+    CK(hipMemset(p, 0, b));
+    bufs.push_back(p);
+    return p;
+  };
+  for (int k = 0; k < 12; ++k) s.rd[k] = static_cast<const u32x4*>(alloc(elems * 2));
+  for (int k = 0; k < 4; ++k) s.rmw[k] = static_cast<u32x4*>(alloc(elems * 4));
+  for (int k = 0; k < 2; ++k) s.wr[k] = static_cast<u32x4*>(alloc(elems * 4));
+  std::printf("# HBM ceiling probe: %s, %d CUs, %ld-element streams\n\n", prop.gcnArchName, cus,
+              elems);
+  std::printf("GB/s by workgroups per CU; bytes = bytes the pattern moves; peak 8000 GB/s.\n\n");
+  std::printf("| pattern | stores | 1/CU | 2/CU | 4/CU | 8/CU | best | of peak |\n");
+  std::printf("|---|---|---|---|---|---|---|---|\n");
+  run<1, 0, 0, 0>("read1", s, cus, elems);
+  run<0, 0, 1, 0>("write1", s, cus, elems);
+  run<1, 0, 1, 0>("copy", s, cus, elems);
+  run<8, 3, 1, 0>("step_R8", s, cus, elems);
+  run<4, 0, 1, 1>("fedavg_G4", s, cus, elems);
+  for (void* p : bufs) CK(hipFree(p));
+  return 0;
+}

@@ -29,7 +29,7 @@ struct fl_layout {
 namespace {
 
 int g_blocks_per_cu = 0;  // 0: default
-constexpr int kDefaultBlocksPerCu = 8;
+constexpr int kDefaultBlocksPerCu = 1;
 
 constexpr uint64_t kFnvOffset = 0xCBF29CE484222325ULL;
 constexpr uint64_t kFnvPrime = 0x100000001B3ULL;

@@ -24,13 +24,27 @@ namespace {
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
-// Streaming access: data read or written exactly once per pass.
+// Cache hints.  ld_once: streams read once per pass (peer gradients, FedAvg
+// replicas); ld: the read-modify-write state (master, m, v, fp32 gradient);
+// st: every store.
+#ifndef FLR_NT_ONCE
+#define FLR_NT_ONCE 1
+#endif
 #ifndef FLR_NT_LOADS
-#define FLR_NT_LOADS 1
+#define FLR_NT_LOADS 0
 #endif
 #ifndef FLR_NT_STORES
 #define FLR_NT_STORES 1
 #endif
+
+template <typename T>
+__device__ __forceinline__ T ld_once(const T* p) {
+#if FLR_NT_ONCE
+  return __builtin_nontemporal_load(p);
+#else
+  return *p;
+#endif
+}
 
 template <typename T>
 __device__ __forceinline__ T ld(const T* p) {
@@ -112,7 +126,7 @@ __device__ __forceinline__ void reduce_vec(const StepArgs& a, int64_t base, floa
   if constexpr (RT > 0) {
     u32x4 w[RT];
 #pragma unroll
-    for (int r = 0; r < RT; ++r) w[r] = ld(reinterpret_cast<const u32x4*>(a.grads[r] + base));
+    for (int r = 0; r < RT; ++r) w[r] = ld_once(reinterpret_cast<const u32x4*>(a.grads[r] + base));
 #pragma unroll
     for (int r = 0; r < RT; ++r) add_bf16x8(acc, w[r]);
   } else {
@@ -121,7 +135,7 @@ __device__ __forceinline__ void reduce_vec(const StepArgs& a, int64_t base, floa
       u32x4 w[kChunk];
 #pragma unroll
       for (int k = 0; k < kChunk; ++k)
-        if (r0 + k < a.R) w[k] = ld(reinterpret_cast<const u32x4*>(a.grads[r0 + k] + base));
+        if (r0 + k < a.R) w[k] = ld_once(reinterpret_cast<const u32x4*>(a.grads[r0 + k] + base));
 #pragma unroll
       for (int k = 0; k < kChunk; ++k)
         if (r0 + k < a.R) add_bf16x8(acc, w[k]);
@@ -292,7 +306,7 @@ __global__ void __launch_bounds__(kBlock) k_fedavg(const FedArgs a) {
       if constexpr (GT > 0) {
         u32x4 w[GT];
 #pragma unroll
-        for (int k = 0; k < GT; ++k) w[k] = ld(reinterpret_cast<const u32x4*>(a.reps[k] + base));
+        for (int k = 0; k < GT; ++k) w[k] = ld_once(reinterpret_cast<const u32x4*>(a.reps[k] + base));
 #pragma unroll
         for (int k = 0; k < GT; ++k) fma_free_bf16x8(acc, a.w[k], w[k]);
       } else {
@@ -301,7 +315,7 @@ __global__ void __launch_bounds__(kBlock) k_fedavg(const FedArgs a) {
           u32x4 w[kChunk];
 #pragma unroll
           for (int k = 0; k < kChunk; ++k)
-            if (k0 + k < a.G) w[k] = ld(reinterpret_cast<const u32x4*>(a.reps[k0 + k] + base));
+            if (k0 + k < a.G) w[k] = ld_once(reinterpret_cast<const u32x4*>(a.reps[k0 + k] + base));
 #pragma unroll
           for (int k = 0; k < kChunk; ++k)
             if (k0 + k < a.G) fma_free_bf16x8(acc, a.w[k0 + k], w[k]);
