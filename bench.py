@@ -1,7 +1,8 @@
 """Benchmark of one GPU's share of the FL+FSDP parameter sync (fl_round).
 
 A step is one fl_round: A = 8 fused local steps (R = 8 peer gradients ->
-AdamW on the fp32 master shard -> bf16 working copy) and one FedAvg of G = 4
+AdamW on the fp32 master shard -> bf16 working copy, with the per-segment
+sums of squares of each step's reduced gradient) and one FedAvg of G = 4
 federation-group replicas, on the Llama-3.1-8B shard of a rank in a sharding
 group of 8 (N = 1,003,782,144 parameters in 290 segments), with every input
 already resident in HBM.  Prints one JSON line.
@@ -54,7 +55,7 @@ def read_traffic(current_hash):
         return None
 
 
-LOCAL_STEP_KERNEL = "k_step<8, 0, false>"
+LOCAL_STEP_KERNEL = "k_step<8, 0, true>"
 FEDAVG_KERNEL = "k_fedavg<4>"
 COPY_KERNEL = "__amd_rocclr_copyBuffer"
 
@@ -230,8 +231,12 @@ def main():
     events = [P.HipEvents(w.A + 2) for _ in range(K)]
     cfg_plain = P.make_round_cfg(w.R, w.G, w.A, w.weights, w.hp, self_group=w.self_group,
                                  grad_scale=w.grad_scale, step0=w.step0)
+    # every round also returns the per-segment sums of squares of each local
+    # step's reduced gradient (A x n_seg floats)
+    seg_sumsq = torch.empty(w.A * w.n_seg, dtype=torch.float32, device="cuda")
     for i in range(Wm):
-        P.fl_round(lay, cfg_plain, dev.grads, dev.replicas, dev.master, dev.m, dev.v, dev.working)
+        P.fl_round(lay, cfg_plain, dev.grads, dev.replicas, dev.master, dev.m, dev.v, dev.working,
+                   seg_sumsq=seg_sumsq)
     torch.cuda.synchronize()
     log("warmup done (%d rounds)" % Wm)
 
@@ -244,7 +249,8 @@ def main():
     t_wall = time.perf_counter()
     start.record(stream)
     for k in range(K):
-        P.fl_round(lay, cfgs[k], dev.grads, dev.replicas, dev.master, dev.m, dev.v, dev.working)
+        P.fl_round(lay, cfgs[k], dev.grads, dev.replicas, dev.master, dev.m, dev.v, dev.working,
+                   seg_sumsq=seg_sumsq)
     stop.record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t_wall
@@ -286,7 +292,7 @@ def main():
                           fedavg_gbs=round(fed_bytes / (avg_fed * 1e-3) / 1e9, 2)),
         "roofline": {
             "bound": "hbm",
-            "kernel": "k_step<R=8, fused> (one local step)",
+            "kernel": "k_step<R=8, fused, per-segment sums> (one local step)",
             "achieved": round(achieved, 2),
             "peak": PEAK_HBM_GBS,
             "unit": "GB/s",

@@ -11,6 +11,9 @@
 //   step_R8    8 bf16 streams read, 3 fp32 streams read and written, 1 bf16
 //              stream written: the traffic of one fused local step (R = 8)
 //   fedavg_G4  4 bf16 streams read, 1 fp32 and 1 bf16 stream written
+//   step_R8_tiled  as step_R8, but the three fp32 state arrays interleaved per
+//              2048-element tile ([tile][master | m | v]), i.e. one 24 KB
+//              read-modify-write chunk per tile instead of three streams
 // each with plain and nontemporal stores, for 1..8 workgroups per CU.
 // Buffers are sized for the 1,003,782,144-element shard.
 //
@@ -32,12 +35,65 @@ typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
     }                                                                                 \
   } while (0)
 
+template <typename F>
+float time_ms(F launch, int reps);
+
 struct Streams {
   const u32x4* rd[12];  // read-only 16-byte streams, in units of u32x4
   u32x4* rmw[4];        // read-modify-write streams (fp32, 2 x 16 B per thread)
   u32x4* wr[2];         // write-only streams
+  u32x4* tiled;         // 3 fp32 arrays interleaved per 2048-element tile
   long nvec;            // 16-byte vectors per bf16 stream
 };
+
+// 8 bf16 streams read; master/m/v tile-interleaved (read and written); one
+// bf16 stream written.  Tile of vector i: i / 256; its state block holds
+// 3 x 512 vectors.  Indices stay below 6 * nvec.
+template <bool NTS>
+__global__ void __launch_bounds__(256) k_step_tiled(Streams s) {
+  const long stride = (long)gridDim.x * 256;
+  for (long i = (long)blockIdx.x * 256 + threadIdx.x; i < s.nvec; i += stride) {
+    u32x4 x = {(unsigned)i, 0u, 0u, 0u};
+#pragma unroll
+    for (int k = 0; k < 8; ++k) x += __builtin_nontemporal_load(s.rd[k] + i);
+    const long base = (i / 256) * 1536 + (i % 256) * 2;
+    u32x4 a[6];
+#pragma unroll
+    for (int k = 0; k < 3; ++k) {
+      a[2 * k] = s.tiled[base + 512 * k];
+      a[2 * k + 1] = s.tiled[base + 512 * k + 1];
+    }
+#pragma unroll
+    for (int k = 0; k < 6; ++k) {
+      u32x4* q = s.tiled + base + 512 * (k / 2) + (k & 1);
+      if (NTS) __builtin_nontemporal_store(a[k] + x, q); else *q = a[k] + x;
+    }
+    if (NTS) __builtin_nontemporal_store(x, s.wr[0] + i); else s.wr[0][i] = x;
+  }
+}
+
+void run_tiled(Streams s, int cus, long elems) {
+  const double bytes = (double)elems * 42.0;
+  for (int nts = 0; nts < 2; ++nts) {
+    double best = 0.0;
+    int best_bpc = 0;
+    std::printf("| %-9s | %-5s |", "step_R8_tiled", nts ? "nt" : "plain");
+    for (int bpc : {1, 2, 4, 8}) {
+      const int grid = bpc * cus;
+      float ms = nts ? time_ms([&] { k_step_tiled<true><<<grid, 256>>>(s); }, 5)
+                     : time_ms([&] { k_step_tiled<false><<<grid, 256>>>(s); }, 5);
+      CK(hipGetLastError());
+      const double gbs = bytes / (ms * 1e-3) / 1e9;
+      std::printf(" %7.1f |", gbs);
+      if (gbs > best) {
+        best = gbs;
+        best_bpc = bpc;
+      }
+    }
+    std::printf(" %7.1f (%d/CU) | %5.1f %% |\n", best, best_bpc, 100.0 * best / 8000.0);
+    std::fflush(stdout);
+  }
+}
 
 // NRD bf16 streams read, NRMW fp32 streams read+written, NWH bf16 streams
 // written, NWF fp32 streams written.  fp32 streams hold 2 vectors per bf16
@@ -146,6 +202,7 @@ int main(int argc, char** argv) {
   for (int k = 0; k < 12; ++k) s.rd[k] = static_cast<const u32x4*>(alloc(elems * 2));
   for (int k = 0; k < 4; ++k) s.rmw[k] = static_cast<u32x4*>(alloc(elems * 4));
   for (int k = 0; k < 2; ++k) s.wr[k] = static_cast<u32x4*>(alloc(elems * 4));
+  s.tiled = static_cast<u32x4*>(alloc(elems * 12 + 3 * 2048 * 4));
   std::printf("# HBM ceiling probe: %s, %d CUs, %ld-element streams\n\n", prop.gcnArchName, cus,
               elems);
   std::printf("GB/s by workgroups per CU; bytes = bytes the pattern moves; peak 8000 GB/s.\n\n");
@@ -156,6 +213,7 @@ int main(int argc, char** argv) {
   run<1, 0, 1, 0>("copy", s, cus, elems);
   run<8, 3, 1, 0>("step_R8", s, cus, elems);
   run<4, 0, 1, 1>("fedavg_G4", s, cus, elems);
+  run_tiled(s, cus, elems);
   for (void* p : bufs) CK(hipFree(p));
   return 0;
 }

@@ -121,7 +121,7 @@ typedef struct {
  * seg_sumsq: NULL, or device pointer to n_seg floats receiving, per segment,
  *   the sum of grad_out[i]^2 (fp32 squares, partial sums in a fixed tree,
  *   final sum in double): per-layer gradient-norm telemetry.  Needs a
- *   stream-ordered temporary of 4 bytes per (2048-element tile, segment)
+ *   stream-ordered temporary of 16 bytes per (2048-element tile, segment)
  *   pair, allocated and freed on `stream`.
  * 1 <= R <= FL_MAX_PEERS; grad_scale finite.
  * ---------------------------------------------------------------------- */

@@ -10,6 +10,8 @@ namespace flr {
 constexpr int kBlock = 256;            // threads per workgroup (4 wave64)
 constexpr int kVec = 8;                // elements per thread per tile (16 B of bf16)
 constexpr int kTile = kBlock * kVec;   // elements per tile: 2048
+constexpr int kWaves = kBlock / 64;    // wave64s per workgroup: one partial slot each
+constexpr int kChunkPieces = 1024;    // pieces folded by one workgroup in the finalize
 constexpr int kMaxPeers = 64;
 constexpr int kMaxGroups = 64;
 
@@ -37,6 +39,11 @@ struct LayoutDev {
   const TileInfo* tiles;      // n_tiles
   const int64_t* seg_piece0;  // n_seg + 1: pieces of segment s are
                               // [seg_piece0[s], seg_piece0[s+1])
+  int64_t n_chunks;
+  const int64_t* chunk_p0;    // n_chunks + 1: chunk c folds pieces
+                              // [chunk_p0[c], chunk_p0[c+1]), all of one segment
+  const int64_t* seg_chunk0;  // n_seg + 1: chunks of segment s are
+                              // [seg_chunk0[s], seg_chunk0[s+1])
 };
 
 // Per-step AdamW scalars, computed on the host in double, rounded to float.
@@ -58,7 +65,8 @@ struct StepArgs {
   uint16_t* working;   // may be null for the standalone AdamW step
   float* g_out;        // standalone reduce: fp32 reduced gradient
   const float* g_in;   // standalone AdamW: fp32 gradient
-  float* partials;     // per-piece sums of squares (null: not requested)
+  float* partials;     // per-(piece, wave) sums of squares, kWaves per piece
+                       // (null: not requested)
 };
 
 struct FedArgs {
@@ -74,7 +82,9 @@ hipError_t launch_local_step(const StepArgs& a, int grid, hipStream_t st);
 hipError_t launch_reduce(const StepArgs& a, int grid, hipStream_t st);
 hipError_t launch_adamw(const StepArgs& a, int grid, hipStream_t st);
 hipError_t launch_fedavg(const FedArgs& a, int grid, hipStream_t st);
-hipError_t launch_seg_finalize(const LayoutDev& L, const float* partials, float* out,
-                               hipStream_t st);
+// Per-segment totals from the (piece, wave) partials; chunk_sums is a
+// temporary of L.n_chunks doubles.
+hipError_t launch_seg_finalize(const LayoutDev& L, const float* partials, double* chunk_sums,
+                               float* out, hipStream_t st);
 
 }  // namespace flr

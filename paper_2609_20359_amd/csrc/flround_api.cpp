@@ -153,22 +153,30 @@ int check_peers(int R, const uint16_t* const* peers, int64_t n) {
   return FL_OK;
 }
 
-// Stream-ordered temporary for the per-piece partial sums.
+// Stream-ordered temporary for the per-segment sums of squares: the
+// (piece, wave) partials (kWaves floats per piece) followed by one double
+// per finalize chunk.
 struct Workspace {
   float* p = nullptr;
+  double* chunks = nullptr;
   hipStream_t st = nullptr;
-  int alloc(int64_t n_pieces, hipStream_t stream) {
+  int alloc(const flr::LayoutDev& L, hipStream_t stream) {
     st = stream;
+    size_t slots = (size_t)(L.n_pieces > 0 ? L.n_pieces : 1) * flr::kWaves;
+    slots = (slots + 3) & ~(size_t)3;  // keep the double region 16-byte aligned
+    const size_t bytes = slots * sizeof(float) + (size_t)(L.n_chunks > 0 ? L.n_chunks : 1) * sizeof(double);
     void* q = nullptr;
-    const hipError_t e = hipMallocAsync(&q, (size_t)(n_pieces > 0 ? n_pieces : 1) * sizeof(float), st);
+    const hipError_t e = hipMallocAsync(&q, bytes, st);
     if (e != hipSuccess) return status_of(e);
     p = static_cast<float*>(q);
+    chunks = reinterpret_cast<double*>(p + slots);
     return FL_OK;
   }
   int release() {
     if (!p) return FL_OK;
     const hipError_t e = hipFreeAsync(p, st);
     p = nullptr;
+    chunks = nullptr;
     return status_of(e);
   }
 };
@@ -183,7 +191,7 @@ flr::StepArgs step_args(const fl_layout* lay) {
 // Enqueue one fused local step (and, with seg_sumsq, its per-segment sums).
 int enqueue_local_step(const fl_layout* lay, const fl_adamw_hparams& h, int64_t step, int R,
                        const uint16_t* const* peers, float grad_scale, float* master, float* m,
-                       float* v, uint16_t* working, float* partials, float* seg_sumsq,
+                       float* v, uint16_t* working, const Workspace& ws, float* seg_sumsq,
                        hipStream_t st) {
   flr::StepArgs a = step_args(lay);
   for (int r = 0; r < R; ++r) a.grads[r] = peers[r];
@@ -194,9 +202,10 @@ int enqueue_local_step(const fl_layout* lay, const fl_adamw_hparams& h, int64_t 
   a.m = m;
   a.v = v;
   a.working = working;
-  a.partials = seg_sumsq ? partials : nullptr;
+  a.partials = seg_sumsq ? ws.p : nullptr;
   int rc = status_of(flr::launch_local_step(a, grid_for(lay, lay->L.n_tiles), st));
-  if (rc == FL_OK && seg_sumsq) rc = status_of(flr::launch_seg_finalize(lay->L, partials, seg_sumsq, st));
+  if (rc == FL_OK && seg_sumsq)
+    rc = status_of(flr::launch_seg_finalize(lay->L, ws.p, ws.chunks, seg_sumsq, st));
   return rc;
 }
 
@@ -277,6 +286,17 @@ int fl_layout_create(int64_t n, int64_t n_seg, const int64_t* seg_offsets,
     pieces += ti.nseg;
   }
   seg_piece0[(size_t)n_seg] = pieces;
+  // Finalize chunks: each segment's pieces in runs of at most kChunkPieces.
+  std::vector<int64_t> chunk_p0;
+  std::vector<int64_t> seg_chunk0((size_t)n_seg + 1, 0);
+  for (int64_t k = 0; k < n_seg; ++k) {
+    seg_chunk0[(size_t)k] = (int64_t)chunk_p0.size();
+    for (int64_t p = seg_piece0[(size_t)k]; p < seg_piece0[(size_t)k + 1]; p += flr::kChunkPieces)
+      chunk_p0.push_back(p);
+  }
+  const int64_t n_chunks = (int64_t)chunk_p0.size();
+  seg_chunk0[(size_t)n_seg] = n_chunks;
+  chunk_p0.push_back(pieces);
   std::vector<uint8_t> decay((size_t)n_seg);
   for (int64_t k = 0; k < n_seg; ++k) decay[(size_t)k] = (seg_decay == nullptr || seg_decay[k]) ? 1 : 0;
 
@@ -299,13 +319,17 @@ int fl_layout_create(int64_t n, int64_t n_seg, const int64_t* seg_offsets,
   lay->L.n_seg = n_seg;
   lay->L.n_tiles = n_tiles;
   lay->L.n_pieces = pieces;
+  lay->L.n_chunks = n_chunks;
 
-  // One device allocation: [seg_off | seg_piece0 | tiles | seg_decay].
+  // One device allocation:
+  // [seg_off | seg_piece0 | seg_chunk0 | chunk_p0 | tiles | seg_decay].
   const size_t b_off = sizeof(int64_t) * (size_t)(n_seg + 1);
   const size_t b_pp = sizeof(int64_t) * (size_t)(n_seg + 1);
+  const size_t b_sc = sizeof(int64_t) * (size_t)(n_seg + 1);
+  const size_t b_cp = sizeof(int64_t) * (size_t)(n_chunks + 1);
   const size_t b_tiles = sizeof(flr::TileInfo) * (size_t)n_tiles;
   const size_t b_dec = (size_t)n_seg;
-  const size_t total = b_off + b_pp + b_tiles + b_dec + 64;
+  const size_t total = b_off + b_pp + b_sc + b_cp + b_tiles + b_dec + 64;
   void* mem = nullptr;
   hipError_t e = hipMalloc(&mem, total);
   if (e != hipSuccess) {
@@ -313,22 +337,30 @@ int fl_layout_create(int64_t n, int64_t n_seg, const int64_t* seg_offsets,
     return status_of(e);
   }
   char* base = static_cast<char*>(mem);
-  e = hipMemcpy(base, seg_offsets, b_off, hipMemcpyHostToDevice);
-  if (e == hipSuccess) e = hipMemcpy(base + b_off, seg_piece0.data(), b_pp, hipMemcpyHostToDevice);
-  if (e == hipSuccess && b_tiles)
-    e = hipMemcpy(base + b_off + b_pp, tiles.data(), b_tiles, hipMemcpyHostToDevice);
-  if (e == hipSuccess && b_dec)
-    e = hipMemcpy(base + b_off + b_pp + b_tiles, decay.data(), b_dec, hipMemcpyHostToDevice);
+  char* p_off = base;
+  char* p_pp = p_off + b_off;
+  char* p_sc = p_pp + b_pp;
+  char* p_cp = p_sc + b_sc;
+  char* p_tiles = p_cp + b_cp;
+  char* p_dec = p_tiles + b_tiles;
+  e = hipMemcpy(p_off, seg_offsets, b_off, hipMemcpyHostToDevice);
+  if (e == hipSuccess) e = hipMemcpy(p_pp, seg_piece0.data(), b_pp, hipMemcpyHostToDevice);
+  if (e == hipSuccess) e = hipMemcpy(p_sc, seg_chunk0.data(), b_sc, hipMemcpyHostToDevice);
+  if (e == hipSuccess) e = hipMemcpy(p_cp, chunk_p0.data(), b_cp, hipMemcpyHostToDevice);
+  if (e == hipSuccess && b_tiles) e = hipMemcpy(p_tiles, tiles.data(), b_tiles, hipMemcpyHostToDevice);
+  if (e == hipSuccess && b_dec) e = hipMemcpy(p_dec, decay.data(), b_dec, hipMemcpyHostToDevice);
   if (e != hipSuccess) {
     (void)hipFree(mem);
     delete lay;
     return status_of(e);
   }
   lay->dev_mem = mem;
-  lay->L.seg_off = reinterpret_cast<const int64_t*>(base);
-  lay->L.seg_piece0 = reinterpret_cast<const int64_t*>(base + b_off);
-  lay->L.tiles = reinterpret_cast<const flr::TileInfo*>(base + b_off + b_pp);
-  lay->L.seg_decay = reinterpret_cast<const uint8_t*>(base + b_off + b_pp + b_tiles);
+  lay->L.seg_off = reinterpret_cast<const int64_t*>(p_off);
+  lay->L.seg_piece0 = reinterpret_cast<const int64_t*>(p_pp);
+  lay->L.seg_chunk0 = reinterpret_cast<const int64_t*>(p_sc);
+  lay->L.chunk_p0 = reinterpret_cast<const int64_t*>(p_cp);
+  lay->L.tiles = reinterpret_cast<const flr::TileInfo*>(p_tiles);
+  lay->L.seg_decay = reinterpret_cast<const uint8_t*>(p_dec);
   *out = lay;
   return FL_OK;
 }
@@ -368,7 +400,7 @@ int fl_shard_reduce(const fl_layout* layout, int R, const uint16_t* const* peer_
   if (n == 0) return FL_OK;
   hipStream_t st = static_cast<hipStream_t>(stream);
   Workspace ws;
-  if (seg_sumsq && (rc = ws.alloc(layout->L.n_pieces, st)) != FL_OK) return rc;
+  if (seg_sumsq && (rc = ws.alloc(layout->L, st)) != FL_OK) return rc;
   flr::StepArgs a = step_args(layout);
   for (int r = 0; r < R; ++r) a.grads[r] = peer_grads[r];
   a.R = R;
@@ -376,7 +408,8 @@ int fl_shard_reduce(const fl_layout* layout, int R, const uint16_t* const* peer_
   a.g_out = grad_out;
   a.partials = ws.p;
   rc = status_of(flr::launch_reduce(a, grid_for(layout, layout->L.n_tiles), st));
-  if (rc == FL_OK && seg_sumsq) rc = status_of(flr::launch_seg_finalize(layout->L, ws.p, seg_sumsq, st));
+  if (rc == FL_OK && seg_sumsq)
+    rc = status_of(flr::launch_seg_finalize(layout->L, ws.p, ws.chunks, seg_sumsq, st));
   const int rc2 = ws.release();
   return rc != FL_OK ? rc : rc2;
 }
@@ -423,9 +456,9 @@ int fl_local_step(const fl_layout* layout, const fl_adamw_hparams* h, int64_t st
   if (n == 0) return FL_OK;
   hipStream_t st = static_cast<hipStream_t>(stream);
   Workspace ws;
-  if (seg_sumsq && (rc = ws.alloc(layout->L.n_pieces, st)) != FL_OK) return rc;
-  rc = enqueue_local_step(layout, *h, step, R, peer_grads, grad_scale, master, m, v, working,
-                          ws.p, seg_sumsq, st);
+  if (seg_sumsq && (rc = ws.alloc(layout->L, st)) != FL_OK) return rc;
+  rc = enqueue_local_step(layout, *h, step, R, peer_grads, grad_scale, master, m, v, working, ws,
+                          seg_sumsq, st);
   const int rc2 = ws.release();
   return rc != FL_OK ? rc : rc2;
 }
@@ -497,12 +530,12 @@ int fl_round(const fl_layout* layout, const fl_round_cfg* cfg, const uint16_t* c
     return status_of(hipEventRecord(static_cast<hipEvent_t>(c.phase_events[k]), st));
   };
   Workspace ws;
-  if (n > 0 && seg_sumsq && (rc = ws.alloc(layout->L.n_pieces, st)) != FL_OK) return rc;
+  if (n > 0 && seg_sumsq && (rc = ws.alloc(layout->L, st)) != FL_OK) return rc;
   for (int a = 0; a < c.A && rc == FL_OK; ++a) {
     rc = record(a);
     if (rc == FL_OK && n > 0)
       rc = enqueue_local_step(layout, c.h, c.step0 + a, c.R, grads + (size_t)a * (size_t)c.R,
-                              c.grad_scale, master, m, v, working, ws.p,
+                              c.grad_scale, master, m, v, working, ws,
                               seg_sumsq ? seg_sumsq + (size_t)a * (size_t)layout->L.n_seg : nullptr,
                               st);
   }

@@ -13,9 +13,11 @@
 //     correctly rounded operation at a time (the file is built with
 //     -ffp-contract=off), so results are bitwise those of the definition and
 //     do not depend on the grid;
-//   * per-segment sums of squares use wave64 butterfly reductions and a
-//     4-entry LDS exchange per workgroup; only tiles that straddle a segment
-//     boundary (rare) resolve segments per element.
+//   * per-segment sums of squares use wave64 butterfly reductions only: each
+//     wave writes one fp32 partial per (tile, segment) piece it covers, with
+//     no workgroup barrier in the streaming loop, and a small two-stage
+//     finalize folds the partials per segment in double; only tiles that straddle a
+//     segment boundary (rare) resolve segments per element.
 #include "flr_internal.h"
 
 namespace flr {
@@ -158,18 +160,12 @@ __device__ __forceinline__ void reduce_tail(const StepArgs& a, int64_t base, int
   }
 }
 
-// Fixed-tree sum over the workgroup: wave64 butterfly (every lane ends with
-// the same bits), then the four wave totals in order.
-__device__ __forceinline__ float block_sum(float v, float* red) {
+// Fixed-tree sum over one wave64: butterfly exchange, after which every lane
+// holds the same bits (each step adds the same two partials in both lanes).
+__device__ __forceinline__ float wave_sum(float v) {
 #pragma unroll
   for (int off = 32; off >= 1; off >>= 1) v = v + __shfl_xor(v, off, 64);
-  const int lane = threadIdx.x & 63;
-  const int wid = threadIdx.x >> 6;
-  if (lane == 0) red[wid] = v;
-  __syncthreads();
-  const float r = ((red[0] + red[1]) + red[2]) + red[3];
-  __syncthreads();
-  return r;
+  return v;
 }
 
 // Segment of element `i`, searching [lo, hi] (segments overlapping the tile).
@@ -185,7 +181,6 @@ __device__ __forceinline__ int find_seg(const int64_t* off, int lo, int hi, int6
 // 2: AdamW only (g_in).  SUMSQ: per-piece sums of squares of g.
 template <int RT, int MODE, bool SUMSQ>
 __global__ void __launch_bounds__(kBlock) k_step(const StepArgs a) {
-  __shared__ float red[4];
   const int tid = threadIdx.x;
   for (int64_t t = blockIdx.x; t < a.L.n_tiles; t += gridDim.x) {
     const TileInfo ti = a.L.tiles[t];
@@ -273,20 +268,23 @@ __global__ void __launch_bounds__(kBlock) k_step(const StepArgs a) {
     }
 
     if constexpr (SUMSQ) {
+      // One partial per (piece, wave): the wave's share of the piece, summed
+      // in fp32 (8 elements in order, then the wave butterfly); no barrier.
+      const int wid = tid >> 6;
       if (ti.nseg == 1) {
         float acc = 0.f;
 #pragma unroll
         for (int e = 0; e < 8; ++e) if (e < cnt) acc = acc + g[e] * g[e];
-        const float tot = block_sum(acc, red);
-        if (tid == 0) a.partials[ti.piece0] = tot;
+        const float tot = wave_sum(acc);
+        if ((tid & 63) == 0) a.partials[(int64_t)ti.piece0 * kWaves + wid] = tot;
       } else {
         for (int j = 0; j < ti.nseg; ++j) {
           const int sj = ti.seg0 + j;
           float acc = 0.f;
 #pragma unroll
           for (int e = 0; e < 8; ++e) if (e < cnt && seg[e] == sj) acc = acc + g[e] * g[e];
-          const float tot = block_sum(acc, red);
-          if (tid == 0) a.partials[ti.piece0 + j] = tot;
+          const float tot = wave_sum(acc);
+          if ((tid & 63) == 0) a.partials[((int64_t)ti.piece0 + j) * kWaves + wid] = tot;
         }
       }
     }
@@ -339,22 +337,42 @@ __global__ void __launch_bounds__(kBlock) k_fedavg(const FedArgs a) {
   }
 }
 
-// Per-segment total of the piece partials, in double, fixed order: thread j
-// sums pieces j, j+256, ...; then a wave64 butterfly and the 4 wave totals.
-__global__ void __launch_bounds__(kBlock) k_seg_finalize(const LayoutDev L, const float* partials,
-                                                         float* out) {
+// Per-segment totals of the (piece, wave) partials, in double, in two fixed
+// trees that do not depend on the grid.  Stage 1: one workgroup per chunk of
+// up to kChunkPieces pieces of one segment; thread j folds pieces j, j+256,
+// ... (each piece's kWaves slots in order), then a wave64 butterfly and the 4
+// wave totals in order.  Stage 2: one thread per segment adds its chunks in
+// order.
+__global__ void __launch_bounds__(kBlock) k_seg_chunks(const LayoutDev L, const float* partials,
+                                                       double* chunk_sums) {
   __shared__ double red[4];
-  for (int64_t s = blockIdx.x; s < L.n_seg; s += gridDim.x) {
-    const int64_t p0 = L.seg_piece0[s];
-    const int64_t p1 = L.seg_piece0[s + 1];
+  for (int64_t c = blockIdx.x; c < L.n_chunks; c += gridDim.x) {
+    const int64_t p0 = L.chunk_p0[c];
+    const int64_t p1 = L.chunk_p0[c + 1];
     double acc = 0.0;
-    for (int64_t p = p0 + threadIdx.x; p < p1; p += kBlock) acc = acc + (double)partials[p];
+    for (int64_t p = p0 + threadIdx.x; p < p1; p += kBlock) {
+      const f32x4 w = *reinterpret_cast<const f32x4*>(partials + p * kWaves);
+      acc = acc + (double)w.x;
+      acc = acc + (double)w.y;
+      acc = acc + (double)w.z;
+      acc = acc + (double)w.w;
+    }
 #pragma unroll
     for (int off = 32; off >= 1; off >>= 1) acc = acc + __shfl_xor(acc, off, 64);
     if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = acc;
     __syncthreads();
-    if (threadIdx.x == 0) out[s] = (float)(((red[0] + red[1]) + red[2]) + red[3]);
+    if (threadIdx.x == 0) chunk_sums[c] = ((red[0] + red[1]) + red[2]) + red[3];
     __syncthreads();
+  }
+}
+
+__global__ void __launch_bounds__(kBlock) k_seg_totals(const LayoutDev L, const double* chunk_sums,
+                                                       float* out) {
+  const int64_t stride = (int64_t)gridDim.x * kBlock;
+  for (int64_t s = (int64_t)blockIdx.x * kBlock + threadIdx.x; s < L.n_seg; s += stride) {
+    double acc = 0.0;
+    for (int64_t c = L.seg_chunk0[s]; c < L.seg_chunk0[s + 1]; ++c) acc = acc + chunk_sums[c];
+    out[s] = (float)acc;
   }
 }
 
@@ -401,13 +419,18 @@ hipError_t launch_fedavg(const FedArgs& a, int grid, hipStream_t st) {
   }
 }
 
-hipError_t launch_seg_finalize(const LayoutDev& L, const float* partials, float* out,
-                               hipStream_t st) {
+hipError_t launch_seg_finalize(const LayoutDev& L, const float* partials, double* chunk_sums,
+                               float* out, hipStream_t st) {
   if (L.n_seg == 0) return hipSuccess;
-  const int grid = (int)(L.n_seg < 65535 ? L.n_seg : 65535);
-  void* args[] = {const_cast<LayoutDev*>(&L), &partials, &out};
-  return hipLaunchKernel((const void*)k_seg_finalize, dim3((unsigned)grid), dim3(kBlock), args, 0,
-                         st);
+  const int g1 = (int)(L.n_chunks < 65535 ? L.n_chunks : 65535);
+  void* a1[] = {const_cast<LayoutDev*>(&L), &partials, &chunk_sums};
+  hipError_t e = hipLaunchKernel((const void*)k_seg_chunks, dim3((unsigned)g1), dim3(kBlock), a1,
+                                 0, st);
+  if (e != hipSuccess) return e;
+  const int64_t b2 = (L.n_seg + kBlock - 1) / kBlock;
+  const int g2 = (int)(b2 < 65535 ? b2 : 65535);
+  void* a2[] = {const_cast<LayoutDev*>(&L), &chunk_sums, &out};
+  return hipLaunchKernel((const void*)k_seg_totals, dim3((unsigned)g2), dim3(kBlock), a2, 0, st);
 }
 
 }  // namespace flr
