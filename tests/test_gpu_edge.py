@@ -1,0 +1,145 @@
+"""GPU edge cases beyond the main parity suite: segment structures that stress
+the straddling-tile path, optimiser and weight edge values, two streams
+sharing one layout, and capture of fl_round in a HIP graph."""
+import numpy as np
+import pytest
+
+import harness as H
+import synth.buffers as B
+from synth import workloads as W
+
+pytestmark = pytest.mark.gpu
+
+
+def _say(*a):
+    print("[gpu-edge]", *a, flush=True)
+
+
+@pytest.fixture(scope="module")
+def env():
+    import torch
+
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import oracle
+    import paper_2609_20359_amd as P
+
+    P.lib()
+    return dict(torch=torch, P=P, orc=oracle.Oracle())
+
+
+def _state(dev):
+    return dict(master=dev.master.cpu().numpy(), m=dev.m.cpu().numpy(), v=dev.v.cpu().numpy(),
+                working=H.to_u16(dev.working))
+
+
+def _parity(env, w, tag):
+    torch, P, orc = env["torch"], env["P"], env["orc"]
+    _say(tag, w.describe())
+    lay = P.Layout(w.seg_offsets, w.seg_decay)
+    dev = B.DeviceInputs(w)
+    ss = torch.full((w.A * w.n_seg,), -1.0, dtype=torch.float32, device="cuda")
+    H.gpu_round(P, lay, w, dev, seg_sumsq=ss)
+    torch.cuda.synchronize()
+    host = B.HostInputs(w)
+    ss_ref = H.oracle_round(orc, w, host, want_sumsq=True)
+    H.assert_state_parity(tag, _state(dev), dict(master=host.master, m=host.m, v=host.v,
+                                                 working=host.working), bitwise=True)
+    H.assert_sumsq(tag, ss.cpu().numpy(), ss_ref.reshape(-1))
+    lay.close()
+
+
+def test_tiles_with_many_segments(env):
+    """Runs of one-element and tiny segments, so single 2048-element tiles
+    hold hundreds of segments, between large ones."""
+    sizes = [5000] + [1] * 700 + [3, 2, 1] * 100 + [4096, 1, 2047, 2049] + [7] * 300 + [10000]
+    r = np.random.default_rng(21)
+    flags = r.integers(0, 2, len(sizes)).astype(np.uint8)
+    w = W.make_workload("many_segments", sizes, flags, R=3, G=2, A=2)
+    _parity(env, w, "many_segments")
+
+
+@pytest.mark.parametrize("hp,step0", [
+    (dict(lr=3e-4, beta1=0.0, beta2=0.0, eps=1e-8, weight_decay=0.1), 1),
+    (dict(lr=3e-4, beta1=0.9, beta2=0.95, eps=1e-8, weight_decay=0.0), 1_000_000),
+    (dict(lr=0.5, beta1=0.99, beta2=0.999, eps=1e-3, weight_decay=1.5), 2),
+    (dict(lr=0.0, beta1=0.9, beta2=0.95, eps=1e-8, weight_decay=0.1), 7),
+])
+def test_optimiser_edge_values(env, hp, step0):
+    r = np.random.default_rng(22)
+    sizes = r.integers(1, 30000, 10)
+    flags = r.integers(0, 2, sizes.size).astype(np.uint8)
+    w = W.make_workload("hp_edges", sizes, flags, R=2, G=3, A=2, hp=hp, step0=step0,
+                        weights=np.array([0.0, 2.0, 0.0], np.float32), self_group=1)
+    _parity(env, w, "hp %s step0 %d" % (hp, step0))
+
+
+def test_two_streams_share_a_layout(env):
+    """Two rounds on two streams at once, one layout, each with its own
+    per-segment temporary; both match the oracle."""
+    torch, P, orc = env["torch"], env["P"], env["orc"]
+    r = np.random.default_rng(23)
+    sizes = r.integers(1, 200000, 30)
+    flags = r.integers(0, 2, sizes.size).astype(np.uint8)
+    wa = W.make_workload("stream_a", sizes, flags, R=4, G=2, A=3, seed=1)
+    wb = W.make_workload("stream_b", sizes, flags, R=4, G=2, A=3, seed=2)
+    lay = P.Layout(wa.seg_offsets, wa.seg_decay)
+    da, db = B.DeviceInputs(wa), B.DeviceInputs(wb)
+    torch.cuda.synchronize()
+    sa, sb = torch.cuda.Stream(), torch.cuda.Stream()
+    ssa = torch.empty(wa.A * wa.n_seg, dtype=torch.float32, device="cuda")
+    ssb = torch.empty(wb.A * wb.n_seg, dtype=torch.float32, device="cuda")
+    with torch.cuda.stream(sa):
+        H.gpu_round(P, lay, wa, da, seg_sumsq=ssa)
+    with torch.cuda.stream(sb):
+        H.gpu_round(P, lay, wb, db, seg_sumsq=ssb)
+    torch.cuda.synchronize()
+    for w, d, ss in ((wa, da, ssa), (wb, db, ssb)):
+        host = B.HostInputs(w)
+        ref = H.oracle_round(orc, w, host, want_sumsq=True)
+        H.assert_state_parity(w.name, _state(d), dict(master=host.master, m=host.m, v=host.v,
+                                                      working=host.working), bitwise=True)
+        H.assert_sumsq(w.name, ss.cpu().numpy(), ref.reshape(-1))
+    lay.close()
+
+
+def test_round_captured_in_a_hip_graph(env):
+    """fl_round (without per-segment sums it allocates nothing) captured once
+    and replayed three times, with eager work and synchronisation between
+    replays; every replay equals the eager result of the same round."""
+    torch, P = env["torch"], env["P"]
+    r = np.random.default_rng(24)
+    sizes = r.integers(1, 60000, 12)
+    flags = r.integers(0, 2, sizes.size).astype(np.uint8)
+    w = W.make_workload("graph", sizes, flags, R=4, G=3, A=2)
+    lay = P.Layout(w.seg_offsets, w.seg_decay)
+    eager = B.DeviceInputs(w)
+    graphed = B.DeviceInputs(w)
+    cfg = P.make_round_cfg(w.R, w.G, w.A, w.weights, w.hp, self_group=w.self_group,
+                           grad_scale=w.grad_scale, step0=w.step0)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    # the capture records the same kernel launches; it does not run them
+    snapshot = [t.clone() for t in (graphed.master, graphed.m, graphed.v, graphed.working)]
+    with torch.cuda.graph(g, stream=s):
+        P.fl_round(lay, cfg, graphed.grads, graphed.replicas, graphed.master, graphed.m,
+                   graphed.v, graphed.working)
+    torch.cuda.synchronize()
+    for t, snap in zip((graphed.master, graphed.m, graphed.v, graphed.working), snapshot):
+        assert torch.equal(t.view(torch.int16), snap.view(torch.int16)), "capture ran kernels"
+    for rep in range(3):
+        P.fl_round(lay, cfg, eager.grads, eager.replicas, eager.master, eager.m, eager.v,
+                   eager.working)
+        junk = torch.randn(1 << 20, device="cuda").sum()  # unrelated eager work
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        for name in ("master", "m", "v", "working"):
+            a = getattr(eager, name)
+            b = getattr(graphed, name)
+            assert torch.equal(a.view(torch.int16), b.view(torch.int16)), \
+                "replay %d differs in %s" % (rep, name)
+        del junk
+    lay.close()
