@@ -35,6 +35,13 @@ def _declare(lib):
     lib.orc_round.argtypes = [ctypes.c_int64, _P, _P, ctypes.c_int, ctypes.c_int, ctypes.c_int,
                               ctypes.c_int, ctypes.c_float, ctypes.POINTER(Hparams),
                               ctypes.c_int64, _P, _P, _P, _P, _P, _P, _P, _P]
+    lib.orc_shard_reduce_wire.argtypes = [ctypes.c_int64, ctypes.c_int, _P, ctypes.c_float, _P]
+    lib.orc_broadcast_recv.argtypes = [ctypes.c_int64, _P, _P, _P]
+    lib.orc_round_hsdp.argtypes = [ctypes.c_int64, _P, _P, ctypes.c_int, ctypes.c_int,
+                                   ctypes.c_int, ctypes.c_float, ctypes.c_int, ctypes.c_int,
+                                   ctypes.c_int, ctypes.c_int, ctypes.c_float,
+                                   ctypes.POINTER(Hparams), ctypes.c_int64, _P, _P, _P, _P, _P,
+                                   _P, _P, _P, _P, _P]
     return lib
 
 
@@ -130,6 +137,53 @@ class Oracle:
         if rc:
             raise ValueError("orc_fedavg: %d" % rc)
         return master_out, working_out
+
+    def shard_reduce_wire(self, grads, grad_scale):
+        grads = [_c(g, np.uint16) for g in grads]
+        n = grads[0].size
+        out = np.empty(n, np.uint16)
+        rc = self.L.orc_shard_reduce_wire(n, len(grads), _ptr_array(grads), grad_scale,
+                                          out.ctypes.data)
+        if rc:
+            raise ValueError("orc_shard_reduce_wire: %d" % rc)
+        return out
+
+    def broadcast_recv(self, recv, master, working):
+        recv = _c(recv, np.float32)
+        rc = self.L.orc_broadcast_recv(recv.size, recv.ctypes.data, master.ctypes.data,
+                                       working.ctypes.data)
+        if rc:
+            raise ValueError("orc_broadcast_recv: %d" % rc)
+
+    def round_hsdp(self, seg_off, seg_decay, R, H, replica, hsdp_scale, member, G, A,
+                   self_group, grad_scale, hp, step0, weights, grads, replica_wires, replicas,
+                   bcast, master, m, v, working, want_sumsq=False):
+        """One FL+HSDP round in place.  replica_wires: A*H arrays (entry
+        a*H + replica ignored, may be None); replicas: G arrays or None
+        (member only); bcast: fp32 array (non-member only)."""
+        seg_off = _c(seg_off, np.int64)
+        seg_decay = _c(seg_decay, np.uint8)
+        n_seg = seg_off.size - 1
+        n = int(seg_off[-1])
+        dummy = np.zeros(max(n, 1), np.uint16)
+        grads = [_c(g, np.uint16) for g in grads]
+        wires = [dummy if x is None else _c(x, np.uint16) for x in (replica_wires or [])]
+        reps = [working if x is None else _c(x, np.uint16) for x in (replicas or [])]
+        w = _c(weights if weights is not None else [1.0], np.float32)
+        bc = None if bcast is None else _c(bcast, np.float32)
+        h = hparams(hp)
+        ss = np.empty(A * n_seg, np.float64) if want_sumsq else None
+        rc = self.L.orc_round_hsdp(n_seg, seg_off.ctypes.data, seg_decay.ctypes.data, R, H, replica,
+                                   hsdp_scale, 1 if member else 0, G, A, self_group, grad_scale,
+                                   ctypes.byref(h), step0, w.ctypes.data, _ptr_array(grads),
+                                   _ptr_array(wires) if wires else None,
+                                   _ptr_array(reps) if reps else None,
+                                   None if bc is None else bc.ctypes.data, master.ctypes.data,
+                                   m.ctypes.data, v.ctypes.data, working.ctypes.data,
+                                   None if ss is None else ss.ctypes.data)
+        if rc:
+            raise ValueError("orc_round_hsdp: %d" % rc)
+        return None if ss is None else ss.reshape(A, n_seg)
 
     def round(self, seg_off, seg_decay, R, G, A, self_group, grad_scale, hp, step0, weights,
               grads, replicas, master, m, v, working, want_sumsq=False):

@@ -153,6 +153,75 @@ int orc_round(int64_t n_seg, const int64_t* seg_off, const uint8_t* seg_decay, i
   return rc;
 }
 
+int orc_shard_reduce_wire(int64_t n, int R, const uint16_t* const* grads, float grad_scale,
+                          uint16_t* wire) {
+  if (n < 0 || R < 1 || (n > 0 && (!grads || !wire))) return -1;
+  for (int64_t i = 0; i < n; ++i) {
+    float acc = 0.0f;
+    for (int r = 0; r < R; ++r) acc = acc + orc_bf16_to_f32(grads[r][i]);
+    wire[i] = orc_f32_to_bf16(acc * grad_scale);
+  }
+  return 0;
+}
+
+int orc_broadcast_recv(int64_t n, const float* recv, float* master, uint16_t* working) {
+  if (n < 0 || (n > 0 && (!recv || !master || !working))) return -1;
+  for (int64_t i = 0; i < n; ++i) {
+    master[i] = recv[i];
+    working[i] = orc_f32_to_bf16(recv[i]);
+  }
+  return 0;
+}
+
+int orc_round_hsdp(int64_t n_seg, const int64_t* seg_off, const uint8_t* seg_decay, int R, int H,
+                   int replica, float hsdp_scale, int member, int G, int A, int self_group,
+                   float grad_scale, const orc_hparams* h, int64_t step0, const float* weights,
+                   const uint16_t* const* grads, const uint16_t* const* replica_wires,
+                   const uint16_t* const* replicas, const float* bcast, float* master, float* m,
+                   float* v, uint16_t* working, double* seg_sumsq) {
+  if (n_seg < 0 || !seg_off || R < 1 || H < 1 || replica < 0 || replica >= H || A < 1 ||
+      !h || step0 < 1 || !grads)
+    return -1;
+  if (H > 1 && !replica_wires) return -1;
+  if (member && (G < 1 || self_group < 0 || self_group >= G || !weights || !replicas)) return -1;
+  if (!member && !bcast && seg_off[n_seg] > 0) return -1;
+  const int64_t n = seg_off[n_seg];
+  if (n > 0 && (!master || !m || !v || !working)) return -1;
+  float* g = (float*)malloc(sizeof(float) * (size_t)(n > 0 ? n : 1));
+  uint16_t* wire = (uint16_t*)malloc(sizeof(uint16_t) * (size_t)(n > 0 ? n : 1));
+  const uint16_t** wires = (const uint16_t**)malloc(sizeof(uint16_t*) * (size_t)H);
+  const uint16_t** reps = (const uint16_t**)malloc(sizeof(uint16_t*) * (size_t)(G > 0 ? G : 1));
+  int rc = (g && wire && wires && reps) ? 0 : -1;
+  for (int a = 0; a < A && rc == 0; ++a) {
+    const uint16_t* const* ga = grads + (size_t)a * (size_t)R;
+    if (H == 1) {
+      rc = orc_shard_reduce(n, R, ga, grad_scale, g);
+    } else {
+      rc = orc_shard_reduce_wire(n, R, ga, grad_scale, wire);
+      for (int k = 0; k < H; ++k)
+        wires[k] = (k == replica) ? wire : replica_wires[(size_t)a * (size_t)H + (size_t)k];
+      if (rc == 0) rc = orc_shard_reduce(n, H, wires, hsdp_scale, g);
+    }
+    if (rc == 0 && seg_sumsq)
+      rc = orc_seg_sumsq(n_seg, seg_off, g, seg_sumsq + (size_t)a * (size_t)n_seg);
+    if (rc == 0)
+      rc = orc_adamw_step(n_seg, seg_off, seg_decay, h, step0 + a, g, master, m, v, working);
+  }
+  if (rc == 0) {
+    if (member) {
+      for (int k = 0; k < G; ++k) reps[k] = (k == self_group) ? working : replicas[k];
+      rc = orc_fedavg(n, G, reps, weights, master, working);
+    } else {
+      rc = orc_broadcast_recv(n, bcast, master, working);
+    }
+  }
+  free(g);
+  free(wire);
+  free(wires);
+  free(reps);
+  return rc;
+}
+
 /* Array forms of the two conversions, for the tests. */
 void orc_f32_to_bf16_array(int64_t n, const float* x, uint16_t* out) {
   for (int64_t i = 0; i < n; ++i) out[i] = orc_f32_to_bf16(x[i]);

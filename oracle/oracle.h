@@ -43,6 +43,18 @@
  *  (a5) per-segment sum of squares of g for each local step, accumulated in
  *       double in index order.
  *
+ * FL+HSDP (Section 2, HSDP; Section 4.1, Eq. (2); Section 4.2, Eq. (5)): the
+ * gradient is averaged in two tiers (Section 5.1), first over the sharding
+ * group, then over the H replicas of the replication group, whose all-reduce
+ * carries bf16 shards:
+ *  (n1) wire[i] = bf16_rne(g1[i]), g1 from (a1) over the sharding group;
+ *       g[i] = hsdp_scale * sum_{h=0..H-1} f32(wire_h[i]), h ascending, the own
+ *       replica's wire at its index; with H = 1 the second tier is skipped
+ *       and g = g1 (HSDP with one replica is FSDP).
+ *  (n2) after FedAvg among one replica per group, that replica broadcasts its
+ *       fp32 master shard to the others of its group: master = received,
+ *       working = bf16_rne(received).
+ *
  * Every fp32 operation above is one IEEE-754 binary32 operation rounded to
  * nearest even, evaluated in the written order; the file is compiled with
  * -ffp-contract=off and without fast-math, and subnormals are kept.
@@ -90,6 +102,26 @@ int orc_round(int64_t n_seg, const int64_t* seg_off, const uint8_t* seg_decay, i
               const float* weights, const uint16_t* const* grads,
               const uint16_t* const* replicas, float* master, float* m, float* v,
               uint16_t* working, double* seg_sumsq);
+
+/* (n1) tier 1 to the bf16 wire format. */
+int orc_shard_reduce_wire(int64_t n, int R, const uint16_t* const* grads, float grad_scale,
+                          uint16_t* wire);
+
+/* (n2) receive side of the intra-group broadcast. */
+int orc_broadcast_recv(int64_t n, const float* recv, float* master, uint16_t* working);
+
+/* One FL+HSDP round on one replica.  grads: A*R sharding-peer arrays;
+ * replica_wires: A*H arrays of the other replicas' tier-1 wire shards
+ * (entry a*H + replica ignored); member != 0: this replica takes part in
+ * FedAvg with the G replicas (entry self_group ignored); member == 0: it
+ * receives bcast (fp32) instead.  seg_sumsq: NULL or A*n_seg (of the
+ * tier-2 gradient). */
+int orc_round_hsdp(int64_t n_seg, const int64_t* seg_off, const uint8_t* seg_decay, int R, int H,
+                   int replica, float hsdp_scale, int member, int G, int A, int self_group,
+                   float grad_scale, const orc_hparams* h, int64_t step0, const float* weights,
+                   const uint16_t* const* grads, const uint16_t* const* replica_wires,
+                   const uint16_t* const* replicas, const float* bcast, float* master, float* m,
+                   float* v, uint16_t* working, double* seg_sumsq);
 
 #ifdef __cplusplus
 }

@@ -388,12 +388,9 @@ def pin_golden_hand_cases(orc):
 
 # ---- (a4) whole rounds: float64 brute force with error bounds ---------------
 
-def brute_force_round(hp, seg_off, seg_decay, R, G, A, self_group, grad_scale, step0, weights,
-                      grads, replicas, p0, m0, v0, oracle_working_after_steps=None):
-    """Straight-line float64 recomputation of one round, with a propagated
-    bound on the distance of any binary32 evaluation in the fixed order from
-    the exact result.  Returns dict of (value, bound) plus the per-step g and
-    its bound, and the masks of elements whose bf16 rounding is ambiguous."""
+def _bf_steps(hp, seg_off, seg_decay, step0, gsteps, p0, m0, v0):
+    """float64 AdamW over the given per-step (g, bound on |fp32 g - g|) with
+    propagated bounds on the distance of the binary32 evaluation."""
     h = _hp_f(hp)
     b1, b2, lr, wd, eps = h["beta1"], h["beta2"], h["lr"], h["weight_decay"], h["eps"]
     n = int(seg_off[-1])
@@ -401,7 +398,6 @@ def brute_force_round(hp, seg_off, seg_decay, R, G, A, self_group, grad_scale, s
     for s in range(len(seg_off) - 1):
         decay_flag[seg_off[s]:seg_off[s + 1]] = bool(seg_decay[s])
     decay = np.where(decay_flag, 1.0 - lr * wd, 1.0)
-    s_scale = float(np.float32(grad_scale))
     p = p0.astype(np.float64).copy()
     m = m0.astype(np.float64).copy()
     v = v0.astype(np.float64).copy()
@@ -409,13 +405,8 @@ def brute_force_round(hp, seg_off, seg_decay, R, G, A, self_group, grad_scale, s
     em = np.zeros(n)
     ev = np.zeros(n)
     mabs = np.abs(m)
-    gsteps = []
-    for a in range(A):
+    for a, (g, eg) in enumerate(gsteps):
         t = step0 + a
-        dec = np.stack([bf16_decode(grads[a * R + r]) for r in range(R)])
-        g = dec.sum(0) * s_scale
-        eg = (R + 1) * U * np.abs(dec).sum(0) * abs(s_scale)
-        gsteps.append((g, eg))
         gab = np.abs(g) + eg
         mabs = b1 * mabs + (1 - b1) * gab
         m = b1 * m + (1 - b1) * g
@@ -438,20 +429,58 @@ def brute_force_round(hp, seg_off, seg_decay, R, G, A, self_group, grad_scale, s
         ep = decay * ep + 2 * U * (np.abs(pd) + ep)
         p = pd - upd
         ep = ep + eupd + U * (np.abs(p) + ep)
-    ep, em, ev = 2 * ep + TINY, 2 * em + TINY, 2 * ev + TINY
-    # own bf16 working copy after the local steps
+    return (p, 2 * ep + TINY), (m, 2 * em + TINY), (v, 2 * ev + TINY)
+
+
+def _bf_reduce(grads, scale):
+    """float64 value of an ascending fp32 sum of bf16 arrays times scale, with
+    a bound on the binary32 evaluation's distance."""
+    dec = np.stack([bf16_decode(x) for x in grads])
+    s_scale = float(np.float32(scale))
+    return dec.sum(0) * s_scale, (len(grads) + 1) * U * np.abs(dec).sum(0) * abs(s_scale)
+
+
+def _bf_fedavg(weights, reps):
+    wv = np.asarray(weights, np.float32).astype(np.float64)
+    wn = wv / wv.sum()
+    dec = np.stack([bf16_decode(x) for x in reps])
+    xbar = (wn[:, None] * dec).sum(0)
+    return xbar, 2 * (len(reps) + 2) * U * (wn[:, None] * np.abs(dec)).sum(0) + TINY
+
+
+def _resolve_bf16(val, bnd, oracle_bits):
+    """bf16 rounding of a value known within +-bnd: unique where no rounding
+    boundary lies in the interval (then it must equal oracle_bits if given);
+    elsewhere the oracle's bits are taken after checking that they are the
+    rounding of some value in the interval.  Returns (bits, ambiguous mask)."""
+    amb = bf16_boundary_between(val - bnd, val + bnd)
+    ref = torch_bf16_bits(val.astype(np.float32))
+    if oracle_bits is None:
+        return ref, amb
+    lo = bf16_decode(torch_bf16_bits(np.nextafter((val - bnd).astype(np.float32), np.float32(-np.inf))))
+    hi = bf16_decode(torch_bf16_bits(np.nextafter((val + bnd).astype(np.float32), np.float32(np.inf))))
+    got = bf16_decode(oracle_bits)
+    ok = (~amb & (oracle_bits == ref)) | (amb & (got >= lo) & (got <= hi))
+    assert np.all(ok), "bf16 rounding outside the candidates"
+    return np.where(amb, oracle_bits, ref), amb
+
+
+def brute_force_round(hp, seg_off, seg_decay, R, G, A, self_group, grad_scale, step0, weights,
+                      grads, replicas, p0, m0, v0, oracle_working_after_steps=None):
+    """Straight-line float64 recomputation of one round, with a propagated
+    bound on the distance of any binary32 evaluation in the fixed order from
+    the exact result.  Returns dict of (value, bound) plus the per-step g and
+    its bound, and the masks of elements whose bf16 rounding is ambiguous."""
+    gsteps = [_bf_reduce(grads[a * R:(a + 1) * R], grad_scale) for a in range(A)]
+    (p, ep), (m, em), (v, ev) = _bf_steps(hp, seg_off, seg_decay, step0, gsteps, p0, m0, v0)
     amb_w = bf16_boundary_between(p - ep, p + ep)
     w_ref = torch_bf16_bits(p.astype(np.float32))
     if oracle_working_after_steps is not None:
         w_own = np.where(amb_w, oracle_working_after_steps, w_ref)
     else:
         w_own = w_ref
-    wv = np.asarray(weights, np.float32).astype(np.float64)
-    wn = wv / wv.sum()
     reps = [w_own if k == self_group else replicas[k] for k in range(G)]
-    dec = np.stack([bf16_decode(x) for x in reps])
-    xbar = (wn[:, None] * dec).sum(0)
-    ex = 2 * (G + 2) * U * (wn[:, None] * np.abs(dec)).sum(0) + TINY
+    xbar, ex = _bf_fedavg(weights, reps)
     amb_f = bf16_boundary_between(xbar - ex, xbar + ex)
     return dict(master=(xbar, ex), m=(m, em), v=(v, ev), p_steps=(p, ep), w_own=w_own,
                 amb_own=amb_w, amb_final=amb_f, g=gsteps)
@@ -568,6 +597,124 @@ def pin_round_uses_own_working_copy(orc):
     assert not np.array_equal(work, stale), "round did not use the updated working copy"
 
 
+# ---- FL+HSDP: two-tier gradient average and broadcast receive -------------
+
+def pin_reduce_wire_vs_float64(orc):
+    r = rng(15)
+    for R, scale in ((1, 1.0), (4, 0.25), (8, 0.125), (5, 0.2)):
+        grads = [random_bf16(r, 6000, std=10.0 ** r.uniform(-4, 0)) for _ in range(R)]
+        wire = orc.shard_reduce_wire(grads, scale)
+        val, bnd = _bf_reduce(grads, scale)
+        _resolve_bf16(val, bnd + TINY, wire)
+
+
+def pin_broadcast_recv(orc):
+    r = rng(16)
+    recv = (r.standard_normal(3000) * 0.02).astype(np.float32)
+    recv[:5] = [0.0, -0.0, np.inf, 3e38, 1e-40]
+    master = np.zeros(3000, np.float32)
+    work = np.zeros(3000, np.uint16)
+    orc.broadcast_recv(recv, master, work)
+    assert np.array_equal(master.view(np.uint32), recv.view(np.uint32)), "master != received"
+    assert np.array_equal(work, torch_bf16_bits(recv)), "working != bf16(received)"
+
+
+def _random_hsdp_case(r, R, H, A, member, n=16):
+    c = _random_round_case(r, R, 3, A, n=n)
+    c["H"] = H
+    c["replica"] = int(r.integers(0, H))
+    c["hsdp_scale"] = 1.0 / H
+    c["member"] = member
+    c["replica_wires"] = [None if k == c["replica"] else random_bf16(r, n, std=10.0 ** r.uniform(-4, -1))
+                          for a in range(A) for k in range(H)]
+    c["bcast"] = (c["p0"] + r.standard_normal(n) * 1e-3).astype(np.float32)
+    return c
+
+
+def check_hsdp_against_brute_force(orc, hp, c):
+    n = c["p0"].size
+    master, m, v = c["p0"].copy(), c["m0"].copy(), c["v0"].copy()
+    work = torch_bf16_bits(master)
+    ss = orc.round_hsdp(c["seg_off"], c["seg_decay"], c["R"], c["H"], c["replica"], c["hsdp_scale"],
+                        c["member"], c["G"], c["A"], c["self_group"], c["grad_scale"], hp, c["step0"],
+                        c["weights"], c["grads"], c["replica_wires"], c["replicas"], c["bcast"],
+                        master, m, v, work, want_sumsq=True)
+    tag = "HSDP R=%d H=%d A=%d member=%d" % (c["R"], c["H"], c["A"], c["member"])
+    # tier 1 and 2 per step, float64 with bounds; the own wire shard is the
+    # oracle's where its bf16 rounding is ambiguous within the bound
+    gsteps = []
+    for a in range(c["A"]):
+        ga = c["grads"][a * c["R"]:(a + 1) * c["R"]]
+        g1, e1 = _bf_reduce(ga, c["grad_scale"])
+        if c["H"] == 1:
+            gsteps.append((g1, e1))
+            continue
+        own, _ = _resolve_bf16(g1, e1 + TINY, orc.shard_reduce_wire(ga, c["grad_scale"]))
+        wires = [own if k == c["replica"] else c["replica_wires"][a * c["H"] + k]
+                 for k in range(c["H"])]
+        gsteps.append(_bf_reduce(wires, c["hsdp_scale"]))
+    (p, ep), (mm, em), (vv, ev) = _bf_steps(hp, c["seg_off"], c["seg_decay"], c["step0"], gsteps,
+                                            c["p0"], c["m0"], c["v0"])
+    _check_close("hsdp m " + tag, m, mm, em)
+    _check_close("hsdp v " + tag, v, vv, ev)
+    if c["member"]:
+        mw, mmm, mv = c["p0"].copy(), c["m0"].copy(), c["v0"].copy()
+        ww = torch_bf16_bits(mw)
+        # the oracle's own working copy after the steps, for ambiguous roundings
+        for a in range(c["A"]):
+            g = orc.shard_reduce(c["grads"][a * c["R"]:(a + 1) * c["R"]], c["grad_scale"]) if c["H"] == 1 else \
+                orc.shard_reduce([orc.shard_reduce_wire(c["grads"][a * c["R"]:(a + 1) * c["R"]], c["grad_scale"])
+                                  if k == c["replica"] else c["replica_wires"][a * c["H"] + k]
+                                  for k in range(c["H"])], c["hsdp_scale"])
+            orc.adamw_step(c["seg_off"], c["seg_decay"], hp, c["step0"] + a, g, mw, mmm, mv, ww)
+        own, _ = _resolve_bf16(p, ep, ww)
+        reps = [own if k == c["self_group"] else c["replicas"][k] for k in range(c["G"])]
+        xbar, ex = _bf_fedavg(c["weights"], reps)
+        _check_close("hsdp master " + tag, master, xbar, ex)
+    else:
+        assert np.array_equal(master.view(np.uint32), c["bcast"].view(np.uint32)), "bcast master " + tag
+    assert np.array_equal(work, torch_bf16_bits(master)), "hsdp working " + tag
+    off = c["seg_off"]
+    for a, (g, eg) in enumerate(gsteps):
+        for s_ in range(off.size - 1):
+            sl = slice(off[s_], off[s_ + 1])
+            want = np.sum(g[sl] ** 2)
+            bound = np.sum(2 * np.abs(g[sl]) * eg[sl] + eg[sl] ** 2) * 2 + 1e-12 * want + TINY
+            assert abs(ss[a, s_] - want) <= bound, "hsdp seg_sumsq " + tag
+
+
+def pin_hsdp_round_brute_force_16(orc):
+    """Two-tier rounds for R in {1..3}, H in {1..4}, A in {1, 2}, as a
+    FedAvg member and as a broadcast receiver."""
+    r = rng(17)
+    for hp in (STD_HP, BIG_HP):
+        for R in (1, 2, 3):
+            for H in (1, 2, 3, 4):
+                for A in (1, 2):
+                    for member in (1, 0):
+                        check_hsdp_against_brute_force(orc, hp, _random_hsdp_case(r, R, H, A, member))
+
+
+def pin_hsdp_one_replica_is_fsdp(orc):
+    """Section 4.2: FL+HSDP with one replica per group is FL+FSDP."""
+    r = rng(18)
+    c = _random_round_case(r, 4, 3, 3, n=5000)
+    outs = []
+    for hsdp in (False, True):
+        master, m, v = c["p0"].copy(), c["m0"].copy(), c["v0"].copy()
+        work = torch_bf16_bits(master)
+        if hsdp:
+            orc.round_hsdp(c["seg_off"], c["seg_decay"], 4, 1, 0, 1.0, 1, 3, 3, c["self_group"],
+                           c["grad_scale"], STD_HP, c["step0"], c["weights"], c["grads"], [None] * 3,
+                           c["replicas"], None, master, m, v, work)
+        else:
+            orc.round(c["seg_off"], c["seg_decay"], 4, 3, 3, c["self_group"], c["grad_scale"],
+                      STD_HP, c["step0"], c["weights"], c["grads"], c["replicas"], master, m, v, work)
+        outs.append((master, m, v, work))
+    for x, y in zip(*outs):
+        assert np.array_equal(x.view(np.uint8), y.view(np.uint8)), "H = 1 differs from FSDP"
+
+
 ALL_PINS = [
     pin_bf16_decode_all_patterns,
     pin_bf16_encode_matches_torch,
@@ -587,4 +734,8 @@ ALL_PINS = [
     pin_round_brute_force_16,
     pin_round_single_step_single_group,
     pin_round_uses_own_working_copy,
+    pin_reduce_wire_vs_float64,
+    pin_broadcast_recv,
+    pin_hsdp_round_brute_force_16,
+    pin_hsdp_one_replica_is_fsdp,
 ]

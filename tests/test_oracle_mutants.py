@@ -2,8 +2,9 @@
 catch every one of them (CPU only).
 
 Each mutant is a textual edit of oracle/oracle.c (a dropped term, a wrong sign
-or index, a swapped operand, a misplaced step).  The edited copy is built
-into a temporary directory; the real oracle is never modified.
+or index, a swapped operand, a misplaced step): (pattern, replacement[, k])
+replaces the k-th occurrence (default 0) of the pattern.  The edited copy is
+built into a temporary directory; the real oracle is never modified.
 """
 import os
 import shutil
@@ -62,6 +63,24 @@ MUTANTS = {
     "bf16_truncate": [("if (lower > 0x8000u || (lower == 0x8000u && (upper & 1u))) upper += 1u;", "")],
     "bf16_nan_not_quiet": [("return (uint16_t)((u >> 16) | 0x0040u);", "return (uint16_t)(u >> 16);")],
     "bf16_decode_shift": [("uint32_t u = (uint32_t)h << 16;", "uint32_t u = (uint32_t)h << 15;")],
+    "wire_truncated": [("wire[i] = orc_f32_to_bf16(acc * grad_scale);",
+                        "{ float q = acc * grad_scale; uint32_t b; memcpy(&b, &q, 4); wire[i] = (uint16_t)(b >> 16); }")],
+    "wire_unscaled": [("wire[i] = orc_f32_to_bf16(acc * grad_scale);", "wire[i] = orc_f32_to_bf16(acc);")],
+    "hsdp_skips_tier2": [("    if (H == 1) {\n      rc = orc_shard_reduce(n, R, ga, grad_scale, g);",
+                          "    if (1) {\n      rc = orc_shard_reduce(n, R, ga, grad_scale, g);")],
+    "hsdp_own_wire_not_used": [("wires[k] = (k == replica) ? wire : replica_wires",
+                                "wires[k] = (k == replica) ? replica_wires[(size_t)a * (size_t)H + (size_t)((k + 1) % H)] : replica_wires")],
+    "hsdp_unscaled_tier2": [("rc = orc_shard_reduce(n, H, wires, hsdp_scale, g);",
+                             "rc = orc_shard_reduce(n, H, wires, 1.0f, g);")],
+    "hsdp_member_swapped": [("    if (member) {\n      for (int k = 0; k < G; ++k)",
+                             "    if (!member) {\n      for (int k = 0; k < G; ++k)")],
+    "bcast_master_through_bf16": [("    master[i] = recv[i];\n    working[i] = orc_f32_to_bf16(recv[i]);",
+                                   "    master[i] = orc_bf16_to_f32(orc_f32_to_bf16(recv[i]));\n    working[i] = orc_f32_to_bf16(recv[i]);")],
+    "wire_wrong_peer_index": [("orc_bf16_to_f32(grads[r][i])", "orc_bf16_to_f32(grads[0][i])", 1)],
+    "hsdp_same_step_number": [("h, step0 + a, g, master", "h, step0, g, master", 1)],
+    "hsdp_reuses_first_grads": [("grads + (size_t)a * (size_t)R", "grads", 1)],
+    "hsdp_stale_own_replica": [("reps[k] = (k == self_group) ? working : replicas[k];",
+                                "reps[k] = (k == self_group) ? replicas[(k + 1) % G] : replicas[k];", 1)],
 }
 
 
@@ -74,9 +93,14 @@ def workdir():
 
 def _build_mutant(workdir, name, edits):
     src = open(SRC).read()
-    for old, new in edits:
-        assert src.count(old) == 1, "mutation %s: pattern not unique or missing: %r" % (name, old)
-        src = src.replace(old, new)
+    for edit in edits:
+        old, new = edit[0], edit[1]
+        k = edit[2] if len(edit) > 2 else 0
+        pos = -1
+        for _ in range(k + 1):
+            pos = src.find(old, pos + 1)
+            assert pos >= 0, "mutation %s: occurrence %d of %r missing" % (name, k, old)
+        src = src[:pos] + new + src[pos + len(old):]
     path = os.path.join(workdir, name + ".c")
     with open(path, "w") as f:
         f.write(src)
