@@ -145,25 +145,26 @@ def cpu_baseline(w, n_sample):
     n_sample elements of the same shard (same generator, same segments)."""
     import numpy as np
 
+    import harness as H
     import oracle
     import synth.buffers as B
 
     orc = oracle.Oracle()
+    n_sample = min(n_sample, w.n)
     idx = np.arange(n_sample, dtype=np.int64)
     off = w.seg_offsets[w.seg_offsets < n_sample]
     off = np.append(off, n_sample).astype(np.int64)
     dec = w.seg_decay[:off.size - 1]
     host = B.HostInputs(w, idx)
     t0 = time.perf_counter()
-    orc.round(off, dec, w.R, w.G, w.A, w.self_group, w.grad_scale, w.hp, w.step0, w.weights,
-              host.grads, host.replicas, host.master, host.m, host.v, host.working)
+    H.oracle_round(orc, w, host, seg_off=off, seg_decay=dec, want_sumsq=True)
     dt = time.perf_counter() - t0
     bytes_round = n_sample * (w.A * w.step_bytes_per_param() + w.fedavg_bytes_per_param())
     return dict(value=round(bytes_round / dt / 1e9, 4), unit="GB/s", cores=1, kind="oracle",
                 params_per_s=round(n_sample / dt, 1), seconds=round(dt, 3),
-                sample="one fl_round (A=%d, R=%d, G=%d) on the first %d elements of the same "
-                       "shard (%d segment(s)), single-threaded C oracle" % (
-                           w.A, w.R, w.G, n_sample, off.size - 1))
+                sample="one round with per-segment sums (A=%d, R=%d, G=%d, H=%d) on the first "
+                       "%d elements of the same shard (%d segment(s)), single-threaded C "
+                       "oracle" % (w.A, w.R, w.G, w.H, n_sample, off.size - 1))
 
 
 def main():
@@ -203,6 +204,9 @@ def main():
     import synth.buffers as B
     from synth import workloads as W
 
+    sys.path.insert(0, os.path.join(ROOT, "tests"))
+    import harness as H
+
     if not torch.cuda.is_available():
         print("bench.py needs a GPU", file=sys.stderr)
         sys.exit(1)
@@ -229,28 +233,23 @@ def main():
     stream = torch.cuda.current_stream()
     K, Wm = args.steps, args.warmup
     events = [P.HipEvents(w.A + 2) for _ in range(K)]
-    cfg_plain = P.make_round_cfg(w.R, w.G, w.A, w.weights, w.hp, self_group=w.self_group,
-                                 grad_scale=w.grad_scale, step0=w.step0)
     # every round also returns the per-segment sums of squares of each local
     # step's reduced gradient (A x n_seg floats)
     seg_sumsq = torch.empty(w.A * w.n_seg, dtype=torch.float32, device="cuda")
     for i in range(Wm):
-        P.fl_round(lay, cfg_plain, dev.grads, dev.replicas, dev.master, dev.m, dev.v, dev.working,
-                   seg_sumsq=seg_sumsq)
+        H.gpu_round(P, lay, w, dev, seg_sumsq=seg_sumsq, cfg=H.round_cfg(P, w, w.step0 + w.A * i))
     torch.cuda.synchronize()
     log("warmup done (%d rounds)" % Wm)
 
-    cfgs = [P.make_round_cfg(w.R, w.G, w.A, w.weights, w.hp, self_group=w.self_group,
-                             grad_scale=w.grad_scale, step0=w.step0 + w.A * (Wm + k),
-                             phase_events=events[k].handles) for k in range(K)]
+    cfgs = [H.round_cfg(P, w, w.step0 + w.A * (Wm + k), phase_events=events[k].handles)
+            for k in range(K)]
     start = torch.cuda.Event(enable_timing=True)
     stop = torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     t_wall = time.perf_counter()
     start.record(stream)
     for k in range(K):
-        P.fl_round(lay, cfgs[k], dev.grads, dev.replicas, dev.master, dev.m, dev.v, dev.working,
-                   seg_sumsq=seg_sumsq)
+        H.gpu_round(P, lay, w, dev, seg_sumsq=seg_sumsq, cfg=cfgs[k])
     stop.record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t_wall
@@ -292,7 +291,10 @@ def main():
                           fedavg_gbs=round(fed_bytes / (avg_fed * 1e-3) / 1e9, 2)),
         "roofline": {
             "bound": "hbm",
-            "kernel": "k_step<R=8, fused, per-segment sums> (one local step)",
+            "kernel": ("k_step<R=%d, fused, per-segment sums> (one local step)" % w.R
+                       if w.H == 1 else
+                       "one local step: k_step<R=%d, wire> + k_step<H=%d, fused, per-segment "
+                       "sums>" % (w.R, w.H)),
             "achieved": round(achieved, 2),
             "peak": PEAK_HBM_GBS,
             "unit": "GB/s",

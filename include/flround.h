@@ -224,6 +224,60 @@ int fl_round(const fl_layout* layout, const fl_round_cfg* cfg, const uint16_t* c
              uint16_t* working, float* seg_sumsq, void* stream);
 
 /* ------------------------------------------------------------------------
+ * FL+HSDP (Section 2, HSDP; Section 4.1, Eq. (2); Section 4.2, Eq. (5)).
+ * Each federation group is an HSDP deployment: H replicas of an S-way
+ * sharding group.  Gradients are averaged in two tiers (Section 5.1): over
+ * the sharding group (reduce-scatter), then over the H replicas of the shard
+ * (all-reduce, whose messages are bf16 shards).  After the A-th local step
+ * one replica per group joins FedAvg and then broadcasts its shard to the
+ * other replicas of its group.
+ *
+ * fl_shard_reduce_wire -- tier 1 in the wire format:
+ *     acc = 0; for r in 0..R-1: acc = acc + f32(peer_grads[r][i]);
+ *     wire_out[i] = bf16(acc * grad_scale)
+ *   wire_out: device, N bf16.  Tier 2 is fl_local_step over the H wire
+ *   shards (own included at its index) with grad_scale = 1/H.
+ *
+ * fl_broadcast_recv -- receive side of the broadcast, which carries the fp32
+ *   master shard so that all replicas stay bit-identical:
+ *     master[i] = recv_master[i]; working[i] = bf16(recv_master[i])
+ *   recv_master, master: device, N floats; working: device, N bf16.
+ *
+ * fl_round_hsdp -- one FL+HSDP round on one replica:
+ *     for a in 0..A-1:
+ *       H == 1: fl_local_step(R peers grads[a*R ..])      (FL+FSDP)
+ *       H  > 1: fl_shard_reduce_wire(grads[a*R ..], grad_scale) -> wire;
+ *               fl_local_step(H shards: replica_wires[a*H + k], with
+ *                             wire at k == replica; hsdp_scale)
+ *     then fedavg_member ? fl_fedavg (as in fl_round) : fl_broadcast_recv.
+ *   cfg: as for fl_round (G, self_group, weights, replica_fp are used only
+ *   by a FedAvg member).  replica_wires: host array of A*H device pointers
+ *   (entry a*H + replica ignored), or NULL when H == 1.  wire: device, N
+ *   bf16 scratch that receives this replica's tier-1 shard of each step (the
+ *   message it would send); unused when H == 1.  replicas: as for fl_round
+ *   (member only).  bcast_master: device, N floats (non-member only).
+ *   seg_sumsq: NULL or A*n_seg floats of the tier-2 gradient.
+ *   1 <= H <= FL_MAX_PEERS, 0 <= replica < H, hsdp_scale finite.
+ *   H == 1 is bitwise fl_round.
+ * ---------------------------------------------------------------------- */
+typedef struct {
+  int H;             /* replicas in the replication group (the paper's R) */
+  int replica;       /* this rank's index among the H                     */
+  float hsdp_scale;  /* 1/H for averaging                                 */
+  int fedavg_member; /* nonzero: joins FedAvg; zero: receives the broadcast */
+} fl_hsdp_cfg;
+
+int fl_shard_reduce_wire(const fl_layout* layout, int R, const uint16_t* const* peer_grads,
+                         float grad_scale, uint16_t* wire_out, void* stream);
+int fl_broadcast_recv(const fl_layout* layout, const float* recv_master, float* master,
+                      uint16_t* working, void* stream);
+int fl_round_hsdp(const fl_layout* layout, const fl_round_cfg* cfg, const fl_hsdp_cfg* hc,
+                  const uint16_t* const* grads, const uint16_t* const* replica_wires,
+                  uint16_t* wire, const uint16_t* const* replicas, const float* bcast_master,
+                  float* master, float* m, float* v, uint16_t* working, float* seg_sumsq,
+                  void* stream);
+
+/* ------------------------------------------------------------------------
  * Launch-shape control, for tuning sweeps and for tests that check that
  * results do not depend on the launch shape.  blocks_per_cu > 0 caps the
  * grid of the streaming kernels at blocks_per_cu * (number of CUs); 0

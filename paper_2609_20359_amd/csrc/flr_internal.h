@@ -65,6 +65,7 @@ struct StepArgs {
   uint16_t* working;   // may be null for the standalone AdamW step
   float* g_out;        // standalone reduce: fp32 reduced gradient
   const float* g_in;   // standalone AdamW: fp32 gradient
+  uint16_t* wire_out;  // reduce to the bf16 wire format
   float* partials;     // per-(piece, wave) sums of squares, kWaves per piece
                        // (null: not requested)
 };
@@ -81,6 +82,9 @@ struct FedArgs {
 hipError_t launch_local_step(const StepArgs& a, int grid, hipStream_t st);
 hipError_t launch_reduce(const StepArgs& a, int grid, hipStream_t st);
 hipError_t launch_adamw(const StepArgs& a, int grid, hipStream_t st);
+hipError_t launch_reduce_wire(const StepArgs& a, int grid, hipStream_t st);
+hipError_t launch_bcast_recv(int64_t n, const float* recv, float* master, uint16_t* working,
+                             int grid, hipStream_t st);
 hipError_t launch_fedavg(const FedArgs& a, int grid, hipStream_t st);
 // Per-segment totals from the (piece, wave) partials; chunk_sums is a
 // temporary of L.n_chunks doubles.

@@ -241,7 +241,7 @@ const char* fl_status_string(int status) {
   }
 }
 
-int fl_version(void) { return (1 << 16) | 0; }
+int fl_version(void) { return (1 << 16) | 1; }
 
 int fl_set_blocks_per_cu(int blocks_per_cu) {
   const int prev = g_blocks_per_cu;
@@ -482,6 +482,146 @@ int fl_fedavg(const fl_layout* layout, int G, const uint16_t* const* replicas,
   if (n == 0) return FL_OK;
   return enqueue_fedavg(layout, G, replicas, wn, master_out, working_out,
                         static_cast<hipStream_t>(stream));
+}
+
+int fl_shard_reduce_wire(const fl_layout* layout, int R, const uint16_t* const* peer_grads,
+                         float grad_scale, uint16_t* wire_out, void* stream) {
+  if (!layout) return FL_ERR_INVALID;
+  const int64_t n = layout->L.n;
+  int rc = check_peers(R, peer_grads, n);
+  if (rc != FL_OK) return rc;
+  if (!finite(grad_scale)) return FL_ERR_INVALID;
+  if ((rc = dev_ptr(wire_out, n)) != FL_OK) return rc;
+  if ((rc = check_device(layout)) != FL_OK) return rc;
+  if (n == 0) return FL_OK;
+  flr::StepArgs a = step_args(layout);
+  for (int r = 0; r < R; ++r) a.grads[r] = peer_grads[r];
+  a.R = R;
+  a.grad_scale = grad_scale;
+  a.wire_out = wire_out;
+  return status_of(flr::launch_reduce_wire(a, grid_for(layout, layout->L.n_tiles),
+                                           static_cast<hipStream_t>(stream)));
+}
+
+int fl_broadcast_recv(const fl_layout* layout, const float* recv_master, float* master,
+                      uint16_t* working, void* stream) {
+  if (!layout) return FL_ERR_INVALID;
+  const int64_t n = layout->L.n;
+  int rc;
+  if ((rc = dev_ptr(recv_master, n)) != FL_OK) return rc;
+  if ((rc = dev_ptr(master, n)) != FL_OK) return rc;
+  if ((rc = dev_ptr(working, n)) != FL_OK) return rc;
+  if ((rc = check_device(layout)) != FL_OK) return rc;
+  if (n == 0) return FL_OK;
+  return status_of(flr::launch_bcast_recv(n, recv_master, master, working, fedavg_grid(layout),
+                                          static_cast<hipStream_t>(stream)));
+}
+
+int fl_round_hsdp(const fl_layout* layout, const fl_round_cfg* cfg, const fl_hsdp_cfg* hc,
+                  const uint16_t* const* grads, const uint16_t* const* replica_wires,
+                  uint16_t* wire, const uint16_t* const* replicas, const float* bcast_master,
+                  float* master, float* m, float* v, uint16_t* working, float* seg_sumsq,
+                  void* stream) {
+  if (!layout || !cfg || !hc || !grads) return FL_ERR_INVALID;
+  const fl_round_cfg& c = *cfg;
+  const int64_t n = layout->L.n;
+  const bool member = hc->fedavg_member != 0;
+  if (c.R < 1 || c.R > FL_MAX_PEERS || c.A < 1 || c.step0 < 1 || !finite(c.grad_scale) ||
+      !hparams_ok(&c.h))
+    return FL_ERR_INVALID;
+  if (hc->H < 1 || hc->H > FL_MAX_PEERS || hc->replica < 0 || hc->replica >= hc->H ||
+      !finite(hc->hsdp_scale))
+    return FL_ERR_INVALID;
+  if (c.step0 > INT64_MAX - c.A) return FL_ERR_INVALID;
+  if ((int64_t)c.A * (c.R > hc->H ? c.R : hc->H) > (int64_t)INT32_MAX) return FL_ERR_INVALID;
+  int rc = FL_OK;
+  float wn[FL_MAX_GROUPS];
+  const uint16_t* reps[FL_MAX_GROUPS];
+  if (member) {
+    if (c.G < 1 || c.G > FL_MAX_GROUPS || c.self_group < 0 || c.self_group >= c.G || !replicas)
+      return FL_ERR_INVALID;
+    if ((rc = normalise_weights(c.G, c.weights, wn)) != FL_OK) return rc;
+    for (int g = 0; g < c.G; ++g) {
+      if (g == c.self_group) {
+        reps[g] = working;
+        continue;
+      }
+      if ((rc = dev_ptr(replicas[g], n)) != FL_OK) return rc;
+      reps[g] = replicas[g];
+    }
+    if (c.replica_fp)
+      for (int g = 0; g < c.G; ++g)
+        if (g != c.self_group && c.replica_fp[g] != layout->fingerprint) return FL_ERR_LAYOUT;
+  } else if ((rc = dev_ptr(bcast_master, n)) != FL_OK) {
+    return rc;
+  }
+  for (int64_t k = 0; k < (int64_t)c.A * c.R; ++k)
+    if ((rc = dev_ptr(grads[k], n)) != FL_OK) return rc;
+  if (hc->H > 1) {
+    if (!replica_wires) return FL_ERR_INVALID;
+    for (int a = 0; a < c.A; ++a)
+      for (int k = 0; k < hc->H; ++k)
+        if (k != hc->replica &&
+            (rc = dev_ptr(replica_wires[(size_t)a * (size_t)hc->H + (size_t)k], n)) != FL_OK)
+          return rc;
+    if ((rc = dev_ptr(wire, n)) != FL_OK) return rc;
+  }
+  if ((rc = dev_ptr(master, n)) != FL_OK) return rc;
+  if ((rc = dev_ptr(m, n)) != FL_OK) return rc;
+  if ((rc = dev_ptr(v, n)) != FL_OK) return rc;
+  if ((rc = dev_ptr(working, n)) != FL_OK) return rc;
+  if (n > 0 && (master == m || master == v || m == v)) return FL_ERR_INVALID;
+  if (n > 0 && hc->H > 1 && (wire == working)) return FL_ERR_INVALID;
+  if (seg_sumsq && (reinterpret_cast<uintptr_t>(seg_sumsq) & 3u)) return FL_ERR_ALIGN;
+  if (c.phase_events)
+    for (int k = 0; k < c.A + 2; ++k)
+      if (!c.phase_events[k]) return FL_ERR_INVALID;
+  if ((rc = check_device(layout)) != FL_OK) return rc;
+
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  auto record = [&](int k) -> int {
+    if (!c.phase_events) return FL_OK;
+    return status_of(hipEventRecord(static_cast<hipEvent_t>(c.phase_events[k]), st));
+  };
+  Workspace ws;
+  if (n > 0 && seg_sumsq && (rc = ws.alloc(layout->L, st)) != FL_OK) return rc;
+  for (int a = 0; a < c.A && rc == FL_OK; ++a) {
+    rc = record(a);
+    if (rc != FL_OK || n == 0) continue;
+    float* ss = seg_sumsq ? seg_sumsq + (size_t)a * (size_t)layout->L.n_seg : nullptr;
+    const uint16_t* const* ga = grads + (size_t)a * (size_t)c.R;
+    if (hc->H == 1) {
+      rc = enqueue_local_step(layout, c.h, c.step0 + a, c.R, ga, c.grad_scale, master, m, v,
+                              working, ws, ss, st);
+      continue;
+    }
+    // tier 1: the sharding group's reduction, in the bf16 wire format
+    flr::StepArgs t1 = step_args(layout);
+    for (int r = 0; r < c.R; ++r) t1.grads[r] = ga[r];
+    t1.R = c.R;
+    t1.grad_scale = c.grad_scale;
+    t1.wire_out = wire;
+    rc = status_of(flr::launch_reduce_wire(t1, grid_for(layout, layout->L.n_tiles), st));
+    // tier 2: the replication group's average of the H wire shards, fused
+    // with the optimiser step
+    const uint16_t* wires[FL_MAX_PEERS];
+    for (int k = 0; k < hc->H; ++k)
+      wires[k] = (k == hc->replica) ? wire : replica_wires[(size_t)a * (size_t)hc->H + (size_t)k];
+    if (rc == FL_OK)
+      rc = enqueue_local_step(layout, c.h, c.step0 + a, hc->H, wires, hc->hsdp_scale, master, m,
+                              v, working, ws, ss, st);
+  }
+  if (rc == FL_OK) rc = record(c.A);
+  if (rc == FL_OK && n > 0) {
+    if (member)
+      rc = enqueue_fedavg(layout, c.G, reps, wn, master, working, st);
+    else
+      rc = status_of(flr::launch_bcast_recv(n, bcast_master, master, working, fedavg_grid(layout),
+                                            st));
+  }
+  if (rc == FL_OK) rc = record(c.A + 1);
+  const int rc2 = ws.release();
+  return rc != FL_OK ? rc : rc2;
 }
 
 int fl_round(const fl_layout* layout, const fl_round_cfg* cfg, const uint16_t* const* grads,

@@ -178,7 +178,8 @@ __device__ __forceinline__ int find_seg(const int64_t* off, int lo, int hi, int6
 }
 
 // MODE 0: fused reduce + AdamW + working copy; 1: reduce only (g_out);
-// 2: AdamW only (g_in).  SUMSQ: per-piece sums of squares of g.
+// 2: AdamW only (g_in); 3: reduce to the bf16 wire format (wire_out).
+// SUMSQ: per-piece sums of squares of g.
 template <int RT, int MODE, bool SUMSQ>
 __global__ void __launch_bounds__(kBlock) k_step(const StepArgs a) {
   const int tid = threadIdx.x;
@@ -190,7 +191,7 @@ __global__ void __launch_bounds__(kBlock) k_step(const StepArgs a) {
 
     // segment of each element (only needed where the tile straddles segments)
     int seg[8];
-    if (ti.nseg > 1 && (SUMSQ || MODE != 1)) {
+    if (ti.nseg > 1 && (SUMSQ || MODE == 0 || MODE == 2)) {
       int s = cnt > 0 ? find_seg(a.L.seg_off, ti.seg0, ti.seg0 + ti.nseg - 1, base) : ti.seg0;
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
@@ -203,7 +204,7 @@ __global__ void __launch_bounds__(kBlock) k_step(const StepArgs a) {
     float g[8];
     float p[8], m[8], v[8];
     if (cnt == kVec) {
-      if constexpr (MODE != 1) {
+      if constexpr (MODE == 0 || MODE == 2) {
         load_f32x8(a.master + base, p);
         load_f32x8(a.m + base, m);
         load_f32x8(a.v + base, v);
@@ -214,7 +215,7 @@ __global__ void __launch_bounds__(kBlock) k_step(const StepArgs a) {
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
         p[e] = 0.f; m[e] = 0.f; v[e] = 0.f; g[e] = 0.f;
-        if constexpr (MODE != 1) {
+        if constexpr (MODE == 0 || MODE == 2) {
           if (e < cnt) { p[e] = a.master[base + e]; m[e] = a.m[base + e]; v[e] = a.v[base + e]; }
         }
         if constexpr (MODE == 2) {
@@ -231,6 +232,12 @@ __global__ void __launch_bounds__(kBlock) k_step(const StepArgs a) {
         store_f32x8(a.g_out + base, g);
       } else {
         for (int e = 0; e < cnt; ++e) a.g_out[base + e] = g[e];
+      }
+    } else if constexpr (MODE == 3) {
+      if (cnt == kVec) {
+        st(reinterpret_cast<u32x4*>(a.wire_out + base), pack_bf16x8(g));
+      } else {
+        for (int e = 0; e < cnt; ++e) a.wire_out[base + e] = (uint16_t)to_bf16(g[e]);
       }
     } else {
       const AdamScalars& s = a.s;
@@ -376,6 +383,32 @@ __global__ void __launch_bounds__(kBlock) k_seg_totals(const LayoutDev L, const 
   }
 }
 
+// Broadcast receive: master = recv; working = bf16(recv).
+__global__ void __launch_bounds__(kBlock) k_bcast_recv(const int64_t n, const float* recv,
+                                                       float* master, uint16_t* working) {
+  const int64_t nvec = (n + kVec - 1) / kVec;
+  const int64_t stride = (int64_t)gridDim.x * kBlock;
+  for (int64_t vi = (int64_t)blockIdx.x * kBlock + threadIdx.x; vi < nvec; vi += stride) {
+    const int64_t base = vi * kVec;
+    const int64_t left = n - base;
+    if (left >= kVec) {
+      float x[8];
+      const f32x4 a = ld_once(reinterpret_cast<const f32x4*>(recv + base));
+      const f32x4 b = ld_once(reinterpret_cast<const f32x4*>(recv + base + 4));
+      x[0] = a.x; x[1] = a.y; x[2] = a.z; x[3] = a.w;
+      x[4] = b.x; x[5] = b.y; x[6] = b.z; x[7] = b.w;
+      store_f32x8(master + base, x);
+      st(reinterpret_cast<u32x4*>(working + base), pack_bf16x8(x));
+    } else {
+      for (int e = 0; e < (int)left; ++e) {
+        const float x = recv[base + e];
+        master[base + e] = x;
+        working[base + e] = (uint16_t)to_bf16(x);
+      }
+    }
+  }
+}
+
 template <typename Args>
 hipError_t launch(const void* fn, const Args& a, int grid, hipStream_t st) {
   void* args[] = {const_cast<Args*>(&a)};
@@ -402,6 +435,17 @@ hipError_t launch_local_step(const StepArgs& a, int grid, hipStream_t st) {
 
 hipError_t launch_reduce(const StepArgs& a, int grid, hipStream_t st) {
   return a.partials ? dispatch_step<1, true>(a, grid, st) : dispatch_step<1, false>(a, grid, st);
+}
+
+hipError_t launch_reduce_wire(const StepArgs& a, int grid, hipStream_t st) {
+  return dispatch_step<3, false>(a, grid, st);
+}
+
+hipError_t launch_bcast_recv(int64_t n, const float* recv, float* master, uint16_t* working,
+                             int grid, hipStream_t st) {
+  void* args[] = {&n, &recv, &master, &working};
+  return hipLaunchKernel((const void*)k_bcast_recv, dim3((unsigned)grid), dim3(kBlock), args, 0,
+                         st);
 }
 
 hipError_t launch_adamw(const StepArgs& a, int grid, hipStream_t st) {

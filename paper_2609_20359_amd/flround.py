@@ -28,7 +28,8 @@ FL_MAX_GROUPS = 64
 EXPORTS = ("fl_status_string", "fl_version", "fl_layout_create", "fl_layout_destroy",
            "fl_layout_numel", "fl_layout_num_segments", "fl_fingerprint",
            "fl_layout_fingerprint", "fl_shard_reduce", "fl_adamw_step", "fl_local_step",
-           "fl_fedavg", "fl_round", "fl_set_blocks_per_cu")
+           "fl_fedavg", "fl_round", "fl_set_blocks_per_cu", "fl_shard_reduce_wire",
+           "fl_broadcast_recv", "fl_round_hsdp")
 
 _P = ctypes.c_void_p
 
@@ -51,6 +52,11 @@ class RoundCfg(ctypes.Structure):
                 ("weights", ctypes.POINTER(ctypes.c_float)),
                 ("replica_fp", ctypes.POINTER(ctypes.c_uint64)),
                 ("phase_events", ctypes.POINTER(ctypes.c_void_p))]
+
+
+class HsdpCfg(ctypes.Structure):
+    _fields_ = [("H", ctypes.c_int), ("replica", ctypes.c_int), ("hsdp_scale", ctypes.c_float),
+                ("fedavg_member", ctypes.c_int)]
 
 
 _lib = None
@@ -85,6 +91,10 @@ def lib():
                                     ctypes.c_int, _P, ctypes.c_float, _P, _P, _P, _P, _P, _P]
         L.fl_fedavg.argtypes = [_P, ctypes.c_int, _P, _P, _P, _P, _P, _P]
         L.fl_round.argtypes = [_P, ctypes.POINTER(RoundCfg), _P, _P, _P, _P, _P, _P, _P, _P]
+        L.fl_shard_reduce_wire.argtypes = [_P, ctypes.c_int, _P, ctypes.c_float, _P, _P]
+        L.fl_broadcast_recv.argtypes = [_P, _P, _P, _P, _P]
+        L.fl_round_hsdp.argtypes = [_P, ctypes.POINTER(RoundCfg), ctypes.POINTER(HsdpCfg), _P, _P,
+                                    _P, _P, _P, _P, _P, _P, _P, _P, _P]
         L.fl_set_blocks_per_cu.argtypes = [ctypes.c_int]
         L.fl_set_blocks_per_cu.restype = ctypes.c_int
         _lib = L
@@ -226,6 +236,38 @@ def fl_round(layout, cfg, grads, replicas, master, m, v, working, seg_sumsq=None
                         _ptr_array(replicas), _ptr(master), _ptr(m), _ptr(v), _ptr(working),
                         _ptr(seg_sumsq), _stream(stream))
     _check(rc, "fl_round")
+
+
+def fl_shard_reduce_wire(layout, peer_grads, grad_scale, wire_out, stream=None):
+    rc = lib().fl_shard_reduce_wire(layout.handle, len(peer_grads), _ptr_array(peer_grads),
+                                    float(grad_scale), _ptr(wire_out), _stream(stream))
+    _check(rc, "fl_shard_reduce_wire")
+
+
+def fl_broadcast_recv(layout, recv_master, master, working, stream=None):
+    rc = lib().fl_broadcast_recv(layout.handle, _ptr(recv_master), _ptr(master), _ptr(working),
+                                 _stream(stream))
+    _check(rc, "fl_broadcast_recv")
+
+
+def make_hsdp_cfg(H, replica=0, hsdp_scale=None, fedavg_member=True):
+    return HsdpCfg(int(H), int(replica), float(1.0 / H if hsdp_scale is None else hsdp_scale),
+                   1 if fedavg_member else 0)
+
+
+def fl_round_hsdp(layout, cfg, hcfg, grads, replica_wires, wire, replicas, bcast_master, master,
+                  m, v, working, seg_sumsq=None, stream=None):
+    """grads: A*R tensors; replica_wires: A*H tensors or None (entry
+    a*H + replica ignored), or None when H == 1; wire: bf16 scratch (H > 1);
+    replicas: G tensors/None (FedAvg member) or None; bcast_master: fp32
+    tensor (non-member) or None."""
+    rc = lib().fl_round_hsdp(layout.handle, ctypes.byref(cfg), ctypes.byref(hcfg),
+                             _ptr_array(grads),
+                             None if replica_wires is None else _ptr_array(replica_wires),
+                             _ptr(wire), None if replicas is None else _ptr_array(replicas),
+                             _ptr(bcast_master), _ptr(master), _ptr(m), _ptr(v), _ptr(working),
+                             _ptr(seg_sumsq), _stream(stream))
+    _check(rc, "fl_round_hsdp")
 
 
 # ---- HIP events (for fl_round's per-phase timing) -------------------------

@@ -26,10 +26,23 @@ class DeviceInputs:
         self.grads = [self.grad_arrays[k] for k in w.grad_index]
         self.replicas = [None if sp is None else dev_fill(torch.empty(n, **bf), sp)
                          for sp in w.replica_specs]
+        filled = {}
+
+        def wire_buf(sp):
+            if sp.key() not in filled:
+                filled[sp.key()] = dev_fill(torch.empty(n, **bf), sp)
+            return filled[sp.key()]
+
+        self.replica_wires = [None if sp is None else wire_buf(sp) for sp in w.wire_specs] or None
+        self.wire = torch.empty(n, **bf) if w.H > 1 else None
+        self.bcast = None if w.bcast_spec is None else dev_fill(torch.empty(n, **f32),
+                                                                 w.bcast_spec)
 
     def bytes(self):
         t = [self.master, self.m, self.v, self.working] + self.grad_arrays + \
-            [r for r in self.replicas if r is not None]
+            [r for r in self.replicas if r is not None] + \
+            list({id(r): r for r in (self.replica_wires or []) if r is not None}.values()) + \
+            [x for x in (self.wire, self.bcast) if x is not None]
         return sum(x.numel() * x.element_size() for x in t)
 
 
@@ -68,3 +81,5 @@ class HostInputs:
         self.grad_arrays = [fill(sp) for sp in w.grad_specs]
         self.grads = [self.grad_arrays[k] for k in w.grad_index]
         self.replicas = [None if sp is None else fill(sp) for sp in w.replica_specs]
+        self.replica_wires = [None if sp is None else fill(sp) for sp in w.wire_specs] or None
+        self.bcast = None if w.bcast_spec is None else fill(w.bcast_spec)

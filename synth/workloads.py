@@ -26,6 +26,8 @@ MASTER_STREAM = 1
 GRAD_STREAM0 = 1000
 DRIFT_STREAM0 = 2000
 LAYOUT_STREAM = 3000
+WIRE_STREAM0 = 4000
+BCAST_STREAM = 2500
 
 MASTER_STD = 0.02
 GRAD_STD = 1e-3
@@ -109,6 +111,13 @@ class Workload:
     step0: int = 1
     grad_scale: Optional[float] = None
     note: str = ""
+    # FL+HSDP: H replicas of the sharding group; this rank is `replica`;
+    # hsdp_member: it joins FedAvg (else it receives the broadcast)
+    H: int = 1
+    replica: int = 0
+    hsdp_member: bool = True
+    wire_specs: list = field(default_factory=list)   # A*H entries, None at own index
+    bcast_spec: object = None
 
     def __post_init__(self):
         if self.grad_scale is None:
@@ -126,22 +135,32 @@ class Workload:
         return len(self.seg_offsets) - 1
 
     def step_bytes_per_param(self):
-        """Algorithmic HBM bytes per parameter of one fused local step:
-        R bf16 gradients read, fp32 master/m/v read and written, bf16
-        working copy written."""
-        return 2 * self.R + 12 + 12 + 2
+        """Algorithmic HBM bytes per parameter of one local step: R bf16
+        gradients read, fp32 master/m/v read and written, bf16 working copy
+        written; with H > 1 replicas also the own bf16 wire shard written and
+        the H wire shards read."""
+        base = 2 * self.R + 12 + 12 + 2
+        if self.H > 1:
+            base += 2 + 2 * self.H
+        return base
 
     def fedavg_bytes_per_param(self):
         """G bf16 replicas read (own working copy included), fp32 master and
-        bf16 working copy written."""
+        bf16 working copy written; a broadcast receiver reads the fp32 shard
+        instead."""
+        if self.H > 1 and not self.hsdp_member:
+            return 4 + 4 + 2
         return 2 * self.G + 4 + 2
 
     def round_bytes(self):
         return self.n * (self.A * self.step_bytes_per_param() + self.fedavg_bytes_per_param())
 
     def describe(self):
-        return dict(workload=self.name, n=self.n, n_seg=self.n_seg, R=self.R, G=self.G,
-                    A=self.A, distinct_grad_arrays=len(self.grad_specs))
+        d = dict(workload=self.name, n=self.n, n_seg=self.n_seg, R=self.R, G=self.G,
+                 A=self.A, distinct_grad_arrays=len(self.grad_specs))
+        if self.H > 1:
+            d.update(H=self.H, replica=self.replica, fedavg_member=self.hsdp_member)
+        return d
 
 
 def _replicas(G, self_group, seed, mean=0.0, std=MASTER_STD, drift=DRIFT_STD):
@@ -161,7 +180,8 @@ def _normal_grads(n_arrays, seed, std=GRAD_STD):
 
 def make_workload(name, seg_sizes, seg_decay, R, G, A, *, weights=None, seed=0,
                   distinct_grads=True, student=False, own_drift=False, hp=None,
-                  self_group=0, step0=1, grad_scale=None, note=""):
+                  self_group=0, step0=1, grad_scale=None, note="", H=1, replica=0,
+                  hsdp_member=True):
     """General constructor used by the named workloads and by the tests.
 
     distinct_grads: A*R distinct gradient arrays (else R arrays reused by
@@ -186,12 +206,24 @@ def make_workload(name, seg_sizes, seg_decay, R, G, A, *, weights=None, seed=0,
         working = spec(NORMAL_BF16, MASTER_STREAM, seed, 0.0, MASTER_STD)
     if weights is None:
         weights = np.full(G, 1.0 / G, dtype=np.float32)
+    wires = []
+    bcast = None
+    if H > 1:
+        # the other replicas' tier-1 shards: the mean of R peers' N(0, 1e-3)
+        # (reused by every step when the gradient arrays are)
+        wires = [None if k == replica else
+                 spec(NORMAL_BF16, WIRE_STREAM0 + (a * H if distinct_grads else 0) + k, seed, 0.0,
+                      GRAD_STD / np.sqrt(R))
+                 for a in range(A) for k in range(H)]
+        bcast = spec(DRIFT_F32, MASTER_STREAM, seed, 0.0, MASTER_STD, stream2=BCAST_STREAM,
+                     std2=DRIFT_STD)
     return Workload(name=name, seg_offsets=off, seg_decay=np.asarray(seg_decay, np.uint8),
                     R=R, G=G, A=A, weights=np.asarray(weights, np.float32), master_spec=master,
                     grad_specs=grads, grad_index=gidx,
                     replica_specs=_replicas(G, self_group, seed), working_spec=working,
                     hp=dict(hp or ADAMW), self_group=self_group, step0=step0,
-                    grad_scale=grad_scale, note=note)
+                    grad_scale=grad_scale, note=note, H=H, replica=replica,
+                    hsdp_member=hsdp_member, wire_specs=wires, bcast_spec=bcast)
 
 
 def tiny(seed=0):
@@ -240,8 +272,19 @@ def stress(seed=0):
                          seed=seed, distinct_grads=True, student=True)
 
 
+def hsdp_s4_h2(seed=0, member=True):
+    """The FL+HSDP-shaped shard (S = 4) with its replication group made
+    explicit: H = 2 replicas, two-tier gradient average, this replica the
+    group's FedAvg member (member=False: the broadcast receiver)."""
+    sizes, dec = llama31_8b_segments(4)
+    return make_workload("llama31_8b_flhsdp_s4_h2_r4_g4_a8" + ("" if member else "_recv"), sizes,
+                         dec, R=4, G=4, A=8, seed=seed, distinct_grads=False, H=2, replica=0,
+                         hsdp_member=member)
+
+
 ALL = dict(tiny=tiny, llama8b_s8=llama8b_s8, fedavg_heavy=fedavg_heavy, hsdp_s4=hsdp_s4,
-           stress=stress)
+           stress=stress, hsdp_s4_h2=hsdp_s4_h2,
+           hsdp_s4_h2_recv=lambda seed=0: hsdp_s4_h2(seed, member=False))
 
 
 def sample_indices(w, n_random=1 << 16, seed=1, full_segments=4, max_full=4096):

@@ -43,22 +43,40 @@ def compact_layout(w: Workload, idx, full_segments=()):
 
 def oracle_round(orc, w: Workload, host: HostInputs, seg_off=None, seg_decay=None,
                  want_sumsq=False):
-    """Run the oracle round in place on host arrays (copies are the caller's
-    business).  Returns the per-step per-segment sums of squares or None."""
+    """Run the oracle round (FL+FSDP, or FL+HSDP when w.H > 1) in place on host
+    arrays.  Returns the per-step per-segment sums of squares or None."""
     seg_off = w.seg_offsets if seg_off is None else seg_off
     seg_decay = w.seg_decay if seg_decay is None else seg_decay
+    if w.H > 1:
+        return orc.round_hsdp(seg_off, seg_decay, w.R, w.H, w.replica, 1.0 / w.H, w.hsdp_member,
+                              w.G, w.A, w.self_group, w.grad_scale, w.hp, w.step0, w.weights,
+                              host.grads, host.replica_wires, host.replicas, host.bcast,
+                              host.master, host.m, host.v, host.working, want_sumsq=want_sumsq)
     return orc.round(seg_off, seg_decay, w.R, w.G, w.A, w.self_group, w.grad_scale, w.hp,
                      w.step0, w.weights, host.grads, host.replicas, host.master, host.m, host.v,
                      host.working, want_sumsq=want_sumsq)
 
 
+def round_cfg(P, w: Workload, step0=None, phase_events=None):
+    return P.make_round_cfg(w.R, w.G, w.A, w.weights, w.hp, self_group=w.self_group,
+                            grad_scale=w.grad_scale, step0=w.step0 if step0 is None else step0,
+                            phase_events=phase_events)
+
+
 def gpu_round(P, layout, w: Workload, dev: DeviceInputs, seg_sumsq=None, phase_events=None,
               cfg=None):
+    """One fl_round (or fl_round_hsdp when w.H > 1) through the C ABI."""
     if cfg is None:
-        cfg = P.make_round_cfg(w.R, w.G, w.A, w.weights, w.hp, self_group=w.self_group,
-                               grad_scale=w.grad_scale, step0=w.step0, phase_events=phase_events)
-    P.fl_round(layout, cfg, dev.grads, dev.replicas, dev.master, dev.m, dev.v, dev.working,
-               seg_sumsq=seg_sumsq)
+        cfg = round_cfg(P, w, phase_events=phase_events)
+    if w.H > 1:
+        hc = P.make_hsdp_cfg(w.H, w.replica, 1.0 / w.H, w.hsdp_member)
+        P.fl_round_hsdp(layout, cfg, hc, dev.grads, dev.replica_wires, dev.wire,
+                        dev.replicas if w.hsdp_member else None,
+                        None if w.hsdp_member else dev.bcast, dev.master, dev.m, dev.v,
+                        dev.working, seg_sumsq=seg_sumsq)
+    else:
+        P.fl_round(layout, cfg, dev.grads, dev.replicas, dev.master, dev.m, dev.v, dev.working,
+                   seg_sumsq=seg_sumsq)
     return cfg
 
 

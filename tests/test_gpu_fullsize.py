@@ -13,7 +13,7 @@ from synth import workloads as W
 
 pytestmark = pytest.mark.gpu
 
-WORKLOADS = ["llama8b_s8", "fedavg_heavy", "hsdp_s4", "stress"]
+WORKLOADS = ["llama8b_s8", "fedavg_heavy", "hsdp_s4", "stress", "hsdp_s4_h2", "hsdp_s4_h2_recv"]
 
 
 def _say(*a):
