@@ -15,6 +15,14 @@ _LIB_PATH = os.path.join(HERE, "liboracle.so")
 _P = ctypes.c_void_p
 
 
+class Outer(ctypes.Structure):
+    _fields_ = [("lr", ctypes.c_float), ("momentum", ctypes.c_float), ("nesterov", ctypes.c_int)]
+
+
+def outer(oh):
+    return Outer(oh["lr"], oh["momentum"], 1 if oh.get("nesterov", True) else 0)
+
+
 class Hparams(ctypes.Structure):
     _fields_ = [("lr", ctypes.c_float), ("beta1", ctypes.c_float), ("beta2", ctypes.c_float),
                 ("eps", ctypes.c_float), ("weight_decay", ctypes.c_float)]
@@ -42,6 +50,12 @@ def _declare(lib):
                                    ctypes.c_int, ctypes.c_int, ctypes.c_float,
                                    ctypes.POINTER(Hparams), ctypes.c_int64, _P, _P, _P, _P, _P,
                                    _P, _P, _P, _P, _P]
+    lib.orc_fedopt.argtypes = [ctypes.c_int64, ctypes.c_int, _P, _P, ctypes.POINTER(Outer), _P,
+                               _P, _P, _P]
+    lib.orc_round_outer.argtypes = [ctypes.c_int64, _P, _P, ctypes.c_int, ctypes.c_int,
+                                    ctypes.c_int, ctypes.c_int, ctypes.c_float,
+                                    ctypes.POINTER(Hparams), ctypes.c_int64, _P,
+                                    ctypes.POINTER(Outer), _P, _P, _P, _P, _P, _P, _P, _P, _P]
     return lib
 
 
@@ -183,6 +197,43 @@ class Oracle:
                                    None if ss is None else ss.ctypes.data)
         if rc:
             raise ValueError("orc_round_hsdp: %d" % rc)
+        return None if ss is None else ss.reshape(A, n_seg)
+
+    def fedopt(self, replicas, weights, oh, prev, buf, master_out=None, working_out=None):
+        """Outer step in place on prev and buf; returns (master, working)."""
+        replicas = [_c(r, np.uint16) for r in replicas]
+        n = replicas[0].size
+        w = _c(weights, np.float32)
+        o = outer(oh)
+        master_out = np.empty(n, np.float32) if master_out is None else master_out
+        working_out = np.empty(n, np.uint16) if working_out is None else working_out
+        rc = self.L.orc_fedopt(n, len(replicas), _ptr_array(replicas), w.ctypes.data,
+                               ctypes.byref(o), prev.ctypes.data, buf.ctypes.data,
+                               master_out.ctypes.data, working_out.ctypes.data)
+        if rc:
+            raise ValueError("orc_fedopt: %d" % rc)
+        return master_out, working_out
+
+    def round_outer(self, seg_off, seg_decay, R, G, A, self_group, grad_scale, hp, step0,
+                    weights, oh, grads, replicas, prev, buf, master, m, v, working,
+                    want_sumsq=False):
+        seg_off = _c(seg_off, np.int64)
+        seg_decay = _c(seg_decay, np.uint8)
+        n_seg = seg_off.size - 1
+        grads = [_c(g, np.uint16) for g in grads]
+        reps = [working if r is None else _c(r, np.uint16) for r in replicas]
+        w = _c(weights, np.float32)
+        h = hparams(hp)
+        o = outer(oh)
+        ss = np.empty(A * n_seg, np.float64) if want_sumsq else None
+        rc = self.L.orc_round_outer(n_seg, seg_off.ctypes.data, seg_decay.ctypes.data, R, G, A,
+                                    self_group, grad_scale, ctypes.byref(h), step0, w.ctypes.data,
+                                    ctypes.byref(o), _ptr_array(grads), _ptr_array(reps),
+                                    prev.ctypes.data, buf.ctypes.data, master.ctypes.data,
+                                    m.ctypes.data, v.ctypes.data, working.ctypes.data,
+                                    None if ss is None else ss.ctypes.data)
+        if rc:
+            raise ValueError("orc_round_outer: %d" % rc)
         return None if ss is None else ss.reshape(A, n_seg)
 
     def round(self, seg_off, seg_decay, R, G, A, self_group, grad_scale, hp, step0, weights,

@@ -222,6 +222,65 @@ int orc_round_hsdp(int64_t n_seg, const int64_t* seg_off, const uint8_t* seg_dec
   return rc;
 }
 
+int orc_fedopt(int64_t n, int G, const uint16_t* const* replicas, const float* weights,
+               const orc_outer* o, float* prev, float* buf, float* master_out,
+               uint16_t* working_out) {
+  if (n < 0 || G < 1 || !weights || !o ||
+      (n > 0 && (!replicas || !prev || !buf || !master_out || !working_out)))
+    return -1;
+  float* wn = (float*)malloc(sizeof(float) * (size_t)G);
+  if (!wn) return -1;
+  if (orc_norm_weights(G, weights, wn) != 0) {
+    free(wn);
+    return -1;
+  }
+  const float eta = o->lr;
+  const float mu = o->momentum;
+  for (int64_t i = 0; i < n; ++i) {
+    float xbar = 0.0f;
+    for (int k = 0; k < G; ++k) xbar = xbar + (wn[k] * orc_bf16_to_f32(replicas[k][i]));
+    const float delta = prev[i] - xbar;
+    const float b = (mu * buf[i]) + delta;
+    const float d = o->nesterov ? (delta + (mu * b)) : b;
+    const float p = prev[i] - (eta * d);
+    buf[i] = b;
+    prev[i] = p;
+    master_out[i] = p;
+    working_out[i] = orc_f32_to_bf16(p);
+  }
+  free(wn);
+  return 0;
+}
+
+int orc_round_outer(int64_t n_seg, const int64_t* seg_off, const uint8_t* seg_decay, int R, int G,
+                    int A, int self_group, float grad_scale, const orc_hparams* h, int64_t step0,
+                    const float* weights, const orc_outer* o, const uint16_t* const* grads,
+                    const uint16_t* const* replicas, float* prev, float* buf, float* master,
+                    float* m, float* v, uint16_t* working, double* seg_sumsq) {
+  if (n_seg < 0 || !seg_off || R < 1 || G < 1 || A < 1 || self_group < 0 ||
+      self_group >= G || !h || !o || step0 < 1 || !weights || !grads || !replicas)
+    return -1;
+  const int64_t n = seg_off[n_seg];
+  if (n > 0 && (!master || !m || !v || !working || !prev || !buf)) return -1;
+  float* g = (float*)malloc(sizeof(float) * (size_t)(n > 0 ? n : 1));
+  const uint16_t** reps = (const uint16_t**)malloc(sizeof(uint16_t*) * (size_t)G);
+  int rc = (g && reps) ? 0 : -1;
+  for (int a = 0; a < A && rc == 0; ++a) {
+    rc = orc_shard_reduce(n, R, grads + (size_t)a * (size_t)R, grad_scale, g);
+    if (rc == 0 && seg_sumsq)
+      rc = orc_seg_sumsq(n_seg, seg_off, g, seg_sumsq + (size_t)a * (size_t)n_seg);
+    if (rc == 0)
+      rc = orc_adamw_step(n_seg, seg_off, seg_decay, h, step0 + a, g, master, m, v, working);
+  }
+  if (rc == 0) {
+    for (int k = 0; k < G; ++k) reps[k] = (k == self_group) ? working : replicas[k];
+    rc = orc_fedopt(n, G, reps, weights, o, prev, buf, master, working);
+  }
+  free(g);
+  free(reps);
+  return rc;
+}
+
 /* Array forms of the two conversions, for the tests. */
 void orc_f32_to_bf16_array(int64_t n, const float* x, uint16_t* out) {
   for (int64_t i = 0; i < n; ++i) out[i] = orc_f32_to_bf16(x[i]);

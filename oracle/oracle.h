@@ -55,6 +55,18 @@
  *       fp32 master shard to the others of its group: master = received,
  *       working = bf16_rne(received).
  *
+ * Outer optimiser (Section 3: DiLoCo and Photon pair the inner AdamW with an
+ * outer Nesterov-momentum step; Section 4.1: other aggregation strategies
+ * build on FedAvg).  The outer gradient is the global model at the start of
+ * the round minus the weighted average of the groups' models:
+ *  (n3) xbar = FedAvg sum of (a3); delta = prev - xbar;
+ *       buf = mu * buf + delta;
+ *       d = nesterov ? delta + mu * buf : buf;
+ *       p = prev - eta * d;
+ *       master = p; working = bf16_rne(p); prev = p   (fp32, in this order)
+ *       With eta = 1 and mu = 0 this is FedAvg up to the rounding of
+ *       prev - (prev - xbar).
+ *
  * Every fp32 operation above is one IEEE-754 binary32 operation rounded to
  * nearest even, evaluated in the written order; the file is compiled with
  * -ffp-contract=off and without fast-math, and subnormals are kept.
@@ -122,6 +134,24 @@ int orc_round_hsdp(int64_t n_seg, const int64_t* seg_off, const uint8_t* seg_dec
                    const uint16_t* const* grads, const uint16_t* const* replica_wires,
                    const uint16_t* const* replicas, const float* bcast, float* master, float* m,
                    float* v, uint16_t* working, double* seg_sumsq);
+
+typedef struct {
+  float lr, momentum;
+  int nesterov;
+} orc_outer;
+
+/* (n3) outer step.  prev, buf: fp32 state (in/out); working_out may be one
+ * of replicas[]. */
+int orc_fedopt(int64_t n, int G, const uint16_t* const* replicas, const float* weights,
+               const orc_outer* o, float* prev, float* buf, float* master_out,
+               uint16_t* working_out);
+
+/* A local steps as in orc_round, then the outer step (n3) instead of FedAvg. */
+int orc_round_outer(int64_t n_seg, const int64_t* seg_off, const uint8_t* seg_decay, int R, int G,
+                    int A, int self_group, float grad_scale, const orc_hparams* h, int64_t step0,
+                    const float* weights, const orc_outer* o, const uint16_t* const* grads,
+                    const uint16_t* const* replicas, float* prev, float* buf, float* master,
+                    float* m, float* v, uint16_t* working, double* seg_sumsq);
 
 #ifdef __cplusplus
 }

@@ -715,6 +715,139 @@ def pin_hsdp_one_replica_is_fsdp(orc):
         assert np.array_equal(x.view(np.uint8), y.view(np.uint8)), "H = 1 differs from FSDP"
 
 
+# ---- outer optimiser (FedOpt / FedMom with Nesterov momentum) --------------
+
+OUTER_HP = [dict(lr=0.7, momentum=0.9, nesterov=True), dict(lr=1.3, momentum=0.5, nesterov=False),
+            dict(lr=0.7, momentum=0.0, nesterov=True)]
+
+
+def _bf_outer(oh, prev, eprev, buf, ebuf, xbar, ex):
+    """float64 outer step with propagated bounds on the binary32 evaluation."""
+    eta, mu = float(np.float32(oh["lr"])), float(np.float32(oh["momentum"]))
+    delta = prev - xbar
+    ed = eprev + ex + U * (np.abs(delta) + eprev + ex)
+    b = mu * buf + delta
+    eb = mu * ebuf + ed + U * mu * (np.abs(buf) + ebuf) + U * (np.abs(b) + mu * ebuf + ed)
+    if oh.get("nesterov", True):
+        d = delta + mu * b
+        e_d = ed + mu * eb + U * mu * (np.abs(b) + eb) + U * (np.abs(d) + ed + mu * eb)
+    else:
+        d, e_d = b, eb
+    p = prev - eta * d
+    ep = eprev + eta * e_d + U * eta * (np.abs(d) + e_d) + U * (np.abs(p) + eprev + eta * e_d)
+    return p, 2 * ep + TINY, b, 2 * eb + TINY
+
+
+def pin_outer_vs_torch_sgd(orc):
+    """Four outer steps against torch.optim.SGD (momentum, dampening 0,
+    Nesterov or not) run in float64 on the outer gradient prev - average."""
+    r = rng(19)
+    for oh in OUTER_HP:
+        n, G = 3000, 4
+        prev = (r.standard_normal(n) * 0.02).astype(np.float32)
+        buf = np.zeros(n, np.float32)
+        theta = torch.tensor(prev.astype(np.float64), requires_grad=True)
+        opt = torch.optim.SGD([theta], lr=float(np.float32(oh["lr"])),
+                              momentum=float(np.float32(oh["momentum"])), dampening=0.0,
+                              nesterov=bool(oh["nesterov"] and oh["momentum"] > 0),
+                              weight_decay=0.0)
+        p64, ep = prev.astype(np.float64), np.zeros(n)
+        b64, eb = np.zeros(n), np.zeros(n)
+        for rnd in range(4):
+            reps = [torch_bf16_bits((prev + r.standard_normal(n) * 1e-3).astype(np.float32))
+                    for _ in range(G)]
+            w = r.uniform(0.5, 3.0, G).astype(np.float32)
+            master, work = orc.fedopt(reps, w, oh, prev, buf)
+            xbar, ex = _bf_fedavg(w, reps)
+            theta.grad = torch.tensor(theta.detach().numpy() - xbar)
+            opt.step()
+            p64, ep, b64, eb = _bf_outer(oh, p64, ep, b64, eb, xbar, ex)
+            tag = "outer %s round %d" % (oh, rnd)
+            _check_close(tag + " torch param", prev, theta.detach().numpy(), ep)
+            if oh["momentum"] > 0:
+                tb = opt.state[theta]["momentum_buffer"].numpy()
+                _check_close(tag + " torch buffer", buf, tb, eb)
+            assert np.array_equal(master.view(np.uint32), prev.view(np.uint32)), tag + " master"
+            assert np.array_equal(work, torch_bf16_bits(master)), tag + " working"
+
+
+def pin_outer_unit_lr_no_momentum_is_fedavg(orc):
+    """eta = 1, mu = 0: p = prev - (prev - xbar); where prev and xbar are
+    within a factor of 2 both subtractions are exact (Sterbenz), so master is
+    FedAvg's bitwise; elsewhere within the two roundings' bound."""
+    r = rng(20)
+    n, G = 5000, 3
+    prev = (r.standard_normal(n) * 0.02).astype(np.float32)
+    reps = [torch_bf16_bits((prev + r.standard_normal(n) * 1e-4).astype(np.float32))
+            for _ in range(G)]
+    w = np.array([1.0, 2.0, 3.0], np.float32)
+    fa, _ = orc.fedavg(reps, w)
+    p, b = prev.copy(), np.zeros(n, np.float32)
+    master, _ = orc.fedopt(reps, w, dict(lr=1.0, momentum=0.0, nesterov=True), p, b)
+    exact = (np.sign(prev) == np.sign(fa)) & (np.abs(fa) <= 2 * np.abs(prev)) & \
+        (np.abs(prev) <= 2 * np.abs(fa))
+    assert exact.mean() > 0.9
+    assert np.array_equal(master[exact].view(np.uint32), fa[exact].view(np.uint32)), "not FedAvg"
+    d64 = prev.astype(np.float64) - fa.astype(np.float64)
+    bound = 2 * U * (np.abs(d64) + np.abs(fa.astype(np.float64))) + TINY
+    _check_close("eta1 mu0", master[~exact], fa[~exact].astype(np.float64), bound[~exact])
+
+
+def pin_outer_fixed_point(orc):
+    """Replicas equal to the global model and no momentum: nothing moves."""
+    r = rng(21)
+    x = random_bf16(r, 4000, std=0.02)
+    prev = bf16_decode(x).astype(np.float32)
+    buf = np.zeros(4000, np.float32)
+    master, work = orc.fedopt([x, x, x], np.array([1, 1, 2], np.float32),
+                              dict(lr=0.7, momentum=0.9, nesterov=True), prev, buf)
+    assert np.array_equal(master, bf16_decode(x).astype(np.float32)), "fixed point moved"
+    assert not buf.any() and np.array_equal(work, x)
+
+
+def pin_round_outer_brute_force_16(orc):
+    """A local steps then the outer step, every (R, G, A) in {1..3}^3, two
+    outer settings, two rounds in a row (prev and buf carried over)."""
+    r = rng(22)
+    for oh in OUTER_HP[:2]:
+        for R in (1, 2, 3):
+            for G in (1, 2, 3):
+                for A in (1, 2, 3):
+                    c = _random_round_case(r, R, G, A)
+                    n = c["p0"].size
+                    prev = (c["p0"] + r.standard_normal(n) * 1e-3).astype(np.float32)
+                    buf = (r.standard_normal(n) * 1e-4).astype(np.float32)
+                    p64, ep = prev.astype(np.float64), np.zeros(n)
+                    b64, eb = buf.astype(np.float64), np.zeros(n)
+                    master, m, v = c["p0"].copy(), c["m0"].copy(), c["v0"].copy()
+                    work = torch_bf16_bits(master)
+                    orc.round_outer(c["seg_off"], c["seg_decay"], R, G, A, c["self_group"],
+                                    c["grad_scale"], STD_HP, c["step0"], c["weights"], oh,
+                                    c["grads"], c["replicas"], prev, buf, master, m, v, work)
+                    # float64 local steps; own bf16 copy from the oracle where ambiguous
+                    mw, mm, mv = c["p0"].copy(), c["m0"].copy(), c["v0"].copy()
+                    ww = torch_bf16_bits(mw)
+                    for a in range(A):
+                        g = orc.shard_reduce(c["grads"][a * R:(a + 1) * R], c["grad_scale"])
+                        orc.adamw_step(c["seg_off"], c["seg_decay"], STD_HP, c["step0"] + a, g,
+                                       mw, mm, mv, ww)
+                    gsteps = [_bf_reduce(c["grads"][a * R:(a + 1) * R], c["grad_scale"])
+                              for a in range(A)]
+                    (p, e_p), (mm64, em), (vv64, ev) = _bf_steps(
+                        STD_HP, c["seg_off"], c["seg_decay"], c["step0"], gsteps, c["p0"],
+                        c["m0"], c["v0"])
+                    own, _ = _resolve_bf16(p, e_p, ww)
+                    reps = [own if k == c["self_group"] else c["replicas"][k] for k in range(G)]
+                    xbar, ex = _bf_fedavg(c["weights"], reps)
+                    p64, ep, b64, eb = _bf_outer(oh, p64, ep, b64, eb, xbar, ex)
+                    tag = "round_outer %s R=%d G=%d A=%d" % (oh, R, G, A)
+                    _check_close(tag + " master", master, p64, ep)
+                    _check_close(tag + " prev", prev, p64, ep)
+                    _check_close(tag + " buf", buf, b64, eb)
+                    _check_close(tag + " m", m, mm64, em)
+                    assert np.array_equal(work, torch_bf16_bits(master)), tag
+
+
 ALL_PINS = [
     pin_bf16_decode_all_patterns,
     pin_bf16_encode_matches_torch,
@@ -738,4 +871,8 @@ ALL_PINS = [
     pin_broadcast_recv,
     pin_hsdp_round_brute_force_16,
     pin_hsdp_one_replica_is_fsdp,
+    pin_outer_vs_torch_sgd,
+    pin_outer_unit_lr_no_momentum_is_fedavg,
+    pin_outer_fixed_point,
+    pin_round_outer_brute_force_16,
 ]

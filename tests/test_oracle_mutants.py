@@ -79,6 +79,15 @@ MUTANTS = {
     "wire_wrong_peer_index": [("orc_bf16_to_f32(grads[r][i])", "orc_bf16_to_f32(grads[0][i])", 1)],
     "hsdp_same_step_number": [("h, step0 + a, g, master", "h, step0, g, master", 1)],
     "hsdp_reuses_first_grads": [("grads + (size_t)a * (size_t)R", "grads", 1)],
+    "outer_delta_sign": [("const float delta = prev[i] - xbar;", "const float delta = xbar - prev[i];")],
+    "outer_no_momentum": [("const float b = (mu * buf[i]) + delta;", "const float b = delta;")],
+    "outer_nesterov_uses_old_buf": [("(delta + (mu * b))", "(delta + (mu * buf[i]))")],
+    "outer_nesterov_inverted": [("o->nesterov ? (delta + (mu * b)) : b", "o->nesterov ? b : (delta + (mu * b))")],
+    "outer_buf_not_stored": [("    buf[i] = b;\n", "")],
+    "outer_prev_not_updated": [("    prev[i] = p;\n", "")],
+    "outer_lr_ignored": [("const float p = prev[i] - (eta * d);", "const float p = prev[i] - d;")],
+    "outer_unnormalised_weights": [("if (orc_norm_weights(G, weights, wn) != 0) {", "if (orc_norm_weights(G, weights, wn) != 0 || (wn[0] = weights[0], 0)) {", 1)],
+    "round_outer_skips_outer": [("rc = orc_fedopt(n, G, reps, weights, o, prev, buf, master, working);", "rc = orc_fedavg(n, G, reps, weights, master, working);")],
     "hsdp_stale_own_replica": [("reps[k] = (k == self_group) ? working : replicas[k];",
                                 "reps[k] = (k == self_group) ? replicas[(k + 1) % G] : replicas[k];", 1)],
 }
