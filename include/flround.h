@@ -224,6 +224,43 @@ int fl_round(const fl_layout* layout, const fl_round_cfg* cfg, const uint16_t* c
              uint16_t* working, float* seg_sumsq, void* stream);
 
 /* ------------------------------------------------------------------------
+ * Outer optimiser (Section 3: DiLoCo and Photon pair the inner AdamW with an
+ * outer Nesterov-momentum step, FedOpt / FedMom; Section 4.1: aggregation
+ * strategies that build on FedAvg).  The outer gradient is the global model
+ * at the start of the round (prev) minus the FedAvg average of the groups'
+ * models:
+ *     xbar = the FedAvg sum of fl_fedavg, in the same order
+ *     delta = prev[i] - xbar
+ *     buf[i] = momentum * buf[i] + delta
+ *     d = nesterov ? delta + momentum * buf[i] : buf[i]
+ *     p = prev[i] - lr * d
+ *     master_out[i] = prev[i] = p; working_out[i] = bf16(p)
+ * (torch's SGD with dampening 0 on the outer gradient; with lr = 1 and
+ * momentum = 0 it is FedAvg up to the rounding of prev - (prev - xbar)).
+ * prev, buf: device, N floats each, caller-owned outer state (start: prev =
+ * the global model every group began the round from, buf = 0).
+ *
+ * fl_fedopt: arguments as fl_fedavg plus the outer state; prev, buf and
+ *   master_out pairwise distinct.  Requirements: finite lr >= 0,
+ *   0 <= momentum <= 1.
+ * fl_round_outer: fl_round with the outer step in place of FedAvg; prev and
+ *   buf distinct from master, m, v and each other.
+ * ---------------------------------------------------------------------- */
+typedef struct {
+  float lr;       /* outer learning rate (DiLoCo: 0.7)   */
+  float momentum; /* outer momentum (DiLoCo: 0.9)        */
+  int nesterov;   /* nonzero: Nesterov form              */
+} fl_outer_hparams;
+
+int fl_fedopt(const fl_layout* layout, int G, const uint16_t* const* replicas,
+              const float* weights, const uint64_t* replica_fp, const fl_outer_hparams* outer,
+              float* prev, float* buf, float* master_out, uint16_t* working_out, void* stream);
+int fl_round_outer(const fl_layout* layout, const fl_round_cfg* cfg, const fl_outer_hparams* outer,
+                   const uint16_t* const* grads, const uint16_t* const* replicas, float* prev,
+                   float* buf, float* master, float* m, float* v, uint16_t* working,
+                   float* seg_sumsq, void* stream);
+
+/* ------------------------------------------------------------------------
  * FL+HSDP (Section 2, HSDP; Section 4.1, Eq. (2); Section 4.2, Eq. (5)).
  * Each federation group is an HSDP deployment: H replicas of an S-way
  * sharding group.  Gradients are averaged in two tiers (Section 5.1): over

@@ -77,6 +77,11 @@ struct FedArgs {
   int G;
   float* master;
   uint16_t* working;
+  // outer optimiser step (prev == null: plain FedAvg)
+  float* prev;
+  float* buf;
+  float eta, mu;
+  int nesterov;
 };
 
 hipError_t launch_local_step(const StepArgs& a, int grid, hipStream_t st);

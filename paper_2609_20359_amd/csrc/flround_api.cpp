@@ -209,10 +209,24 @@ int enqueue_local_step(const fl_layout* lay, const fl_adamw_hparams& h, int64_t 
   return rc;
 }
 
+bool outer_ok(const fl_outer_hparams* o) {
+  return o && finite(o->lr) && finite(o->momentum) && o->lr >= 0.f && o->momentum >= 0.f &&
+         o->momentum <= 1.f;
+}
+
 int enqueue_fedavg(const fl_layout* lay, int G, const uint16_t* const* reps, const float* wn,
-                   float* master, uint16_t* working, hipStream_t st) {
+                   float* master, uint16_t* working, hipStream_t st,
+                   const fl_outer_hparams* outer = nullptr, float* prev = nullptr,
+                   float* buf = nullptr) {
   flr::FedArgs f;
   std::memset(&f, 0, sizeof f);
+  if (outer) {
+    f.prev = prev;
+    f.buf = buf;
+    f.eta = outer->lr;
+    f.mu = outer->momentum;
+    f.nesterov = outer->nesterov ? 1 : 0;
+  }
   f.n = lay->L.n;
   f.G = G;
   for (int g = 0; g < G; ++g) {
@@ -241,7 +255,7 @@ const char* fl_status_string(int status) {
   }
 }
 
-int fl_version(void) { return (1 << 16) | 1; }
+int fl_version(void) { return (1 << 16) | 2; }
 
 int fl_set_blocks_per_cu(int blocks_per_cu) {
   const int prev = g_blocks_per_cu;
@@ -624,9 +638,57 @@ int fl_round_hsdp(const fl_layout* layout, const fl_round_cfg* cfg, const fl_hsd
   return rc != FL_OK ? rc : rc2;
 }
 
+int fl_fedopt(const fl_layout* layout, int G, const uint16_t* const* replicas,
+              const float* weights, const uint64_t* replica_fp, const fl_outer_hparams* outer,
+              float* prev, float* buf, float* master_out, uint16_t* working_out, void* stream) {
+  if (!layout || G < 1 || G > FL_MAX_GROUPS || !replicas || !outer_ok(outer))
+    return FL_ERR_INVALID;
+  const int64_t n = layout->L.n;
+  float wn[FL_MAX_GROUPS];
+  int rc = normalise_weights(G, weights, wn);
+  if (rc != FL_OK) return rc;
+  for (int g = 0; g < G; ++g)
+    if ((rc = dev_ptr(replicas[g], n)) != FL_OK) return rc;
+  if ((rc = dev_ptr(prev, n)) != FL_OK) return rc;
+  if ((rc = dev_ptr(buf, n)) != FL_OK) return rc;
+  if ((rc = dev_ptr(master_out, n)) != FL_OK) return rc;
+  if ((rc = dev_ptr(working_out, n)) != FL_OK) return rc;
+  if (n > 0 && (prev == buf || prev == master_out || buf == master_out)) return FL_ERR_INVALID;
+  if (replica_fp)
+    for (int g = 0; g < G; ++g)
+      if (replica_fp[g] != layout->fingerprint) return FL_ERR_LAYOUT;
+  if ((rc = check_device(layout)) != FL_OK) return rc;
+  if (n == 0) return FL_OK;
+  return enqueue_fedavg(layout, G, replicas, wn, master_out, working_out,
+                        static_cast<hipStream_t>(stream), outer, prev, buf);
+}
+
+// Shared body of fl_round and fl_round_outer (outer == nullptr: FedAvg).
+static int round_impl(const fl_layout* layout, const fl_round_cfg* cfg,
+                      const fl_outer_hparams* outer, const uint16_t* const* grads,
+                      const uint16_t* const* replicas, float* prev, float* buf, float* master,
+                      float* m, float* v, uint16_t* working, float* seg_sumsq, void* stream);
+
+int fl_round_outer(const fl_layout* layout, const fl_round_cfg* cfg, const fl_outer_hparams* outer,
+                   const uint16_t* const* grads, const uint16_t* const* replicas, float* prev,
+                   float* buf, float* master, float* m, float* v, uint16_t* working,
+                   float* seg_sumsq, void* stream) {
+  if (!outer_ok(outer)) return FL_ERR_INVALID;
+  return round_impl(layout, cfg, outer, grads, replicas, prev, buf, master, m, v, working,
+                    seg_sumsq, stream);
+}
+
 int fl_round(const fl_layout* layout, const fl_round_cfg* cfg, const uint16_t* const* grads,
              const uint16_t* const* replicas, float* master, float* m, float* v,
              uint16_t* working, float* seg_sumsq, void* stream) {
+  return round_impl(layout, cfg, nullptr, grads, replicas, nullptr, nullptr, master, m, v,
+                    working, seg_sumsq, stream);
+}
+
+static int round_impl(const fl_layout* layout, const fl_round_cfg* cfg,
+                      const fl_outer_hparams* outer, const uint16_t* const* grads,
+                      const uint16_t* const* replicas, float* prev, float* buf, float* master,
+                      float* m, float* v, uint16_t* working, float* seg_sumsq, void* stream) {
   if (!layout || !cfg || !grads || !replicas) return FL_ERR_INVALID;
   const fl_round_cfg& c = *cfg;
   const int64_t n = layout->L.n;
@@ -655,6 +717,16 @@ int fl_round(const fl_layout* layout, const fl_round_cfg* cfg, const uint16_t* c
   if ((rc = dev_ptr(v, n)) != FL_OK) return rc;
   if ((rc = dev_ptr(working, n)) != FL_OK) return rc;
   if (n > 0 && (master == m || master == v || m == v)) return FL_ERR_INVALID;
+  if (outer) {
+    if ((rc = dev_ptr(prev, n)) != FL_OK) return rc;
+    if ((rc = dev_ptr(buf, n)) != FL_OK) return rc;
+    if (n > 0) {
+      const void* state[] = {master, m, v, prev, buf};
+      for (int i = 0; i < 5; ++i)
+        for (int j = i + 1; j < 5; ++j)
+          if (state[i] == state[j]) return FL_ERR_INVALID;
+    }
+  }
   if (seg_sumsq && (reinterpret_cast<uintptr_t>(seg_sumsq) & 3u)) return FL_ERR_ALIGN;
   if (c.replica_fp)
     for (int g = 0; g < c.G; ++g)
@@ -680,7 +752,8 @@ int fl_round(const fl_layout* layout, const fl_round_cfg* cfg, const uint16_t* c
                               st);
   }
   if (rc == FL_OK) rc = record(c.A);
-  if (rc == FL_OK && n > 0) rc = enqueue_fedavg(layout, c.G, reps, wn, master, working, st);
+  if (rc == FL_OK && n > 0)
+    rc = enqueue_fedavg(layout, c.G, reps, wn, master, working, st, outer, prev, buf);
   if (rc == FL_OK) rc = record(c.A + 1);
   const int rc2 = ws.release();
   return rc != FL_OK ? rc : rc2;

@@ -299,15 +299,25 @@ __global__ void __launch_bounds__(kBlock) k_step(const StepArgs a) {
 }
 
 // FedAvg: master = sum_g w_g * f32(rep_g), ascending g; working = bf16(master).
-template <int GT>
+// OUTER: the outer optimiser step on that average instead:
+//   delta = prev - xbar; buf = mu * buf + delta;
+//   d = nesterov ? delta + mu * buf : buf; p = prev - eta * d;
+//   master = prev = p; working = bf16(p).
+template <int GT, bool OUTER>
 __global__ void __launch_bounds__(kBlock) k_fedavg(const FedArgs a) {
   const int64_t nvec = (a.n + kVec - 1) / kVec;
   const int64_t stride = (int64_t)gridDim.x * kBlock;
   for (int64_t vi = (int64_t)blockIdx.x * kBlock + threadIdx.x; vi < nvec; vi += stride) {
     const int64_t base = vi * kVec;
     const int64_t left = a.n - base;
+    const int cnt = left >= kVec ? kVec : (int)left;
     float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-    if (left >= kVec) {
+    float prev[8], buf[8];
+    if (cnt == kVec) {
+      if constexpr (OUTER) {
+        load_f32x8(a.prev + base, prev);
+        load_f32x8(a.buf + base, buf);
+      }
       if constexpr (GT > 0) {
         u32x4 w[GT];
 #pragma unroll
@@ -326,19 +336,45 @@ __global__ void __launch_bounds__(kBlock) k_fedavg(const FedArgs a) {
             if (k0 + k < a.G) fma_free_bf16x8(acc, a.w[k0 + k], w[k]);
         }
       }
-      store_f32x8(a.master + base, acc);
-      st(reinterpret_cast<u32x4*>(a.working + base), pack_bf16x8(acc));
     } else {
-      const int cnt = (int)left;
       for (int e = 0; e < cnt; ++e) {
         float s = 0.f;
         for (int k = 0; k < a.G; ++k)
           s = s + (a.w[k] * __uint_as_float((uint32_t)a.reps[k][base + e] << 16));
         acc[e] = s;
+        if constexpr (OUTER) {
+          prev[e] = a.prev[base + e];
+          buf[e] = a.buf[base + e];
+        }
       }
+    }
+    if constexpr (OUTER) {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        if (e < cnt) {
+          const float delta = prev[e] - acc[e];
+          const float b = (a.mu * buf[e]) + delta;
+          const float d = a.nesterov ? (delta + (a.mu * b)) : b;
+          acc[e] = prev[e] - (a.eta * d);
+          buf[e] = b;
+        }
+      }
+    }
+    if (cnt == kVec) {
+      store_f32x8(a.master + base, acc);
+      st(reinterpret_cast<u32x4*>(a.working + base), pack_bf16x8(acc));
+      if constexpr (OUTER) {
+        store_f32x8(a.prev + base, acc);
+        store_f32x8(a.buf + base, buf);
+      }
+    } else {
       for (int e = 0; e < cnt; ++e) {
         a.master[base + e] = acc[e];
         a.working[base + e] = (uint16_t)to_bf16(acc[e]);
+        if constexpr (OUTER) {
+          a.prev[base + e] = acc[e];
+          a.buf[base + e] = buf[e];
+        }
       }
     }
   }
@@ -452,15 +488,20 @@ hipError_t launch_adamw(const StepArgs& a, int grid, hipStream_t st) {
   return launch((const void*)k_step<1, 2, false>, a, grid, st);
 }
 
-hipError_t launch_fedavg(const FedArgs& a, int grid, hipStream_t st) {
+template <bool OUTER>
+hipError_t dispatch_fedavg(const FedArgs& a, int grid, hipStream_t st) {
   switch (a.G) {
-    case 1: return launch((const void*)k_fedavg<1>, a, grid, st);
-    case 2: return launch((const void*)k_fedavg<2>, a, grid, st);
-    case 4: return launch((const void*)k_fedavg<4>, a, grid, st);
-    case 8: return launch((const void*)k_fedavg<8>, a, grid, st);
-    case 16: return launch((const void*)k_fedavg<16>, a, grid, st);
-    default: return launch((const void*)k_fedavg<0>, a, grid, st);
+    case 1: return launch((const void*)k_fedavg<1, OUTER>, a, grid, st);
+    case 2: return launch((const void*)k_fedavg<2, OUTER>, a, grid, st);
+    case 4: return launch((const void*)k_fedavg<4, OUTER>, a, grid, st);
+    case 8: return launch((const void*)k_fedavg<8, OUTER>, a, grid, st);
+    case 16: return launch((const void*)k_fedavg<16, OUTER>, a, grid, st);
+    default: return launch((const void*)k_fedavg<0, OUTER>, a, grid, st);
   }
+}
+
+hipError_t launch_fedavg(const FedArgs& a, int grid, hipStream_t st) {
+  return a.prev ? dispatch_fedavg<true>(a, grid, st) : dispatch_fedavg<false>(a, grid, st);
 }
 
 hipError_t launch_seg_finalize(const LayoutDev& L, const float* partials, double* chunk_sums,

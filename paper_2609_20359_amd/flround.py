@@ -29,7 +29,7 @@ EXPORTS = ("fl_status_string", "fl_version", "fl_layout_create", "fl_layout_dest
            "fl_layout_numel", "fl_layout_num_segments", "fl_fingerprint",
            "fl_layout_fingerprint", "fl_shard_reduce", "fl_adamw_step", "fl_local_step",
            "fl_fedavg", "fl_round", "fl_set_blocks_per_cu", "fl_shard_reduce_wire",
-           "fl_broadcast_recv", "fl_round_hsdp")
+           "fl_broadcast_recv", "fl_round_hsdp", "fl_fedopt", "fl_round_outer")
 
 _P = ctypes.c_void_p
 
@@ -52,6 +52,16 @@ class RoundCfg(ctypes.Structure):
                 ("weights", ctypes.POINTER(ctypes.c_float)),
                 ("replica_fp", ctypes.POINTER(ctypes.c_uint64)),
                 ("phase_events", ctypes.POINTER(ctypes.c_void_p))]
+
+
+class OuterHparams(ctypes.Structure):
+    _fields_ = [("lr", ctypes.c_float), ("momentum", ctypes.c_float), ("nesterov", ctypes.c_int)]
+
+
+def outer_hparams(oh):
+    if isinstance(oh, OuterHparams):
+        return oh
+    return OuterHparams(oh["lr"], oh["momentum"], 1 if oh.get("nesterov", True) else 0)
 
 
 class HsdpCfg(ctypes.Structure):
@@ -95,6 +105,10 @@ def lib():
         L.fl_broadcast_recv.argtypes = [_P, _P, _P, _P, _P]
         L.fl_round_hsdp.argtypes = [_P, ctypes.POINTER(RoundCfg), ctypes.POINTER(HsdpCfg), _P, _P,
                                     _P, _P, _P, _P, _P, _P, _P, _P, _P]
+        L.fl_fedopt.argtypes = [_P, ctypes.c_int, _P, _P, _P, ctypes.POINTER(OuterHparams), _P, _P,
+                                _P, _P, _P]
+        L.fl_round_outer.argtypes = [_P, ctypes.POINTER(RoundCfg), ctypes.POINTER(OuterHparams),
+                                     _P, _P, _P, _P, _P, _P, _P, _P, _P, _P]
         L.fl_set_blocks_per_cu.argtypes = [ctypes.c_int]
         L.fl_set_blocks_per_cu.restype = ctypes.c_int
         _lib = L
@@ -268,6 +282,28 @@ def fl_round_hsdp(layout, cfg, hcfg, grads, replica_wires, wire, replicas, bcast
                              _ptr(bcast_master), _ptr(master), _ptr(m), _ptr(v), _ptr(working),
                              _ptr(seg_sumsq), _stream(stream))
     _check(rc, "fl_round_hsdp")
+
+
+def fl_fedopt(layout, replicas, weights, outer, prev, buf, master_out, working_out,
+              replica_fp=None, stream=None):
+    G = len(replicas)
+    w = (ctypes.c_float * G)(*[float(x) for x in weights])
+    fp = None if replica_fp is None else (ctypes.c_uint64 * G)(*[int(x) for x in replica_fp])
+    o = outer_hparams(outer)
+    rc = lib().fl_fedopt(layout.handle, G, _ptr_array(replicas), w, fp, ctypes.byref(o),
+                         _ptr(prev), _ptr(buf), _ptr(master_out), _ptr(working_out),
+                         _stream(stream))
+    _check(rc, "fl_fedopt")
+
+
+def fl_round_outer(layout, cfg, outer, grads, replicas, prev, buf, master, m, v, working,
+                   seg_sumsq=None, stream=None):
+    o = outer_hparams(outer)
+    rc = lib().fl_round_outer(layout.handle, ctypes.byref(cfg), ctypes.byref(o),
+                              _ptr_array(grads), _ptr_array(replicas), _ptr(prev), _ptr(buf),
+                              _ptr(master), _ptr(m), _ptr(v), _ptr(working), _ptr(seg_sumsq),
+                              _stream(stream))
+    _check(rc, "fl_round_outer")
 
 
 # ---- HIP events (for fl_round's per-phase timing) -------------------------

@@ -35,6 +35,8 @@ class DeviceInputs:
 
         self.replica_wires = [None if sp is None else wire_buf(sp) for sp in w.wire_specs] or None
         self.wire = torch.empty(n, **bf) if w.H > 1 else None
+        self.prev = dev_fill(torch.empty(n, **f32), w.master_spec) if w.outer else None
+        self.buf = torch.zeros(n, **f32) if w.outer else None
         self.bcast = None if w.bcast_spec is None else dev_fill(torch.empty(n, **f32),
                                                                  w.bcast_spec)
 
@@ -42,7 +44,7 @@ class DeviceInputs:
         t = [self.master, self.m, self.v, self.working] + self.grad_arrays + \
             [r for r in self.replicas if r is not None] + \
             list({id(r): r for r in (self.replica_wires or []) if r is not None}.values()) + \
-            [x for x in (self.wire, self.bcast) if x is not None]
+            [x for x in (self.wire, self.bcast, self.prev, self.buf) if x is not None]
         return sum(x.numel() * x.element_size() for x in t)
 
 
@@ -83,3 +85,5 @@ class HostInputs:
         self.replicas = [None if sp is None else fill(sp) for sp in w.replica_specs]
         self.replica_wires = [None if sp is None else fill(sp) for sp in w.wire_specs] or None
         self.bcast = None if w.bcast_spec is None else fill(w.bcast_spec)
+        self.prev = fill(w.master_spec) if w.outer else None
+        self.buf = np.zeros(n, np.float32) if w.outer else None

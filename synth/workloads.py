@@ -118,6 +118,9 @@ class Workload:
     hsdp_member: bool = True
     wire_specs: list = field(default_factory=list)   # A*H entries, None at own index
     bcast_spec: object = None
+    # outer optimiser (None: plain FedAvg): dict(lr, momentum, nesterov); the
+    # outer state starts at prev = the initial master, buf = 0
+    outer: Optional[dict] = None
 
     def __post_init__(self):
         if self.grad_scale is None:
@@ -150,6 +153,8 @@ class Workload:
         instead."""
         if self.H > 1 and not self.hsdp_member:
             return 4 + 4 + 2
+        if self.outer is not None:
+            return 2 * self.G + 4 + 2 + 16   # + prev and buf read and written
         return 2 * self.G + 4 + 2
 
     def round_bytes(self):
@@ -160,6 +165,8 @@ class Workload:
                  A=self.A, distinct_grad_arrays=len(self.grad_specs))
         if self.H > 1:
             d.update(H=self.H, replica=self.replica, fedavg_member=self.hsdp_member)
+        if self.outer is not None:
+            d.update(outer=self.outer)
         return d
 
 
@@ -181,7 +188,7 @@ def _normal_grads(n_arrays, seed, std=GRAD_STD):
 def make_workload(name, seg_sizes, seg_decay, R, G, A, *, weights=None, seed=0,
                   distinct_grads=True, student=False, own_drift=False, hp=None,
                   self_group=0, step0=1, grad_scale=None, note="", H=1, replica=0,
-                  hsdp_member=True):
+                  hsdp_member=True, outer=None):
     """General constructor used by the named workloads and by the tests.
 
     distinct_grads: A*R distinct gradient arrays (else R arrays reused by
@@ -223,7 +230,8 @@ def make_workload(name, seg_sizes, seg_decay, R, G, A, *, weights=None, seed=0,
                     replica_specs=_replicas(G, self_group, seed), working_spec=working,
                     hp=dict(hp or ADAMW), self_group=self_group, step0=step0,
                     grad_scale=grad_scale, note=note, H=H, replica=replica,
-                    hsdp_member=hsdp_member, wire_specs=wires, bcast_spec=bcast)
+                    hsdp_member=hsdp_member, wire_specs=wires, bcast_spec=bcast,
+                    outer=None if outer is None else dict(outer))
 
 
 def tiny(seed=0):
@@ -282,9 +290,21 @@ def hsdp_s4_h2(seed=0, member=True):
                          hsdp_member=member)
 
 
+DILOCO_OUTER = dict(lr=0.7, momentum=0.9, nesterov=True)
+
+
+def llama8b_s8_outer(seed=0):
+    """The Llama-3.1-8B S=8 round with the outer Nesterov-momentum step
+    (outer lr 0.7, momentum 0.9, as DiLoCo uses) in place of plain FedAvg."""
+    sizes, dec = llama31_8b_segments(8)
+    return make_workload("llama31_8b_fsdp_s8_r8_g4_a8_fedmom", sizes, dec, R=8, G=4, A=8,
+                         seed=seed, distinct_grads=False, outer=DILOCO_OUTER)
+
+
 ALL = dict(tiny=tiny, llama8b_s8=llama8b_s8, fedavg_heavy=fedavg_heavy, hsdp_s4=hsdp_s4,
            stress=stress, hsdp_s4_h2=hsdp_s4_h2,
-           hsdp_s4_h2_recv=lambda seed=0: hsdp_s4_h2(seed, member=False))
+           hsdp_s4_h2_recv=lambda seed=0: hsdp_s4_h2(seed, member=False),
+           llama8b_s8_outer=llama8b_s8_outer)
 
 
 def sample_indices(w, n_random=1 << 16, seed=1, full_segments=4, max_full=4096):

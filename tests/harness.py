@@ -47,6 +47,11 @@ def oracle_round(orc, w: Workload, host: HostInputs, seg_off=None, seg_decay=Non
     arrays.  Returns the per-step per-segment sums of squares or None."""
     seg_off = w.seg_offsets if seg_off is None else seg_off
     seg_decay = w.seg_decay if seg_decay is None else seg_decay
+    if w.outer is not None:
+        return orc.round_outer(seg_off, seg_decay, w.R, w.G, w.A, w.self_group, w.grad_scale,
+                               w.hp, w.step0, w.weights, w.outer, host.grads, host.replicas,
+                               host.prev, host.buf, host.master, host.m, host.v, host.working,
+                               want_sumsq=want_sumsq)
     if w.H > 1:
         return orc.round_hsdp(seg_off, seg_decay, w.R, w.H, w.replica, 1.0 / w.H, w.hsdp_member,
                               w.G, w.A, w.self_group, w.grad_scale, w.hp, w.step0, w.weights,
@@ -68,7 +73,10 @@ def gpu_round(P, layout, w: Workload, dev: DeviceInputs, seg_sumsq=None, phase_e
     """One fl_round (or fl_round_hsdp when w.H > 1) through the C ABI."""
     if cfg is None:
         cfg = round_cfg(P, w, phase_events=phase_events)
-    if w.H > 1:
+    if w.outer is not None:
+        P.fl_round_outer(layout, cfg, w.outer, dev.grads, dev.replicas, dev.prev, dev.buf,
+                         dev.master, dev.m, dev.v, dev.working, seg_sumsq=seg_sumsq)
+    elif w.H > 1:
         hc = P.make_hsdp_cfg(w.H, w.replica, 1.0 / w.H, w.hsdp_member)
         P.fl_round_hsdp(layout, cfg, hc, dev.grads, dev.replica_wires, dev.wire,
                         dev.replicas if w.hsdp_member else None,

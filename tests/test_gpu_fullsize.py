@@ -13,7 +13,8 @@ from synth import workloads as W
 
 pytestmark = pytest.mark.gpu
 
-WORKLOADS = ["llama8b_s8", "fedavg_heavy", "hsdp_s4", "stress", "hsdp_s4_h2", "hsdp_s4_h2_recv"]
+WORKLOADS = ["llama8b_s8", "fedavg_heavy", "hsdp_s4", "stress", "hsdp_s4_h2", "hsdp_s4_h2_recv",
+             "llama8b_s8_outer"]
 
 
 def _say(*a):
@@ -57,6 +58,8 @@ def test_full_size_round_sampled(env, name):
     idx_dev = torch.from_numpy(idx).cuda()
     got = dict(master=H.gather_f32(dev.master, idx_dev), m=H.gather_f32(dev.m, idx_dev),
                v=H.gather_f32(dev.v, idx_dev), working=H.gather_u16(dev.working, idx_dev))
+    if w.outer is not None:
+        got_outer = dict(master=H.gather_f32(dev.prev, idx_dev), m=H.gather_f32(dev.buf, idx_dev))
     ss_gpu = ss.cpu().numpy().reshape(w.A, w.n_seg)
     del dev
     torch.cuda.empty_cache()
@@ -66,6 +69,9 @@ def test_full_size_round_sampled(env, name):
     ss_ref = H.oracle_round(orc, w, host, seg_off=off, seg_decay=dec, want_sumsq=True)
     ref = dict(master=host.master, m=host.m, v=host.v, working=host.working)
     errs = H.assert_state_parity(name, got, ref, bitwise=True)
+    if w.outer is not None:
+        H.assert_state_parity(name + " outer state", got_outer,
+                              dict(master=host.prev, m=host.buf), bitwise=True)
     for s, cs in cmap.items():
         H.assert_sumsq("%s seg %d" % (name, s), ss_gpu[:, s], ss_ref[:, cs])
     lay.close()
