@@ -42,20 +42,24 @@ def _declare(lib):
     lib.orc_fedavg.argtypes = [ctypes.c_int64, ctypes.c_int, _P, _P, _P, _P]
     lib.orc_round.argtypes = [ctypes.c_int64, _P, _P, ctypes.c_int, ctypes.c_int, ctypes.c_int,
                               ctypes.c_int, ctypes.c_float, ctypes.POINTER(Hparams),
-                              ctypes.c_int64, _P, _P, _P, _P, _P, _P, _P, _P]
+                              ctypes.c_int64, _P, _P, _P, _P, _P, _P, _P, _P, _P]
+    lib.orc_lr_cosine.argtypes = [ctypes.c_int64, ctypes.c_int64, ctypes.c_int64, ctypes.c_float,
+                                  ctypes.c_float]
+    lib.orc_lr_cosine.restype = ctypes.c_float
     lib.orc_shard_reduce_wire.argtypes = [ctypes.c_int64, ctypes.c_int, _P, ctypes.c_float, _P]
     lib.orc_broadcast_recv.argtypes = [ctypes.c_int64, _P, _P, _P]
     lib.orc_round_hsdp.argtypes = [ctypes.c_int64, _P, _P, ctypes.c_int, ctypes.c_int,
                                    ctypes.c_int, ctypes.c_float, ctypes.c_int, ctypes.c_int,
                                    ctypes.c_int, ctypes.c_int, ctypes.c_float,
                                    ctypes.POINTER(Hparams), ctypes.c_int64, _P, _P, _P, _P, _P,
-                                   _P, _P, _P, _P, _P]
+                                   _P, _P, _P, _P, _P, _P]
     lib.orc_fedopt.argtypes = [ctypes.c_int64, ctypes.c_int, _P, _P, ctypes.POINTER(Outer), _P,
                                _P, _P, _P]
     lib.orc_round_outer.argtypes = [ctypes.c_int64, _P, _P, ctypes.c_int, ctypes.c_int,
                                     ctypes.c_int, ctypes.c_int, ctypes.c_float,
                                     ctypes.POINTER(Hparams), ctypes.c_int64, _P,
-                                    ctypes.POINTER(Outer), _P, _P, _P, _P, _P, _P, _P, _P, _P]
+                                    ctypes.POINTER(Outer), _P, _P, _P, _P, _P, _P, _P, _P, _P,
+                                    _P]
     return lib
 
 
@@ -81,6 +85,19 @@ def _c(a, dtype):
 
 def _ptr_array(arrays):
     return (ctypes.c_void_p * len(arrays))(*[a.ctypes.data for a in arrays])
+
+
+_keep = []
+
+
+def _lr_ptr(step_lr, A):
+    if step_lr is None:
+        return None
+    a = np.ascontiguousarray(step_lr, dtype=np.float32)
+    assert a.size == A, "step_lr needs one value per local step"
+    _keep.append(a)
+    del _keep[:-4]
+    return a.ctypes.data
 
 
 def hparams(hp):
@@ -171,7 +188,7 @@ class Oracle:
 
     def round_hsdp(self, seg_off, seg_decay, R, H, replica, hsdp_scale, member, G, A,
                    self_group, grad_scale, hp, step0, weights, grads, replica_wires, replicas,
-                   bcast, master, m, v, working, want_sumsq=False):
+                   bcast, master, m, v, working, want_sumsq=False, step_lr=None):
         """One FL+HSDP round in place.  replica_wires: A*H arrays (entry
         a*H + replica ignored, may be None); replicas: G arrays or None
         (member only); bcast: fp32 array (non-member only)."""
@@ -194,7 +211,7 @@ class Oracle:
                                    _ptr_array(reps) if reps else None,
                                    None if bc is None else bc.ctypes.data, master.ctypes.data,
                                    m.ctypes.data, v.ctypes.data, working.ctypes.data,
-                                   None if ss is None else ss.ctypes.data)
+                                   None if ss is None else ss.ctypes.data, _lr_ptr(step_lr, A))
         if rc:
             raise ValueError("orc_round_hsdp: %d" % rc)
         return None if ss is None else ss.reshape(A, n_seg)
@@ -216,7 +233,7 @@ class Oracle:
 
     def round_outer(self, seg_off, seg_decay, R, G, A, self_group, grad_scale, hp, step0,
                     weights, oh, grads, replicas, prev, buf, master, m, v, working,
-                    want_sumsq=False):
+                    want_sumsq=False, step_lr=None):
         seg_off = _c(seg_off, np.int64)
         seg_decay = _c(seg_decay, np.uint8)
         n_seg = seg_off.size - 1
@@ -231,13 +248,16 @@ class Oracle:
                                     ctypes.byref(o), _ptr_array(grads), _ptr_array(reps),
                                     prev.ctypes.data, buf.ctypes.data, master.ctypes.data,
                                     m.ctypes.data, v.ctypes.data, working.ctypes.data,
-                                    None if ss is None else ss.ctypes.data)
+                                    None if ss is None else ss.ctypes.data, _lr_ptr(step_lr, A))
         if rc:
             raise ValueError("orc_round_outer: %d" % rc)
         return None if ss is None else ss.reshape(A, n_seg)
 
+    def lr_cosine(self, t, total_steps, warmup_steps, lr_max, lr_min=0.0):
+        return self.L.orc_lr_cosine(t, total_steps, warmup_steps, lr_max, lr_min)
+
     def round(self, seg_off, seg_decay, R, G, A, self_group, grad_scale, hp, step0, weights,
-              grads, replicas, master, m, v, working, want_sumsq=False):
+              grads, replicas, master, m, v, working, want_sumsq=False, step_lr=None):
         """In place on master, m, v, working.  grads: A*R arrays step-major;
         replicas: G arrays (entry self_group ignored, may be None).
         Returns the A x n_seg per-segment sums of squares, or None."""
@@ -253,7 +273,7 @@ class Oracle:
                               self_group, grad_scale, ctypes.byref(h), step0, w.ctypes.data,
                               _ptr_array(grads), _ptr_array(reps), master.ctypes.data,
                               m.ctypes.data, v.ctypes.data, working.ctypes.data,
-                              None if ss is None else ss.ctypes.data)
+                              None if ss is None else ss.ctypes.data, _lr_ptr(step_lr, A))
         if rc:
             raise ValueError("orc_round: %d" % rc)
         return None if ss is None else ss.reshape(A, n_seg)

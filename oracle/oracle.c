@@ -5,6 +5,10 @@
  */
 #include "oracle.h"
 
+#ifndef M_PI
+#define M_PI 3.14159265358979323846
+#endif
+
 #include <math.h>
 #include <stdlib.h>
 #include <string.h>
@@ -123,7 +127,7 @@ int orc_round(int64_t n_seg, const int64_t* seg_off, const uint8_t* seg_decay, i
               int A, int self_group, float grad_scale, const orc_hparams* h, int64_t step0,
               const float* weights, const uint16_t* const* grads,
               const uint16_t* const* replicas, float* master, float* m, float* v,
-              uint16_t* working, double* seg_sumsq) {
+              uint16_t* working, double* seg_sumsq, const float* step_lr) {
   if (n_seg < 0 || !seg_off || R < 1 || G < 1 || A < 1 || self_group < 0 ||
       self_group >= G || !h || step0 < 1 || !weights || !grads || !replicas)
     return -1;
@@ -141,8 +145,10 @@ int orc_round(int64_t n_seg, const int64_t* seg_off, const uint8_t* seg_decay, i
     rc = orc_shard_reduce(n, R, grads + (size_t)a * (size_t)R, grad_scale, g);
     if (rc == 0 && seg_sumsq)
       rc = orc_seg_sumsq(n_seg, seg_off, g, seg_sumsq + (size_t)a * (size_t)n_seg);
+    orc_hparams ha = *h;
+    if (step_lr) ha.lr = step_lr[a];
     if (rc == 0)
-      rc = orc_adamw_step(n_seg, seg_off, seg_decay, h, step0 + a, g, master, m, v, working);
+      rc = orc_adamw_step(n_seg, seg_off, seg_decay, &ha, step0 + a, g, master, m, v, working);
   }
   if (rc == 0) {
     for (int k = 0; k < G; ++k) reps[k] = (k == self_group) ? working : replicas[k];
@@ -178,7 +184,7 @@ int orc_round_hsdp(int64_t n_seg, const int64_t* seg_off, const uint8_t* seg_dec
                    float grad_scale, const orc_hparams* h, int64_t step0, const float* weights,
                    const uint16_t* const* grads, const uint16_t* const* replica_wires,
                    const uint16_t* const* replicas, const float* bcast, float* master, float* m,
-                   float* v, uint16_t* working, double* seg_sumsq) {
+                   float* v, uint16_t* working, double* seg_sumsq, const float* step_lr) {
   if (n_seg < 0 || !seg_off || R < 1 || H < 1 || replica < 0 || replica >= H || A < 1 ||
       !h || step0 < 1 || !grads)
     return -1;
@@ -204,8 +210,10 @@ int orc_round_hsdp(int64_t n_seg, const int64_t* seg_off, const uint8_t* seg_dec
     }
     if (rc == 0 && seg_sumsq)
       rc = orc_seg_sumsq(n_seg, seg_off, g, seg_sumsq + (size_t)a * (size_t)n_seg);
+    orc_hparams ha = *h;
+    if (step_lr) ha.lr = step_lr[a];
     if (rc == 0)
-      rc = orc_adamw_step(n_seg, seg_off, seg_decay, h, step0 + a, g, master, m, v, working);
+      rc = orc_adamw_step(n_seg, seg_off, seg_decay, &ha, step0 + a, g, master, m, v, working);
   }
   if (rc == 0) {
     if (member) {
@@ -256,7 +264,8 @@ int orc_round_outer(int64_t n_seg, const int64_t* seg_off, const uint8_t* seg_de
                     int A, int self_group, float grad_scale, const orc_hparams* h, int64_t step0,
                     const float* weights, const orc_outer* o, const uint16_t* const* grads,
                     const uint16_t* const* replicas, float* prev, float* buf, float* master,
-                    float* m, float* v, uint16_t* working, double* seg_sumsq) {
+                    float* m, float* v, uint16_t* working, double* seg_sumsq,
+                    const float* step_lr) {
   if (n_seg < 0 || !seg_off || R < 1 || G < 1 || A < 1 || self_group < 0 ||
       self_group >= G || !h || !o || step0 < 1 || !weights || !grads || !replicas)
     return -1;
@@ -269,8 +278,10 @@ int orc_round_outer(int64_t n_seg, const int64_t* seg_off, const uint8_t* seg_de
     rc = orc_shard_reduce(n, R, grads + (size_t)a * (size_t)R, grad_scale, g);
     if (rc == 0 && seg_sumsq)
       rc = orc_seg_sumsq(n_seg, seg_off, g, seg_sumsq + (size_t)a * (size_t)n_seg);
+    orc_hparams ha = *h;
+    if (step_lr) ha.lr = step_lr[a];
     if (rc == 0)
-      rc = orc_adamw_step(n_seg, seg_off, seg_decay, h, step0 + a, g, master, m, v, working);
+      rc = orc_adamw_step(n_seg, seg_off, seg_decay, &ha, step0 + a, g, master, m, v, working);
   }
   if (rc == 0) {
     for (int k = 0; k < G; ++k) reps[k] = (k == self_group) ? working : replicas[k];
@@ -279,6 +290,24 @@ int orc_round_outer(int64_t n_seg, const int64_t* seg_off, const uint8_t* seg_de
   free(g);
   free(reps);
   return rc;
+}
+
+float orc_lr_cosine(int64_t t, int64_t total_steps, int64_t warmup_steps, float lr_max,
+                    float lr_min) {
+  const double s = (double)(t - 1);
+  const double w = (double)warmup_steps;
+  double f;
+  if (s < w) {
+    f = s / (w > 1.0 ? w : 1.0);
+  } else {
+    const double span = (double)(total_steps - warmup_steps);
+    const double q = (s - w) / (span > 1.0 ? span : 1.0);
+    const double rho = (double)lr_min / (double)lr_max;
+    f = 0.5 * (1.0 + cos(M_PI * q));
+    f = f * (1.0 - rho) + rho;
+    if (f < 0.0) f = 0.0;
+  }
+  return (float)((double)lr_max * f);
 }
 
 /* Array forms of the two conversions, for the tests. */

@@ -42,6 +42,13 @@
  *       (Section 4.2: FedAvg after the local update every A steps).
  *  (a5) per-segment sum of squares of g for each local step, accumulated in
  *       double in index order.
+ *  (n4) learning-rate schedule (Section 5: cosine decay with 10 % warm-up):
+ *       for optimiser step t (1-based), s = t - 1:
+ *         s < W: f = s / max(1, W)
+ *         else:  q = (s - W) / max(1, T - W); f = 0.5 (1 + cos(pi q));
+ *                f = f (1 - lr_min / lr_max) + lr_min / lr_max; f = max(0, f)
+ *         lr_t = (float)(lr_max * f)                      (all in double)
+ *       A round may give each of its A local steps its own lr.
  *
  * FL+HSDP (Section 2, HSDP; Section 4.1, Eq. (2); Section 4.2, Eq. (5)): the
  * gradient is averaged in two tiers (Section 5.1), first over the sharding
@@ -106,14 +113,19 @@ int orc_adamw_step(int64_t n_seg, const int64_t* seg_off, const uint8_t* seg_dec
 int orc_fedavg(int64_t n, int G, const uint16_t* const* replicas, const float* weights,
                float* master_out, uint16_t* working_out);
 
+/* (n4) scheduled learning rate of optimiser step t. */
+float orc_lr_cosine(int64_t t, int64_t total_steps, int64_t warmup_steps, float lr_max,
+                    float lr_min);
+
 /* (a4) One round.  grads: A*R arrays, step-major.  replicas: G arrays, the
- * entry at self_group is ignored (the working copy is used).  seg_sumsq:
- * NULL or A*n_seg doubles. */
+ * entry at self_group is ignored (the working copy is used).  step_lr: NULL
+ * (every step uses h->lr) or A learning rates.  seg_sumsq: NULL or A*n_seg
+ * doubles. */
 int orc_round(int64_t n_seg, const int64_t* seg_off, const uint8_t* seg_decay, int R, int G,
               int A, int self_group, float grad_scale, const orc_hparams* h, int64_t step0,
               const float* weights, const uint16_t* const* grads,
               const uint16_t* const* replicas, float* master, float* m, float* v,
-              uint16_t* working, double* seg_sumsq);
+              uint16_t* working, double* seg_sumsq, const float* step_lr);
 
 /* (n1) tier 1 to the bf16 wire format. */
 int orc_shard_reduce_wire(int64_t n, int R, const uint16_t* const* grads, float grad_scale,
@@ -133,7 +145,7 @@ int orc_round_hsdp(int64_t n_seg, const int64_t* seg_off, const uint8_t* seg_dec
                    float grad_scale, const orc_hparams* h, int64_t step0, const float* weights,
                    const uint16_t* const* grads, const uint16_t* const* replica_wires,
                    const uint16_t* const* replicas, const float* bcast, float* master, float* m,
-                   float* v, uint16_t* working, double* seg_sumsq);
+                   float* v, uint16_t* working, double* seg_sumsq, const float* step_lr);
 
 typedef struct {
   float lr, momentum;
@@ -151,7 +163,8 @@ int orc_round_outer(int64_t n_seg, const int64_t* seg_off, const uint8_t* seg_de
                     int A, int self_group, float grad_scale, const orc_hparams* h, int64_t step0,
                     const float* weights, const orc_outer* o, const uint16_t* const* grads,
                     const uint16_t* const* replicas, float* prev, float* buf, float* master,
-                    float* m, float* v, uint16_t* working, double* seg_sumsq);
+                    float* m, float* v, uint16_t* working, double* seg_sumsq,
+                    const float* step_lr);
 
 #ifdef __cplusplus
 }

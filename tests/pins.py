@@ -388,16 +388,16 @@ def pin_golden_hand_cases(orc):
 
 # ---- (a4) whole rounds: float64 brute force with error bounds ---------------
 
-def _bf_steps(hp, seg_off, seg_decay, step0, gsteps, p0, m0, v0):
+def _bf_steps(hp, seg_off, seg_decay, step0, gsteps, p0, m0, v0, lrs=None):
     """float64 AdamW over the given per-step (g, bound on |fp32 g - g|) with
-    propagated bounds on the distance of the binary32 evaluation."""
+    propagated bounds on the distance of the binary32 evaluation; lrs: one
+    learning rate per step (else hp's)."""
     h = _hp_f(hp)
     b1, b2, lr, wd, eps = h["beta1"], h["beta2"], h["lr"], h["weight_decay"], h["eps"]
     n = int(seg_off[-1])
     decay_flag = np.zeros(n, bool)
     for s in range(len(seg_off) - 1):
         decay_flag[seg_off[s]:seg_off[s + 1]] = bool(seg_decay[s])
-    decay = np.where(decay_flag, 1.0 - lr * wd, 1.0)
     p = p0.astype(np.float64).copy()
     m = m0.astype(np.float64).copy()
     v = v0.astype(np.float64).copy()
@@ -407,6 +407,9 @@ def _bf_steps(hp, seg_off, seg_decay, step0, gsteps, p0, m0, v0):
     mabs = np.abs(m)
     for a, (g, eg) in enumerate(gsteps):
         t = step0 + a
+        if lrs is not None:
+            lr = float(np.float32(lrs[a]))
+        decay = np.where(decay_flag, 1.0 - lr * wd, 1.0)
         gab = np.abs(g) + eg
         mabs = b1 * mabs + (1 - b1) * gab
         m = b1 * m + (1 - b1) * g
@@ -848,6 +851,71 @@ def pin_round_outer_brute_force_16(orc):
                     assert np.array_equal(work, torch_bf16_bits(master)), tag
 
 
+# ---- learning-rate schedule (cosine decay with warm-up) ----------------------
+
+def pin_lr_cosine_vs_transformers(orc):
+    """Every step of transformers' cosine-with-warm-up schedules (the lr that
+    optimiser step t uses is the scheduler's value after t - 1 steps)."""
+    import transformers
+
+    for T, W, lr_max, lr_min in ((64, 7, 3e-4, 0.0), (1000, 100, 1e-3, 1e-5), (10, 0, 0.5, 0.0),
+                                 (5, 5, 2e-4, 0.0)):
+        base = float(np.float32(lr_max))
+        p = torch.nn.Parameter(torch.zeros(1))
+        opt = torch.optim.SGD([p], lr=base)
+        if lr_min:
+            sch = transformers.get_cosine_with_min_lr_schedule_with_warmup(
+                opt, W, T, min_lr_rate=float(np.float32(lr_min)) / base)
+        else:
+            sch = transformers.get_cosine_schedule_with_warmup(opt, W, T)
+        for t in range(1, T + 3):
+            want = np.float32(opt.param_groups[0]["lr"])
+            got = np.float32(orc.lr_cosine(t, T, W, lr_max, lr_min))
+            assert got == want, "lr at step %d of (T=%d, W=%d): %r vs %r" % (t, T, W, got, want)
+            opt.step()
+            sch.step()
+
+
+def pin_lr_cosine_closed_forms(orc):
+    T, W, lr = 100, 10, np.float32(3e-4)
+    assert orc.lr_cosine(1, T, W, lr) == 0.0, "warm-up starts at 0"
+    assert np.float32(orc.lr_cosine(W + 1, T, W, lr)) == lr, "peak after warm-up"
+    mid = W + 1 + (T - W) // 2
+    assert abs(orc.lr_cosine(mid, T, W, lr) - lr / 2) <= 1e-3 * lr, "half way down"
+    vals = [orc.lr_cosine(t, T, W, lr) for t in range(W + 1, T + 1)]
+    assert all(a >= b for a, b in zip(vals, vals[1:])), "cosine part not decreasing"
+    ramp = [orc.lr_cosine(t, T, W, lr) for t in range(1, W + 2)]
+    assert all(b > a for a, b in zip(ramp, ramp[1:])), "warm-up not increasing"
+
+
+def pin_round_step_lr_brute_force(orc):
+    """A round whose local steps use different learning rates (a schedule)."""
+    r = rng(23)
+    for A in (2, 3):
+        c = _random_round_case(r, 2, 2, A, n=64)
+        lrs = [float(np.float32(x)) for x in r.uniform(1e-4, 5e-2, A)]
+        master, m, v = c["p0"].copy(), c["m0"].copy(), c["v0"].copy()
+        work = torch_bf16_bits(master)
+        orc.round(c["seg_off"], c["seg_decay"], 2, 2, A, c["self_group"], c["grad_scale"], BIG_HP,
+                  c["step0"], c["weights"], c["grads"], c["replicas"], master, m, v, work,
+                  step_lr=lrs)
+        gsteps = [_bf_reduce(c["grads"][a * 2:(a + 1) * 2], c["grad_scale"]) for a in range(A)]
+        (p, ep), (mm, em), (vv, ev) = _bf_steps(BIG_HP, c["seg_off"], c["seg_decay"], c["step0"],
+                                                gsteps, c["p0"], c["m0"], c["v0"], lrs=lrs)
+        _check_close("step_lr m", m, mm, em)
+        _check_close("step_lr v", v, vv, ev)
+        mw, mmm, mv = c["p0"].copy(), c["m0"].copy(), c["v0"].copy()
+        ww = torch_bf16_bits(mw)
+        for a in range(A):
+            g = orc.shard_reduce(c["grads"][a * 2:(a + 1) * 2], c["grad_scale"])
+            orc.adamw_step(c["seg_off"], c["seg_decay"], dict(BIG_HP, lr=lrs[a]), c["step0"] + a,
+                           g, mw, mmm, mv, ww)
+        own, _ = _resolve_bf16(p, ep, ww)
+        reps = [own if k == c["self_group"] else c["replicas"][k] for k in range(2)]
+        xbar, ex = _bf_fedavg(c["weights"], reps)
+        _check_close("step_lr master", master, xbar, ex)
+
+
 ALL_PINS = [
     pin_bf16_decode_all_patterns,
     pin_bf16_encode_matches_torch,
@@ -875,4 +943,7 @@ ALL_PINS = [
     pin_outer_unit_lr_no_momentum_is_fedavg,
     pin_outer_fixed_point,
     pin_round_outer_brute_force_16,
+    pin_lr_cosine_vs_transformers,
+    pin_lr_cosine_closed_forms,
+    pin_round_step_lr_brute_force,
 ]

@@ -53,7 +53,7 @@ MUTANTS = {
                               "for (int k = G - 1; k >= 0; --k) acc = acc + (wn[k] * orc_bf16_to_f32(replicas[k][i]));")],
     "round_stale_own_replica": [("reps[k] = (k == self_group) ? working : replicas[k];",
                                  "reps[k] = (k == self_group) ? replicas[(k + 1) % G] : replicas[k];")],
-    "round_same_step_number": [("h, step0 + a, g, master", "h, step0, g, master")],
+    "round_same_step_number": [("&ha, step0 + a, g, master", "&ha, step0, g, master")],
     "round_skips_fedavg": [("rc = orc_fedavg(n, G, reps, weights, master, working);", "rc = 0;")],
     "round_reuses_first_grads": [("grads + (size_t)a * (size_t)R", "grads")],
     "sumsq_off_by_one": [("for (int64_t i = seg_off[s]; i < seg_off[s + 1]; ++i) sum +=",
@@ -77,7 +77,12 @@ MUTANTS = {
     "bcast_master_through_bf16": [("    master[i] = recv[i];\n    working[i] = orc_f32_to_bf16(recv[i]);",
                                    "    master[i] = orc_bf16_to_f32(orc_f32_to_bf16(recv[i]));\n    working[i] = orc_f32_to_bf16(recv[i]);")],
     "wire_wrong_peer_index": [("orc_bf16_to_f32(grads[r][i])", "orc_bf16_to_f32(grads[0][i])", 1)],
-    "hsdp_same_step_number": [("h, step0 + a, g, master", "h, step0, g, master", 1)],
+    "hsdp_same_step_number": [("&ha, step0 + a, g, master", "&ha, step0, g, master", 1)],
+    "lr_warmup_off_by_one": [("const double s = (double)(t - 1);", "const double s = (double)t;")],
+    "lr_min_ignored": [("    f = f * (1.0 - rho) + rho;\n", "")],
+    "lr_full_cosine_cycle": [("f = 0.5 * (1.0 + cos(M_PI * q));", "f = 0.5 * (1.0 + cos(2.0 * M_PI * q));")],
+    "round_ignores_step_lr": [("    if (step_lr) ha.lr = step_lr[a];\n", "")],
+    "round_first_step_lr_only": [("if (step_lr) ha.lr = step_lr[a];", "if (step_lr) ha.lr = step_lr[0];")],
     "hsdp_reuses_first_grads": [("grads + (size_t)a * (size_t)R", "grads", 1)],
     "outer_delta_sign": [("const float delta = prev[i] - xbar;", "const float delta = xbar - prev[i];")],
     "outer_no_momentum": [("const float b = (mu * buf[i]) + delta;", "const float b = delta;")],
