@@ -200,7 +200,7 @@ int fl_fedavg(const fl_layout* layout, int G, const uint16_t* const* replicas,
  *   see fl_shard_reduce).
  * Configuration: 1 <= R <= FL_MAX_PEERS, 1 <= G <= FL_MAX_GROUPS, A >= 1,
  *   0 <= self_group < G, step0 >= 1, grad_scale finite, h and weights as
- *   above, replica_fp as in fl_fedavg.
+ *   above, replica_fp as in fl_fedavg, step_lr entries finite and >= 0.
  * phase_events: NULL, or host array of A+2 hipEvent_t created by the caller;
  *   event a (a < A) is recorded on `stream` before local step a, event A
  *   before FedAvg, event A+1 after it (per-phase timing of the round, like
@@ -217,11 +217,28 @@ typedef struct {
   const float* weights;      /* host, G FedAvg weights                      */
   const uint64_t* replica_fp;/* NULL or host, G fingerprints                */
   void* const* phase_events; /* NULL or host, A+2 hipEvent_t                */
+  const float* step_lr;      /* NULL or host, A learning rates, one per local
+                                step (overrides h.lr; e.g. fl_lr_cosine)   */
 } fl_round_cfg;
 
 int fl_round(const fl_layout* layout, const fl_round_cfg* cfg, const uint16_t* const* grads,
              const uint16_t* const* replicas, float* master, float* m, float* v,
              uint16_t* working, float* seg_sumsq, void* stream);
+
+/* ------------------------------------------------------------------------
+ * fl_lr_cosine -- the learning rate of optimiser step t (1-based) under
+ * cosine decay with linear warm-up (Section 5: cosine-decay scheduler with
+ * 10 % warm-up steps), in double, rounded once to float; s = t - 1:
+ *     s < warmup:  f = s / max(1, warmup)
+ *     otherwise:   q = (s - warmup) / max(1, total - warmup);
+ *                  f = 0.5 (1 + cos(pi q)); f = f (1 - lr_min/lr_max) + lr_min/lr_max;
+ *                  f = max(0, f)
+ *     returns lr_max * f
+ * The usual warm-up for a 10 % ratio is ceil(0.1 * total).  Host only; a
+ * caller fills fl_round_cfg.step_lr with it for the A steps of a round.
+ * ---------------------------------------------------------------------- */
+float fl_lr_cosine(int64_t t, int64_t total_steps, int64_t warmup_steps, float lr_max,
+                   float lr_min);
 
 /* ------------------------------------------------------------------------
  * Outer optimiser (Section 3: DiLoCo and Photon pair the inner AdamW with an

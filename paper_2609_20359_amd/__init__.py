@@ -10,10 +10,11 @@ thin ctypes binding with the same names.
 from .flround import (FL_MAX_GROUPS, FL_MAX_PEERS, FlError, HipEvents, Layout, fingerprint,
                       fl_adamw_step, fl_broadcast_recv, fl_fedavg, fl_fedopt, fl_local_step,
                       fl_round, fl_round_hsdp, fl_round_outer, fl_shard_reduce,
-                      fl_shard_reduce_wire, lib, make_hsdp_cfg, make_round_cfg,
+                      fl_shard_reduce_wire, lib, lr_cosine, make_hsdp_cfg, make_round_cfg,
                       set_blocks_per_cu, status_string)
 
 __all__ = ["FL_MAX_GROUPS", "FL_MAX_PEERS", "FlError", "HipEvents", "Layout", "fingerprint",
            "fl_adamw_step", "fl_broadcast_recv", "fl_fedavg", "fl_fedopt", "fl_local_step",
-           "fl_round", "fl_round_hsdp", "fl_round_outer", "fl_shard_reduce", "fl_shard_reduce_wire", "lib", "make_hsdp_cfg",
-           "make_round_cfg", "set_blocks_per_cu", "status_string"]
+           "fl_round", "fl_round_hsdp", "fl_round_outer", "fl_shard_reduce",
+           "fl_shard_reduce_wire", "lib", "lr_cosine", "make_hsdp_cfg", "make_round_cfg",
+           "set_blocks_per_cu", "status_string"]

@@ -6,6 +6,7 @@
 // host in double, and enqueues the gfx950 kernels on the caller's stream.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cmath>
 #include <cstdint>
 #include <cstdlib>
@@ -108,6 +109,20 @@ int normalise_weights(int G, const float* w, float* out) {
   if (!(sum > 0.0) || !std::isfinite(sum)) return FL_ERR_INVALID;
   for (int g = 0; g < G; ++g) out[g] = (float)((double)w[g] / sum);
   return FL_OK;
+}
+
+// Hyperparameters of local step a of a round: step_lr overrides lr.
+fl_adamw_hparams step_hparams(const fl_round_cfg& c, int a) {
+  fl_adamw_hparams h = c.h;
+  if (c.step_lr) h.lr = c.step_lr[a];
+  return h;
+}
+
+bool step_lrs_ok(const fl_round_cfg& c) {
+  if (!c.step_lr) return true;
+  for (int a = 0; a < c.A; ++a)
+    if (!std::isfinite(c.step_lr[a]) || !(c.step_lr[a] >= 0.f)) return false;
+  return true;
 }
 
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
@@ -255,7 +270,24 @@ const char* fl_status_string(int status) {
   }
 }
 
-int fl_version(void) { return (1 << 16) | 2; }
+int fl_version(void) { return (1 << 16) | 3; }
+
+float fl_lr_cosine(int64_t t, int64_t total_steps, int64_t warmup_steps, float lr_max,
+                   float lr_min) {
+  const double s = (double)(t - 1);
+  const double w = (double)warmup_steps;
+  double f;
+  if (s < w) {
+    f = s / std::max(1.0, w);
+  } else {
+    const double q = (s - w) / std::max(1.0, (double)(total_steps - warmup_steps));
+    const double rho = (double)lr_min / (double)lr_max;
+    f = 0.5 * (1.0 + std::cos(M_PI * q));
+    f = f * (1.0 - rho) + rho;
+    f = std::max(0.0, f);
+  }
+  return (float)((double)lr_max * f);
+}
 
 int fl_set_blocks_per_cu(int blocks_per_cu) {
   const int prev = g_blocks_per_cu;
@@ -541,7 +573,7 @@ int fl_round_hsdp(const fl_layout* layout, const fl_round_cfg* cfg, const fl_hsd
   const int64_t n = layout->L.n;
   const bool member = hc->fedavg_member != 0;
   if (c.R < 1 || c.R > FL_MAX_PEERS || c.A < 1 || c.step0 < 1 || !finite(c.grad_scale) ||
-      !hparams_ok(&c.h))
+      !hparams_ok(&c.h) || !step_lrs_ok(c))
     return FL_ERR_INVALID;
   if (hc->H < 1 || hc->H > FL_MAX_PEERS || hc->replica < 0 || hc->replica >= hc->H ||
       !finite(hc->hsdp_scale))
@@ -605,8 +637,8 @@ int fl_round_hsdp(const fl_layout* layout, const fl_round_cfg* cfg, const fl_hsd
     float* ss = seg_sumsq ? seg_sumsq + (size_t)a * (size_t)layout->L.n_seg : nullptr;
     const uint16_t* const* ga = grads + (size_t)a * (size_t)c.R;
     if (hc->H == 1) {
-      rc = enqueue_local_step(layout, c.h, c.step0 + a, c.R, ga, c.grad_scale, master, m, v,
-                              working, ws, ss, st);
+      rc = enqueue_local_step(layout, step_hparams(c, a), c.step0 + a, c.R, ga, c.grad_scale,
+                              master, m, v, working, ws, ss, st);
       continue;
     }
     // tier 1: the sharding group's reduction, in the bf16 wire format
@@ -622,8 +654,8 @@ int fl_round_hsdp(const fl_layout* layout, const fl_round_cfg* cfg, const fl_hsd
     for (int k = 0; k < hc->H; ++k)
       wires[k] = (k == hc->replica) ? wire : replica_wires[(size_t)a * (size_t)hc->H + (size_t)k];
     if (rc == FL_OK)
-      rc = enqueue_local_step(layout, c.h, c.step0 + a, hc->H, wires, hc->hsdp_scale, master, m,
-                              v, working, ws, ss, st);
+      rc = enqueue_local_step(layout, step_hparams(c, a), c.step0 + a, hc->H, wires,
+                              hc->hsdp_scale, master, m, v, working, ws, ss, st);
   }
   if (rc == FL_OK) rc = record(c.A);
   if (rc == FL_OK && n > 0) {
@@ -694,7 +726,7 @@ static int round_impl(const fl_layout* layout, const fl_round_cfg* cfg,
   const int64_t n = layout->L.n;
   if (c.R < 1 || c.R > FL_MAX_PEERS || c.G < 1 || c.G > FL_MAX_GROUPS || c.A < 1 ||
       c.self_group < 0 || c.self_group >= c.G || c.step0 < 1 || !finite(c.grad_scale) ||
-      !hparams_ok(&c.h))
+      !hparams_ok(&c.h) || !step_lrs_ok(c))
     return FL_ERR_INVALID;
   if (c.step0 > INT64_MAX - c.A) return FL_ERR_INVALID;
   if ((int64_t)c.A * c.R > (int64_t)INT32_MAX) return FL_ERR_INVALID;
@@ -746,8 +778,8 @@ static int round_impl(const fl_layout* layout, const fl_round_cfg* cfg,
   for (int a = 0; a < c.A && rc == FL_OK; ++a) {
     rc = record(a);
     if (rc == FL_OK && n > 0)
-      rc = enqueue_local_step(layout, c.h, c.step0 + a, c.R, grads + (size_t)a * (size_t)c.R,
-                              c.grad_scale, master, m, v, working, ws,
+      rc = enqueue_local_step(layout, step_hparams(c, a), c.step0 + a, c.R,
+                              grads + (size_t)a * (size_t)c.R, c.grad_scale, master, m, v, working, ws,
                               seg_sumsq ? seg_sumsq + (size_t)a * (size_t)layout->L.n_seg : nullptr,
                               st);
   }

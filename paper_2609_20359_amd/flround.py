@@ -29,7 +29,8 @@ EXPORTS = ("fl_status_string", "fl_version", "fl_layout_create", "fl_layout_dest
            "fl_layout_numel", "fl_layout_num_segments", "fl_fingerprint",
            "fl_layout_fingerprint", "fl_shard_reduce", "fl_adamw_step", "fl_local_step",
            "fl_fedavg", "fl_round", "fl_set_blocks_per_cu", "fl_shard_reduce_wire",
-           "fl_broadcast_recv", "fl_round_hsdp", "fl_fedopt", "fl_round_outer")
+           "fl_broadcast_recv", "fl_round_hsdp", "fl_fedopt", "fl_round_outer",
+           "fl_lr_cosine")
 
 _P = ctypes.c_void_p
 
@@ -51,7 +52,8 @@ class RoundCfg(ctypes.Structure):
                 ("h", AdamwHparams), ("step0", ctypes.c_int64),
                 ("weights", ctypes.POINTER(ctypes.c_float)),
                 ("replica_fp", ctypes.POINTER(ctypes.c_uint64)),
-                ("phase_events", ctypes.POINTER(ctypes.c_void_p))]
+                ("phase_events", ctypes.POINTER(ctypes.c_void_p)),
+                ("step_lr", ctypes.POINTER(ctypes.c_float))]
 
 
 class OuterHparams(ctypes.Structure):
@@ -109,6 +111,9 @@ def lib():
                                 _P, _P, _P]
         L.fl_round_outer.argtypes = [_P, ctypes.POINTER(RoundCfg), ctypes.POINTER(OuterHparams),
                                      _P, _P, _P, _P, _P, _P, _P, _P, _P, _P]
+        L.fl_lr_cosine.argtypes = [ctypes.c_int64, ctypes.c_int64, ctypes.c_int64, ctypes.c_float,
+                                   ctypes.c_float]
+        L.fl_lr_cosine.restype = ctypes.c_float
         L.fl_set_blocks_per_cu.argtypes = [ctypes.c_int]
         L.fl_set_blocks_per_cu.restype = ctypes.c_int
         _lib = L
@@ -232,15 +237,22 @@ def fl_fedavg(layout, replicas, weights, master_out, working_out, replica_fp=Non
 
 
 def make_round_cfg(R, G, A, weights, hp, *, self_group=0, grad_scale=None, step0=1,
-                   replica_fp=None, phase_events=None):
+                   replica_fp=None, phase_events=None, step_lr=None):
     """Build an fl_round_cfg; the returned object keeps its arrays alive."""
     w = (ctypes.c_float * G)(*[float(x) for x in weights])
     fp = None if replica_fp is None else (ctypes.c_uint64 * G)(*[int(x) for x in replica_fp])
     ev = None if phase_events is None else (ctypes.c_void_p * len(phase_events))(*phase_events)
+    lrs = None if step_lr is None else (ctypes.c_float * len(step_lr))(*[float(x) for x in step_lr])
     cfg = RoundCfg(R, G, A, self_group, float(1.0 / R if grad_scale is None else grad_scale),
-                   hparams(hp), int(step0), w, fp, ev)
-    cfg._keep = (w, fp, ev)
+                   hparams(hp), int(step0), w, fp, ev, lrs)
+    cfg._keep = (w, fp, ev, lrs)
     return cfg
+
+
+def lr_cosine(t, total_steps, warmup_steps, lr_max, lr_min=0.0):
+    """fl_lr_cosine: the scheduled learning rate of optimiser step t."""
+    return lib().fl_lr_cosine(int(t), int(total_steps), int(warmup_steps), float(lr_max),
+                              float(lr_min))
 
 
 def fl_round(layout, cfg, grads, replicas, master, m, v, working, seg_sumsq=None, stream=None):

@@ -91,3 +91,26 @@ def test_calls_reject_null_handles_without_a_gpu():
 def test_blocks_per_cu_setting_round_trips():
     prev = P.set_blocks_per_cu(5)
     assert P.set_blocks_per_cu(prev) == 5
+
+
+def test_lr_cosine_matches_the_oracle_and_transformers():
+    import oracle
+    import transformers
+    import torch
+
+    orc = oracle.Oracle()
+    for T, W, lr_max, lr_min in ((64, 7, 3e-4, 0.0), (300, 30, 1e-3, 1e-5)):
+        base = float(np.float32(lr_max))
+        p = torch.nn.Parameter(torch.zeros(1))
+        opt = torch.optim.SGD([p], lr=base)
+        if lr_min:
+            sch = transformers.get_cosine_with_min_lr_schedule_with_warmup(
+                opt, W, T, min_lr_rate=float(np.float32(lr_min)) / base)
+        else:
+            sch = transformers.get_cosine_schedule_with_warmup(opt, W, T)
+        for t in range(1, T + 2):
+            lib_lr = np.float32(P.lr_cosine(t, T, W, lr_max, lr_min))
+            assert lib_lr == np.float32(orc.lr_cosine(t, T, W, lr_max, lr_min))
+            assert lib_lr == np.float32(opt.param_groups[0]["lr"])
+            opt.step()
+            sch.step()

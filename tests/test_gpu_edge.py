@@ -143,3 +143,37 @@ def test_round_captured_in_a_hip_graph(env):
                 "replay %d differs in %s" % (rep, name)
         del junk
     lay.close()
+
+
+def test_round_with_scheduled_learning_rates(env):
+    """Each local step of a round uses its own scheduled learning rate (cosine
+    decay with warm-up); the library's and the oracle's schedules are computed
+    separately and agree bitwise."""
+    torch, P, orc = env["torch"], env["P"], env["orc"]
+    r = np.random.default_rng(25)
+    sizes = r.integers(1, 50000, 9)
+    flags = r.integers(0, 2, sizes.size).astype(np.uint8)
+    w = W.make_workload("sched", sizes, flags, R=3, G=2, A=4, step0=5)
+    T, Wu = 64, 7
+    lib_lrs = [P.lr_cosine(w.step0 + a, T, Wu, w.hp["lr"]) for a in range(w.A)]
+    orc_lrs = [orc.lr_cosine(w.step0 + a, T, Wu, w.hp["lr"]) for a in range(w.A)]
+    assert np.array_equal(np.float32(lib_lrs), np.float32(orc_lrs))
+    assert len(set(lib_lrs)) == w.A
+    lay = P.Layout(w.seg_offsets, w.seg_decay)
+    dev = B.DeviceInputs(w)
+    cfg = P.make_round_cfg(w.R, w.G, w.A, w.weights, w.hp, self_group=w.self_group,
+                           grad_scale=w.grad_scale, step0=w.step0, step_lr=lib_lrs)
+    ss = torch.empty(w.A * w.n_seg, dtype=torch.float32, device="cuda")
+    H.gpu_round(P, lay, w, dev, seg_sumsq=ss, cfg=cfg)
+    torch.cuda.synchronize()
+    host = B.HostInputs(w)
+    ss_ref = orc.round(w.seg_offsets, w.seg_decay, w.R, w.G, w.A, w.self_group, w.grad_scale,
+                       w.hp, w.step0, w.weights, host.grads, host.replicas, host.master, host.m,
+                       host.v, host.working, want_sumsq=True, step_lr=orc_lrs)
+    H.assert_state_parity("sched", _state(dev), dict(master=host.master, m=host.m, v=host.v,
+                                                     working=host.working), bitwise=True)
+    H.assert_sumsq("sched", ss.cpu().numpy(), ss_ref.reshape(-1))
+    bad = P.make_round_cfg(w.R, w.G, w.A, w.weights, w.hp, step_lr=[1e-3, -1.0, 1e-3, 1e-3])
+    with pytest.raises(P.FlError):
+        H.gpu_round(P, lay, w, dev, cfg=bad)
+    lay.close()
