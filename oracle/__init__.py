@@ -42,24 +42,28 @@ def _declare(lib):
     lib.orc_fedavg.argtypes = [ctypes.c_int64, ctypes.c_int, _P, _P, _P, _P]
     lib.orc_round.argtypes = [ctypes.c_int64, _P, _P, ctypes.c_int, ctypes.c_int, ctypes.c_int,
                               ctypes.c_int, ctypes.c_float, ctypes.POINTER(Hparams),
-                              ctypes.c_int64, _P, _P, _P, _P, _P, _P, _P, _P, _P]
+                              ctypes.c_int64, _P, _P, _P, _P, _P, _P, _P, _P, _P, ctypes.c_float]
     lib.orc_lr_cosine.argtypes = [ctypes.c_int64, ctypes.c_int64, ctypes.c_int64, ctypes.c_float,
                                   ctypes.c_float]
     lib.orc_lr_cosine.restype = ctypes.c_float
+    lib.orc_total_sumsq.argtypes = [ctypes.c_int64, _P]
+    lib.orc_total_sumsq.restype = ctypes.c_double
+    lib.orc_clip_coef.argtypes = [ctypes.c_double, ctypes.c_float]
+    lib.orc_clip_coef.restype = ctypes.c_float
     lib.orc_shard_reduce_wire.argtypes = [ctypes.c_int64, ctypes.c_int, _P, ctypes.c_float, _P]
     lib.orc_broadcast_recv.argtypes = [ctypes.c_int64, _P, _P, _P]
     lib.orc_round_hsdp.argtypes = [ctypes.c_int64, _P, _P, ctypes.c_int, ctypes.c_int,
                                    ctypes.c_int, ctypes.c_float, ctypes.c_int, ctypes.c_int,
                                    ctypes.c_int, ctypes.c_int, ctypes.c_float,
                                    ctypes.POINTER(Hparams), ctypes.c_int64, _P, _P, _P, _P, _P,
-                                   _P, _P, _P, _P, _P, _P]
+                                   _P, _P, _P, _P, _P, _P, ctypes.c_float]
     lib.orc_fedopt.argtypes = [ctypes.c_int64, ctypes.c_int, _P, _P, ctypes.POINTER(Outer), _P,
                                _P, _P, _P]
     lib.orc_round_outer.argtypes = [ctypes.c_int64, _P, _P, ctypes.c_int, ctypes.c_int,
                                     ctypes.c_int, ctypes.c_int, ctypes.c_float,
                                     ctypes.POINTER(Hparams), ctypes.c_int64, _P,
                                     ctypes.POINTER(Outer), _P, _P, _P, _P, _P, _P, _P, _P, _P,
-                                    _P]
+                                    _P, ctypes.c_float]
     return lib
 
 
@@ -188,7 +192,8 @@ class Oracle:
 
     def round_hsdp(self, seg_off, seg_decay, R, H, replica, hsdp_scale, member, G, A,
                    self_group, grad_scale, hp, step0, weights, grads, replica_wires, replicas,
-                   bcast, master, m, v, working, want_sumsq=False, step_lr=None):
+                   bcast, master, m, v, working, want_sumsq=False, step_lr=None,
+                   max_grad_norm=0.0):
         """One FL+HSDP round in place.  replica_wires: A*H arrays (entry
         a*H + replica ignored, may be None); replicas: G arrays or None
         (member only); bcast: fp32 array (non-member only)."""
@@ -211,7 +216,8 @@ class Oracle:
                                    _ptr_array(reps) if reps else None,
                                    None if bc is None else bc.ctypes.data, master.ctypes.data,
                                    m.ctypes.data, v.ctypes.data, working.ctypes.data,
-                                   None if ss is None else ss.ctypes.data, _lr_ptr(step_lr, A))
+                                   None if ss is None else ss.ctypes.data, _lr_ptr(step_lr, A),
+                                   max_grad_norm)
         if rc:
             raise ValueError("orc_round_hsdp: %d" % rc)
         return None if ss is None else ss.reshape(A, n_seg)
@@ -233,7 +239,7 @@ class Oracle:
 
     def round_outer(self, seg_off, seg_decay, R, G, A, self_group, grad_scale, hp, step0,
                     weights, oh, grads, replicas, prev, buf, master, m, v, working,
-                    want_sumsq=False, step_lr=None):
+                    want_sumsq=False, step_lr=None, max_grad_norm=0.0):
         seg_off = _c(seg_off, np.int64)
         seg_decay = _c(seg_decay, np.uint8)
         n_seg = seg_off.size - 1
@@ -248,16 +254,25 @@ class Oracle:
                                     ctypes.byref(o), _ptr_array(grads), _ptr_array(reps),
                                     prev.ctypes.data, buf.ctypes.data, master.ctypes.data,
                                     m.ctypes.data, v.ctypes.data, working.ctypes.data,
-                                    None if ss is None else ss.ctypes.data, _lr_ptr(step_lr, A))
+                                    None if ss is None else ss.ctypes.data, _lr_ptr(step_lr, A),
+                                    max_grad_norm)
         if rc:
             raise ValueError("orc_round_outer: %d" % rc)
         return None if ss is None else ss.reshape(A, n_seg)
+
+    def total_sumsq(self, g):
+        g = _c(g, np.float32)
+        return self.L.orc_total_sumsq(g.size, g.ctypes.data)
+
+    def clip_coef(self, total_sumsq, max_norm):
+        return self.L.orc_clip_coef(total_sumsq, max_norm)
 
     def lr_cosine(self, t, total_steps, warmup_steps, lr_max, lr_min=0.0):
         return self.L.orc_lr_cosine(t, total_steps, warmup_steps, lr_max, lr_min)
 
     def round(self, seg_off, seg_decay, R, G, A, self_group, grad_scale, hp, step0, weights,
-              grads, replicas, master, m, v, working, want_sumsq=False, step_lr=None):
+              grads, replicas, master, m, v, working, want_sumsq=False, step_lr=None,
+              max_grad_norm=0.0):
         """In place on master, m, v, working.  grads: A*R arrays step-major;
         replicas: G arrays (entry self_group ignored, may be None).
         Returns the A x n_seg per-segment sums of squares, or None."""
@@ -273,7 +288,8 @@ class Oracle:
                               self_group, grad_scale, ctypes.byref(h), step0, w.ctypes.data,
                               _ptr_array(grads), _ptr_array(reps), master.ctypes.data,
                               m.ctypes.data, v.ctypes.data, working.ctypes.data,
-                              None if ss is None else ss.ctypes.data, _lr_ptr(step_lr, A))
+                              None if ss is None else ss.ctypes.data, _lr_ptr(step_lr, A),
+                              max_grad_norm)
         if rc:
             raise ValueError("orc_round: %d" % rc)
         return None if ss is None else ss.reshape(A, n_seg)

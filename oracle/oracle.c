@@ -55,6 +55,23 @@ int orc_seg_sumsq(int64_t n_seg, const int64_t* seg_off, const float* g, double*
   return 0;
 }
 
+double orc_total_sumsq(int64_t n, const float* g) {
+  double sum = 0.0;
+  for (int64_t i = 0; i < n; ++i) sum += (double)g[i] * (double)g[i];
+  return sum;
+}
+
+float orc_clip_coef(double total_sumsq, float max_norm) {
+  const double c = (double)max_norm / (sqrt(total_sumsq) + 1e-6);
+  return (float)(c < 1.0 ? c : 1.0);
+}
+
+/* (n5) scale g in place by the clip coefficient of its whole-shard norm. */
+static void orc_clip(int64_t n, float* g, float max_norm) {
+  const float coef = orc_clip_coef(orc_total_sumsq(n, g), max_norm);
+  for (int64_t i = 0; i < n; ++i) g[i] = g[i] * coef;
+}
+
 int orc_adamw_step(int64_t n_seg, const int64_t* seg_off, const uint8_t* seg_decay,
                    const orc_hparams* h, int64_t t, const float* g, float* master, float* m,
                    float* v, uint16_t* working) {
@@ -127,7 +144,8 @@ int orc_round(int64_t n_seg, const int64_t* seg_off, const uint8_t* seg_decay, i
               int A, int self_group, float grad_scale, const orc_hparams* h, int64_t step0,
               const float* weights, const uint16_t* const* grads,
               const uint16_t* const* replicas, float* master, float* m, float* v,
-              uint16_t* working, double* seg_sumsq, const float* step_lr) {
+              uint16_t* working, double* seg_sumsq, const float* step_lr,
+              float max_grad_norm) {
   if (n_seg < 0 || !seg_off || R < 1 || G < 1 || A < 1 || self_group < 0 ||
       self_group >= G || !h || step0 < 1 || !weights || !grads || !replicas)
     return -1;
@@ -145,6 +163,7 @@ int orc_round(int64_t n_seg, const int64_t* seg_off, const uint8_t* seg_decay, i
     rc = orc_shard_reduce(n, R, grads + (size_t)a * (size_t)R, grad_scale, g);
     if (rc == 0 && seg_sumsq)
       rc = orc_seg_sumsq(n_seg, seg_off, g, seg_sumsq + (size_t)a * (size_t)n_seg);
+    if (rc == 0 && max_grad_norm > 0.0f) orc_clip(n, g, max_grad_norm);
     orc_hparams ha = *h;
     if (step_lr) ha.lr = step_lr[a];
     if (rc == 0)
@@ -184,7 +203,8 @@ int orc_round_hsdp(int64_t n_seg, const int64_t* seg_off, const uint8_t* seg_dec
                    float grad_scale, const orc_hparams* h, int64_t step0, const float* weights,
                    const uint16_t* const* grads, const uint16_t* const* replica_wires,
                    const uint16_t* const* replicas, const float* bcast, float* master, float* m,
-                   float* v, uint16_t* working, double* seg_sumsq, const float* step_lr) {
+                   float* v, uint16_t* working, double* seg_sumsq, const float* step_lr,
+                   float max_grad_norm) {
   if (n_seg < 0 || !seg_off || R < 1 || H < 1 || replica < 0 || replica >= H || A < 1 ||
       !h || step0 < 1 || !grads)
     return -1;
@@ -210,6 +230,7 @@ int orc_round_hsdp(int64_t n_seg, const int64_t* seg_off, const uint8_t* seg_dec
     }
     if (rc == 0 && seg_sumsq)
       rc = orc_seg_sumsq(n_seg, seg_off, g, seg_sumsq + (size_t)a * (size_t)n_seg);
+    if (rc == 0 && max_grad_norm > 0.0f) orc_clip(n, g, max_grad_norm);
     orc_hparams ha = *h;
     if (step_lr) ha.lr = step_lr[a];
     if (rc == 0)
@@ -265,7 +286,7 @@ int orc_round_outer(int64_t n_seg, const int64_t* seg_off, const uint8_t* seg_de
                     const float* weights, const orc_outer* o, const uint16_t* const* grads,
                     const uint16_t* const* replicas, float* prev, float* buf, float* master,
                     float* m, float* v, uint16_t* working, double* seg_sumsq,
-                    const float* step_lr) {
+                    const float* step_lr, float max_grad_norm) {
   if (n_seg < 0 || !seg_off || R < 1 || G < 1 || A < 1 || self_group < 0 ||
       self_group >= G || !h || !o || step0 < 1 || !weights || !grads || !replicas)
     return -1;
@@ -278,6 +299,7 @@ int orc_round_outer(int64_t n_seg, const int64_t* seg_off, const uint8_t* seg_de
     rc = orc_shard_reduce(n, R, grads + (size_t)a * (size_t)R, grad_scale, g);
     if (rc == 0 && seg_sumsq)
       rc = orc_seg_sumsq(n_seg, seg_off, g, seg_sumsq + (size_t)a * (size_t)n_seg);
+    if (rc == 0 && max_grad_norm > 0.0f) orc_clip(n, g, max_grad_norm);
     orc_hparams ha = *h;
     if (step_lr) ha.lr = step_lr[a];
     if (rc == 0)

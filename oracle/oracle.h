@@ -49,6 +49,12 @@
  *                f = f (1 - lr_min / lr_max) + lr_min / lr_max; f = max(0, f)
  *         lr_t = (float)(lr_max * f)                      (all in double)
  *       A round may give each of its A local steps its own lr.
+ *  (n5) global-norm clipping of each local step's gradient (the clipping of
+ *       torch.nn.utils.clip_grad_norm_), driven by the sum of squares that
+ *       (a5) computes: total = sum_i (double)g[i]^2 (index order);
+ *       coef = (float)min(1, max_norm / (sqrt(total) + 1e-6)) (double);
+ *       g[i] = g[i] * coef (fp32) before AdamW.  The per-segment sums of (a5)
+ *       are those of the unclipped g.  max_norm <= 0: no clipping.
  *
  * FL+HSDP (Section 2, HSDP; Section 4.1, Eq. (2); Section 4.2, Eq. (5)): the
  * gradient is averaged in two tiers (Section 5.1), first over the sharding
@@ -113,6 +119,10 @@ int orc_adamw_step(int64_t n_seg, const int64_t* seg_off, const uint8_t* seg_dec
 int orc_fedavg(int64_t n, int G, const uint16_t* const* replicas, const float* weights,
                float* master_out, uint16_t* working_out);
 
+/* (n5) sum of (double)g[i]^2 over [0, n), index order; clip coefficient. */
+double orc_total_sumsq(int64_t n, const float* g);
+float orc_clip_coef(double total_sumsq, float max_norm);
+
 /* (n4) scheduled learning rate of optimiser step t. */
 float orc_lr_cosine(int64_t t, int64_t total_steps, int64_t warmup_steps, float lr_max,
                     float lr_min);
@@ -125,7 +135,8 @@ int orc_round(int64_t n_seg, const int64_t* seg_off, const uint8_t* seg_decay, i
               int A, int self_group, float grad_scale, const orc_hparams* h, int64_t step0,
               const float* weights, const uint16_t* const* grads,
               const uint16_t* const* replicas, float* master, float* m, float* v,
-              uint16_t* working, double* seg_sumsq, const float* step_lr);
+              uint16_t* working, double* seg_sumsq, const float* step_lr,
+              float max_grad_norm);
 
 /* (n1) tier 1 to the bf16 wire format. */
 int orc_shard_reduce_wire(int64_t n, int R, const uint16_t* const* grads, float grad_scale,
@@ -145,7 +156,8 @@ int orc_round_hsdp(int64_t n_seg, const int64_t* seg_off, const uint8_t* seg_dec
                    float grad_scale, const orc_hparams* h, int64_t step0, const float* weights,
                    const uint16_t* const* grads, const uint16_t* const* replica_wires,
                    const uint16_t* const* replicas, const float* bcast, float* master, float* m,
-                   float* v, uint16_t* working, double* seg_sumsq, const float* step_lr);
+                   float* v, uint16_t* working, double* seg_sumsq, const float* step_lr,
+                   float max_grad_norm);
 
 typedef struct {
   float lr, momentum;
@@ -164,7 +176,7 @@ int orc_round_outer(int64_t n_seg, const int64_t* seg_off, const uint8_t* seg_de
                     const float* weights, const orc_outer* o, const uint16_t* const* grads,
                     const uint16_t* const* replicas, float* prev, float* buf, float* master,
                     float* m, float* v, uint16_t* working, double* seg_sumsq,
-                    const float* step_lr);
+                    const float* step_lr, float max_grad_norm);
 
 #ifdef __cplusplus
 }

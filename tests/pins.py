@@ -916,6 +916,81 @@ def pin_round_step_lr_brute_force(orc):
         _check_close("step_lr master", master, xbar, ex)
 
 
+# ---- global-norm gradient clipping -------------------------------------------
+
+def pin_clip_vs_torch(orc):
+    """Coefficient and clipped gradient against torch.nn.utils.clip_grad_norm_
+    in float64, including a norm small enough that its 1e-6 guard matters."""
+    r = rng(24)
+    for scale, max_norm in ((1e-3, 0.05), (1e-3, 100.0), (1e-9, 1e-10), (0.3, 1.0)):
+        g = (r.standard_normal(20000) * scale).astype(np.float32)
+        t = torch.nn.Parameter(torch.zeros(g.size, dtype=torch.float64))
+        t.grad = torch.tensor(g.astype(np.float64))
+        total_norm = float(torch.nn.utils.clip_grad_norm_([t], max_norm))
+        total = orc.total_sumsq(g)
+        assert abs(total - total_norm ** 2) <= 1e-12 * total_norm ** 2 + 1e-300, "sum of squares"
+        coef = orc.clip_coef(total, max_norm)
+        want = min(1.0, float(np.float32(max_norm)) / (total_norm + 1e-6))
+        assert abs(coef - want) <= 2 * U * want, "clip coefficient %r vs %r" % (coef, want)
+        clipped = g * np.float32(coef)
+        _check_close("clipped g", clipped, t.grad.numpy(), 4 * U * np.abs(t.grad.numpy()) + TINY)
+
+
+def _bf_clip(gsteps, max_norm):
+    """Clipped per-step (g, bound) in float64 from unclipped ones."""
+    out = []
+    M = float(np.float32(max_norm))
+    for g, eg in gsteps:
+        T = np.sum(g * g)
+        dT = np.sum(2 * np.abs(g) * eg + eg * eg) + 1e-15 * T
+        c = min(1.0, M / (np.sqrt(T) + 1e-6))
+        ec = c * (dT / max(T, 1e-300) / 2 + 2 * U) + 1e-300
+        gc = g * c
+        out.append((gc, eg * c + np.abs(g) * ec + U * np.abs(gc)))
+    return out
+
+
+def pin_round_clipped_brute_force(orc):
+    """Rounds with clipping active (norm above max) and inactive."""
+    r = rng(25)
+    for R, A, max_norm in ((2, 2, 1e-3), (3, 3, 5e-4), (2, 2, 1e6)):
+        c = _random_round_case(r, R, 2, A, n=48)
+        master, m, v = c["p0"].copy(), c["m0"].copy(), c["v0"].copy()
+        work = torch_bf16_bits(master)
+        ss = orc.round(c["seg_off"], c["seg_decay"], R, 2, A, c["self_group"], c["grad_scale"],
+                       BIG_HP, c["step0"], c["weights"], c["grads"], c["replicas"], master, m, v,
+                       work, want_sumsq=True, max_grad_norm=max_norm)
+        g0 = [_bf_reduce(c["grads"][a * R:(a + 1) * R], c["grad_scale"]) for a in range(A)]
+        gsteps = _bf_clip(g0, max_norm)
+        (p, ep), (mm, em), (vv, ev) = _bf_steps(BIG_HP, c["seg_off"], c["seg_decay"], c["step0"],
+                                                gsteps, c["p0"], c["m0"], c["v0"])
+        tag = "clip R=%d A=%d max=%g" % (R, A, max_norm)
+        _check_close(tag + " m", m, mm, em)
+        _check_close(tag + " v", v, vv, ev)
+        off = c["seg_off"]
+        for a, (g, eg) in enumerate(g0):   # per-segment sums are of the unclipped g
+            for s_ in range(off.size - 1):
+                sl = slice(off[s_], off[s_ + 1])
+                want = np.sum(g[sl] ** 2)
+                bound = np.sum(2 * np.abs(g[sl]) * eg[sl] + eg[sl] ** 2) * 2 + 1e-12 * want + TINY
+                assert abs(ss[a, s_] - want) <= bound, tag + " seg_sumsq"
+
+
+def pin_clip_inactive_is_bitwise_unclipped(orc):
+    r = rng(26)
+    c = _random_round_case(r, 3, 2, 3, n=4000)
+    outs = []
+    for mx in (0.0, 1e9):
+        master, m, v = c["p0"].copy(), c["m0"].copy(), c["v0"].copy()
+        work = torch_bf16_bits(master)
+        orc.round(c["seg_off"], c["seg_decay"], 3, 2, 3, c["self_group"], c["grad_scale"], STD_HP,
+                  c["step0"], c["weights"], c["grads"], c["replicas"], master, m, v, work,
+                  max_grad_norm=mx)
+        outs.append((master, m, v, work))
+    for x, y in zip(*outs):
+        assert np.array_equal(x.view(np.uint8), y.view(np.uint8)), "coef 1 changed the round"
+
+
 ALL_PINS = [
     pin_bf16_decode_all_patterns,
     pin_bf16_encode_matches_torch,
@@ -946,4 +1021,7 @@ ALL_PINS = [
     pin_lr_cosine_vs_transformers,
     pin_lr_cosine_closed_forms,
     pin_round_step_lr_brute_force,
+    pin_clip_vs_torch,
+    pin_round_clipped_brute_force,
+    pin_clip_inactive_is_bitwise_unclipped,
 ]
