@@ -42,7 +42,8 @@ def _declare(lib):
     lib.orc_fedavg.argtypes = [ctypes.c_int64, ctypes.c_int, _P, _P, _P, _P]
     lib.orc_round.argtypes = [ctypes.c_int64, _P, _P, ctypes.c_int, ctypes.c_int, ctypes.c_int,
                               ctypes.c_int, ctypes.c_float, ctypes.POINTER(Hparams),
-                              ctypes.c_int64, _P, _P, _P, _P, _P, _P, _P, _P, _P, ctypes.c_float]
+                              ctypes.c_int64, _P, _P, _P, _P, _P, _P, _P, _P, _P, ctypes.c_float,
+                              _P]
     lib.orc_lr_cosine.argtypes = [ctypes.c_int64, ctypes.c_int64, ctypes.c_int64, ctypes.c_float,
                                   ctypes.c_float]
     lib.orc_lr_cosine.restype = ctypes.c_float
@@ -50,20 +51,23 @@ def _declare(lib):
     lib.orc_total_sumsq.restype = ctypes.c_double
     lib.orc_clip_coef.argtypes = [ctypes.c_double, ctypes.c_float]
     lib.orc_clip_coef.restype = ctypes.c_float
+    lib.orc_grad_total.argtypes = [ctypes.c_int64, ctypes.c_int, _P, ctypes.c_float,
+                                   ctypes.c_double]
+    lib.orc_grad_total.restype = ctypes.c_double
     lib.orc_shard_reduce_wire.argtypes = [ctypes.c_int64, ctypes.c_int, _P, ctypes.c_float, _P]
     lib.orc_broadcast_recv.argtypes = [ctypes.c_int64, _P, _P, _P]
     lib.orc_round_hsdp.argtypes = [ctypes.c_int64, _P, _P, ctypes.c_int, ctypes.c_int,
                                    ctypes.c_int, ctypes.c_float, ctypes.c_int, ctypes.c_int,
                                    ctypes.c_int, ctypes.c_int, ctypes.c_float,
                                    ctypes.POINTER(Hparams), ctypes.c_int64, _P, _P, _P, _P, _P,
-                                   _P, _P, _P, _P, _P, _P, ctypes.c_float]
+                                   _P, _P, _P, _P, _P, _P, ctypes.c_float, _P]
     lib.orc_fedopt.argtypes = [ctypes.c_int64, ctypes.c_int, _P, _P, ctypes.POINTER(Outer), _P,
                                _P, _P, _P]
     lib.orc_round_outer.argtypes = [ctypes.c_int64, _P, _P, ctypes.c_int, ctypes.c_int,
                                     ctypes.c_int, ctypes.c_int, ctypes.c_float,
                                     ctypes.POINTER(Hparams), ctypes.c_int64, _P,
                                     ctypes.POINTER(Outer), _P, _P, _P, _P, _P, _P, _P, _P, _P,
-                                    _P, ctypes.c_float]
+                                    _P, ctypes.c_float, _P]
     return lib
 
 
@@ -99,6 +103,16 @@ def _lr_ptr(step_lr, A):
         return None
     a = np.ascontiguousarray(step_lr, dtype=np.float32)
     assert a.size == A, "step_lr needs one value per local step"
+    _keep.append(a)
+    del _keep[:-4]
+    return a.ctypes.data
+
+
+def _tot_ptr(totals, A):
+    if totals is None:
+        return None
+    a = np.ascontiguousarray(totals, dtype=np.float64)
+    assert a.size == A, "clip_totals needs one value per local step"
     _keep.append(a)
     del _keep[:-4]
     return a.ctypes.data
@@ -193,7 +207,7 @@ class Oracle:
     def round_hsdp(self, seg_off, seg_decay, R, H, replica, hsdp_scale, member, G, A,
                    self_group, grad_scale, hp, step0, weights, grads, replica_wires, replicas,
                    bcast, master, m, v, working, want_sumsq=False, step_lr=None,
-                   max_grad_norm=0.0):
+                   max_grad_norm=0.0, clip_totals=None):
         """One FL+HSDP round in place.  replica_wires: A*H arrays (entry
         a*H + replica ignored, may be None); replicas: G arrays or None
         (member only); bcast: fp32 array (non-member only)."""
@@ -217,7 +231,7 @@ class Oracle:
                                    None if bc is None else bc.ctypes.data, master.ctypes.data,
                                    m.ctypes.data, v.ctypes.data, working.ctypes.data,
                                    None if ss is None else ss.ctypes.data, _lr_ptr(step_lr, A),
-                                   max_grad_norm)
+                                   max_grad_norm, _tot_ptr(clip_totals, A))
         if rc:
             raise ValueError("orc_round_hsdp: %d" % rc)
         return None if ss is None else ss.reshape(A, n_seg)
@@ -239,7 +253,7 @@ class Oracle:
 
     def round_outer(self, seg_off, seg_decay, R, G, A, self_group, grad_scale, hp, step0,
                     weights, oh, grads, replicas, prev, buf, master, m, v, working,
-                    want_sumsq=False, step_lr=None, max_grad_norm=0.0):
+                    want_sumsq=False, step_lr=None, max_grad_norm=0.0, clip_totals=None):
         seg_off = _c(seg_off, np.int64)
         seg_decay = _c(seg_decay, np.uint8)
         n_seg = seg_off.size - 1
@@ -255,7 +269,7 @@ class Oracle:
                                     prev.ctypes.data, buf.ctypes.data, master.ctypes.data,
                                     m.ctypes.data, v.ctypes.data, working.ctypes.data,
                                     None if ss is None else ss.ctypes.data, _lr_ptr(step_lr, A),
-                                    max_grad_norm)
+                                    max_grad_norm, _tot_ptr(clip_totals, A))
         if rc:
             raise ValueError("orc_round_outer: %d" % rc)
         return None if ss is None else ss.reshape(A, n_seg)
@@ -263,6 +277,11 @@ class Oracle:
     def total_sumsq(self, g):
         g = _c(g, np.float32)
         return self.L.orc_total_sumsq(g.size, g.ctypes.data)
+
+    def grad_total(self, grads, grad_scale, acc0=0.0):
+        grads = [_c(g, np.uint16) for g in grads]
+        return self.L.orc_grad_total(grads[0].size, len(grads), _ptr_array(grads), grad_scale,
+                                     acc0)
 
     def clip_coef(self, total_sumsq, max_norm):
         return self.L.orc_clip_coef(total_sumsq, max_norm)
@@ -272,7 +291,7 @@ class Oracle:
 
     def round(self, seg_off, seg_decay, R, G, A, self_group, grad_scale, hp, step0, weights,
               grads, replicas, master, m, v, working, want_sumsq=False, step_lr=None,
-              max_grad_norm=0.0):
+              max_grad_norm=0.0, clip_totals=None):
         """In place on master, m, v, working.  grads: A*R arrays step-major;
         replicas: G arrays (entry self_group ignored, may be None).
         Returns the A x n_seg per-segment sums of squares, or None."""
@@ -289,7 +308,7 @@ class Oracle:
                               _ptr_array(grads), _ptr_array(reps), master.ctypes.data,
                               m.ctypes.data, v.ctypes.data, working.ctypes.data,
                               None if ss is None else ss.ctypes.data, _lr_ptr(step_lr, A),
-                              max_grad_norm)
+                              max_grad_norm, _tot_ptr(clip_totals, A))
         if rc:
             raise ValueError("orc_round: %d" % rc)
         return None if ss is None else ss.reshape(A, n_seg)

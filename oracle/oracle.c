@@ -66,9 +66,22 @@ float orc_clip_coef(double total_sumsq, float max_norm) {
   return (float)(c < 1.0 ? c : 1.0);
 }
 
-/* (n5) scale g in place by the clip coefficient of its whole-shard norm. */
-static void orc_clip(int64_t n, float* g, float max_norm) {
-  const float coef = orc_clip_coef(orc_total_sumsq(n, g), max_norm);
+double orc_grad_total(int64_t n, int R, const uint16_t* const* grads, float grad_scale,
+                      double acc0) {
+  double sum = acc0;
+  for (int64_t i = 0; i < n; ++i) {
+    float acc = 0.0f;
+    for (int r = 0; r < R; ++r) acc = acc + orc_bf16_to_f32(grads[r][i]);
+    const float g = acc * grad_scale;
+    sum += (double)g * (double)g;
+  }
+  return sum;
+}
+
+/* (n5) scale g in place by the clip coefficient of the whole-shard norm:
+ * that of g itself, or the given total. */
+static void orc_clip(int64_t n, float* g, float max_norm, const double* total) {
+  const float coef = orc_clip_coef(total ? *total : orc_total_sumsq(n, g), max_norm);
   for (int64_t i = 0; i < n; ++i) g[i] = g[i] * coef;
 }
 
@@ -145,7 +158,7 @@ int orc_round(int64_t n_seg, const int64_t* seg_off, const uint8_t* seg_decay, i
               const float* weights, const uint16_t* const* grads,
               const uint16_t* const* replicas, float* master, float* m, float* v,
               uint16_t* working, double* seg_sumsq, const float* step_lr,
-              float max_grad_norm) {
+              float max_grad_norm, const double* clip_totals) {
   if (n_seg < 0 || !seg_off || R < 1 || G < 1 || A < 1 || self_group < 0 ||
       self_group >= G || !h || step0 < 1 || !weights || !grads || !replicas)
     return -1;
@@ -163,7 +176,8 @@ int orc_round(int64_t n_seg, const int64_t* seg_off, const uint8_t* seg_decay, i
     rc = orc_shard_reduce(n, R, grads + (size_t)a * (size_t)R, grad_scale, g);
     if (rc == 0 && seg_sumsq)
       rc = orc_seg_sumsq(n_seg, seg_off, g, seg_sumsq + (size_t)a * (size_t)n_seg);
-    if (rc == 0 && max_grad_norm > 0.0f) orc_clip(n, g, max_grad_norm);
+    if (rc == 0 && max_grad_norm > 0.0f)
+      orc_clip(n, g, max_grad_norm, clip_totals ? clip_totals + a : NULL);
     orc_hparams ha = *h;
     if (step_lr) ha.lr = step_lr[a];
     if (rc == 0)
@@ -204,7 +218,7 @@ int orc_round_hsdp(int64_t n_seg, const int64_t* seg_off, const uint8_t* seg_dec
                    const uint16_t* const* grads, const uint16_t* const* replica_wires,
                    const uint16_t* const* replicas, const float* bcast, float* master, float* m,
                    float* v, uint16_t* working, double* seg_sumsq, const float* step_lr,
-                   float max_grad_norm) {
+                   float max_grad_norm, const double* clip_totals) {
   if (n_seg < 0 || !seg_off || R < 1 || H < 1 || replica < 0 || replica >= H || A < 1 ||
       !h || step0 < 1 || !grads)
     return -1;
@@ -230,7 +244,8 @@ int orc_round_hsdp(int64_t n_seg, const int64_t* seg_off, const uint8_t* seg_dec
     }
     if (rc == 0 && seg_sumsq)
       rc = orc_seg_sumsq(n_seg, seg_off, g, seg_sumsq + (size_t)a * (size_t)n_seg);
-    if (rc == 0 && max_grad_norm > 0.0f) orc_clip(n, g, max_grad_norm);
+    if (rc == 0 && max_grad_norm > 0.0f)
+      orc_clip(n, g, max_grad_norm, clip_totals ? clip_totals + a : NULL);
     orc_hparams ha = *h;
     if (step_lr) ha.lr = step_lr[a];
     if (rc == 0)
@@ -286,7 +301,7 @@ int orc_round_outer(int64_t n_seg, const int64_t* seg_off, const uint8_t* seg_de
                     const float* weights, const orc_outer* o, const uint16_t* const* grads,
                     const uint16_t* const* replicas, float* prev, float* buf, float* master,
                     float* m, float* v, uint16_t* working, double* seg_sumsq,
-                    const float* step_lr, float max_grad_norm) {
+                    const float* step_lr, float max_grad_norm, const double* clip_totals) {
   if (n_seg < 0 || !seg_off || R < 1 || G < 1 || A < 1 || self_group < 0 ||
       self_group >= G || !h || !o || step0 < 1 || !weights || !grads || !replicas)
     return -1;
@@ -299,7 +314,8 @@ int orc_round_outer(int64_t n_seg, const int64_t* seg_off, const uint8_t* seg_de
     rc = orc_shard_reduce(n, R, grads + (size_t)a * (size_t)R, grad_scale, g);
     if (rc == 0 && seg_sumsq)
       rc = orc_seg_sumsq(n_seg, seg_off, g, seg_sumsq + (size_t)a * (size_t)n_seg);
-    if (rc == 0 && max_grad_norm > 0.0f) orc_clip(n, g, max_grad_norm);
+    if (rc == 0 && max_grad_norm > 0.0f)
+      orc_clip(n, g, max_grad_norm, clip_totals ? clip_totals + a : NULL);
     orc_hparams ha = *h;
     if (step_lr) ha.lr = step_lr[a];
     if (rc == 0)

@@ -119,9 +119,14 @@ int orc_adamw_step(int64_t n_seg, const int64_t* seg_off, const uint8_t* seg_dec
 int orc_fedavg(int64_t n, int G, const uint16_t* const* replicas, const float* weights,
                float* master_out, uint16_t* working_out);
 
-/* (n5) sum of (double)g[i]^2 over [0, n), index order; clip coefficient. */
+/* (n5) sum of (double)g[i]^2 over [0, n), index order; clip coefficient.
+ * orc_grad_total: acc0 + the same sum for the reduced gradient of R peers
+ * (g[i] as in (a1)), so a caller can stream a long shard chunk by chunk and
+ * still add in index order. */
 double orc_total_sumsq(int64_t n, const float* g);
 float orc_clip_coef(double total_sumsq, float max_norm);
+double orc_grad_total(int64_t n, int R, const uint16_t* const* grads, float grad_scale,
+                      double acc0);
 
 /* (n4) scheduled learning rate of optimiser step t. */
 float orc_lr_cosine(int64_t t, int64_t total_steps, int64_t warmup_steps, float lr_max,
@@ -130,13 +135,15 @@ float orc_lr_cosine(int64_t t, int64_t total_steps, int64_t warmup_steps, float 
 /* (a4) One round.  grads: A*R arrays, step-major.  replicas: G arrays, the
  * entry at self_group is ignored (the working copy is used).  step_lr: NULL
  * (every step uses h->lr) or A learning rates.  seg_sumsq: NULL or A*n_seg
- * doubles. */
+ * doubles.  clip_totals: NULL (the norm of each step is that of this
+ * shard's g), or A whole-shard sums of squares to clip against (a shard
+ * evaluated on a sample of its elements). */
 int orc_round(int64_t n_seg, const int64_t* seg_off, const uint8_t* seg_decay, int R, int G,
               int A, int self_group, float grad_scale, const orc_hparams* h, int64_t step0,
               const float* weights, const uint16_t* const* grads,
               const uint16_t* const* replicas, float* master, float* m, float* v,
               uint16_t* working, double* seg_sumsq, const float* step_lr,
-              float max_grad_norm);
+              float max_grad_norm, const double* clip_totals);
 
 /* (n1) tier 1 to the bf16 wire format. */
 int orc_shard_reduce_wire(int64_t n, int R, const uint16_t* const* grads, float grad_scale,
@@ -157,7 +164,7 @@ int orc_round_hsdp(int64_t n_seg, const int64_t* seg_off, const uint8_t* seg_dec
                    const uint16_t* const* grads, const uint16_t* const* replica_wires,
                    const uint16_t* const* replicas, const float* bcast, float* master, float* m,
                    float* v, uint16_t* working, double* seg_sumsq, const float* step_lr,
-                   float max_grad_norm);
+                   float max_grad_norm, const double* clip_totals);
 
 typedef struct {
   float lr, momentum;
@@ -176,7 +183,7 @@ int orc_round_outer(int64_t n_seg, const int64_t* seg_off, const uint8_t* seg_de
                     const float* weights, const orc_outer* o, const uint16_t* const* grads,
                     const uint16_t* const* replicas, float* prev, float* buf, float* master,
                     float* m, float* v, uint16_t* working, double* seg_sumsq,
-                    const float* step_lr, float max_grad_norm);
+                    const float* step_lr, float max_grad_norm, const double* clip_totals);
 
 #ifdef __cplusplus
 }

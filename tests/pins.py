@@ -976,6 +976,20 @@ def pin_round_clipped_brute_force(orc):
                 assert abs(ss[a, s_] - want) <= bound, tag + " seg_sumsq"
 
 
+def pin_grad_total_streams(orc):
+    """The streamed whole-shard total equals a float64 sum of the squares of
+    the reduced gradient, and chunking it changes nothing."""
+    r = rng(27)
+    grads = [random_bf16(r, 10000, 1e-3) for _ in range(3)]
+    whole = orc.grad_total(grads, 1.0 / 3)
+    g = orc.shard_reduce(grads, 1.0 / 3).astype(np.float64)
+    assert abs(whole - np.sum(g * g)) <= 1e-12 * whole
+    acc = 0.0
+    for lo in range(0, 10000, 3333):
+        acc = orc.grad_total([x[lo:lo + 3333] for x in grads], 1.0 / 3, acc)
+    assert acc == whole, "chunked total differs"
+
+
 def pin_clip_inactive_is_bitwise_unclipped(orc):
     r = rng(26)
     c = _random_round_case(r, 3, 2, 3, n=4000)
@@ -1024,4 +1038,5 @@ ALL_PINS = [
     pin_clip_vs_torch,
     pin_round_clipped_brute_force,
     pin_clip_inactive_is_bitwise_unclipped,
+    pin_grad_total_streams,
 ]

@@ -84,9 +84,9 @@ MUTANTS = {
     "clip_no_clamp": [("return (float)(c < 1.0 ? c : 1.0);", "return (float)c;")],
     "clip_no_eps": [("(sqrt(total_sumsq) + 1e-6)", "sqrt(total_sumsq)")],
     "clip_no_sqrt": [("(sqrt(total_sumsq) + 1e-6)", "(total_sumsq + 1e-6)")],
-    "clip_ignored": [("    if (rc == 0 && max_grad_norm > 0.0f) orc_clip(n, g, max_grad_norm);\n", "")],
-    "clip_before_sumsq": [("    if (rc == 0 && seg_sumsq)\n      rc = orc_seg_sumsq(n_seg, seg_off, g, seg_sumsq + (size_t)a * (size_t)n_seg);\n    if (rc == 0 && max_grad_norm > 0.0f) orc_clip(n, g, max_grad_norm);",
-                           "    if (rc == 0 && max_grad_norm > 0.0f) orc_clip(n, g, max_grad_norm);\n    if (rc == 0 && seg_sumsq)\n      rc = orc_seg_sumsq(n_seg, seg_off, g, seg_sumsq + (size_t)a * (size_t)n_seg);")],
+    "clip_ignored": [("    if (rc == 0 && max_grad_norm > 0.0f)\n      orc_clip(n, g, max_grad_norm, clip_totals ? clip_totals + a : NULL);\n", "")],
+    "clip_before_sumsq": [("    if (rc == 0 && seg_sumsq)\n      rc = orc_seg_sumsq(n_seg, seg_off, g, seg_sumsq + (size_t)a * (size_t)n_seg);\n    if (rc == 0 && max_grad_norm > 0.0f)\n      orc_clip(n, g, max_grad_norm, clip_totals ? clip_totals + a : NULL);",
+                           "    if (rc == 0 && max_grad_norm > 0.0f)\n      orc_clip(n, g, max_grad_norm, clip_totals ? clip_totals + a : NULL);\n    if (rc == 0 && seg_sumsq)\n      rc = orc_seg_sumsq(n_seg, seg_off, g, seg_sumsq + (size_t)a * (size_t)n_seg);")],
     "round_ignores_step_lr": [("    if (step_lr) ha.lr = step_lr[a];\n", "")],
     "round_first_step_lr_only": [("if (step_lr) ha.lr = step_lr[a];", "if (step_lr) ha.lr = step_lr[0];")],
     "hsdp_reuses_first_grads": [("grads + (size_t)a * (size_t)R", "grads", 1)],
