@@ -56,7 +56,7 @@ def read_traffic(current_hash):
 
 
 LOCAL_STEP_KERNEL = "k_step<8, 0, true>"
-FEDAVG_KERNEL = "k_fedavg<4>"
+FEDAVG_KERNEL = "k_fedavg<4, false>"
 COPY_KERNEL = "__amd_rocclr_copyBuffer"
 
 
@@ -118,11 +118,13 @@ def summarize_pmc(fetch_csv, write_csv, copy_mib, cmd_fetch, cmd_write):
     return "\n".join(lines)
 
 
-def summarize_trace(stats_csv, cmd):
+def summarize_trace(stats_csv, cmd, workload="llama8b_s8"):
     import csv
 
     rows = list(csv.DictReader(open(stats_csv)))
-    lines = ["# Kernel trace, fl_round on the Llama-3.1-8B shard (S=8, R=8, G=4, A=8)", "",
+    d = W_ALL()[workload]().describe()
+    shape = ", ".join("%s=%s" % (k, d[k]) for k in d if k != "workload")
+    lines = ["# Kernel trace, one fl_round per step: %s" % d["workload"], "", shape, "",
              "    " + cmd, "",
              "| kernel | calls | average us | min us | max us | share of GPU time |",
              "|---|---|---|---|---|---|"]
@@ -132,6 +134,21 @@ def summarize_trace(stats_csv, cmd):
             float(r["MinNs"]) / 1e3, float(r["MaxNs"]) / 1e3, float(r["Percentage"])))
     lines.append("")
     return "\n".join(lines)
+
+
+def step_label(w):
+    """The kernels of one local step, as the roofline figure counts them."""
+    fused = "k_step<%s=%d, fused, %s>" % ("R" if w.H == 1 else "H", w.R if w.H == 1 else w.H,
+                                         "clipped" if w.max_grad_norm > 0 else
+                                         "per-segment sums")
+    parts = []
+    if w.H > 1:
+        parts.append("k_step<R=%d, wire>" % w.R)
+    if w.max_grad_norm > 0:
+        parts.append("k_step<%s=%d, sum of squares> + finalize" % (
+            "R" if w.H == 1 else "H", w.R if w.H == 1 else w.H))
+    parts.append(fused)
+    return "one local step: " + " + ".join(parts)
 
 
 def W_ALL():
@@ -190,7 +207,7 @@ def main():
                             args.copy_calibration or 1024, cmds[0], cmds[1]))
         return
     if args.summarize_trace:
-        print(summarize_trace(args.summarize_trace, (args.cmd + [""])[0]))
+        print(summarize_trace(args.summarize_trace, (args.cmd + [""])[0], args.workload))
         return
     if args.gpus != 1:
         print("bench.py measures one GPU's share of the path; the multi-GPU collectives are "
@@ -291,10 +308,7 @@ def main():
                           fedavg_gbs=round(fed_bytes / (avg_fed * 1e-3) / 1e9, 2)),
         "roofline": {
             "bound": "hbm",
-            "kernel": ("k_step<R=%d, fused, per-segment sums> (one local step)" % w.R
-                       if w.H == 1 else
-                       "one local step: k_step<R=%d, wire> + k_step<H=%d, fused, per-segment "
-                       "sums>" % (w.R, w.H)),
+            "kernel": step_label(w),
             "achieved": round(achieved, 2),
             "peak": PEAK_HBM_GBS,
             "unit": "GB/s",

@@ -119,10 +119,11 @@ typedef struct {
  * peer_grads: host array of R device pointers to N bf16 values (may repeat).
  * grad_out: device pointer, N floats (must not overlap an input).
  * seg_sumsq: NULL, or device pointer to n_seg floats receiving, per segment,
- *   the sum of grad_out[i]^2 (fp32 squares, partial sums in a fixed tree,
- *   final sum in double): per-layer gradient-norm telemetry.  Needs a
- *   stream-ordered temporary of 16 bytes per (2048-element tile, segment)
- *   pair, allocated and freed on `stream`.
+ *   the sum of grad_out[i]^2 (
+ *   exact double squares, fixed-tree double sums, rounded once to float):
+ *   per-layer gradient-norm telemetry.  Needs a stream-ordered temporary of
+ *   32 bytes per (2048-element tile, segment) pair, allocated and freed on
+ *   `stream`.
  * 1 <= R <= FL_MAX_PEERS; grad_scale finite.
  * ---------------------------------------------------------------------- */
 int fl_shard_reduce(const fl_layout* layout, int R, const uint16_t* const* peer_grads,
@@ -200,7 +201,8 @@ int fl_fedavg(const fl_layout* layout, int G, const uint16_t* const* replicas,
  *   see fl_shard_reduce).
  * Configuration: 1 <= R <= FL_MAX_PEERS, 1 <= G <= FL_MAX_GROUPS, A >= 1,
  *   0 <= self_group < G, step0 >= 1, grad_scale finite, h and weights as
- *   above, replica_fp as in fl_fedavg, step_lr entries finite and >= 0.
+ *   above, replica_fp as in fl_fedavg, step_lr entries finite and >= 0,
+ *   max_grad_norm finite.
  * phase_events: NULL, or host array of A+2 hipEvent_t created by the caller;
  *   event a (a < A) is recorded on `stream` before local step a, event A
  *   before FedAvg, event A+1 after it (per-phase timing of the round, like
@@ -219,6 +221,8 @@ typedef struct {
   void* const* phase_events; /* NULL or host, A+2 hipEvent_t                */
   const float* step_lr;      /* NULL or host, A learning rates, one per local
                                 step (overrides h.lr; e.g. fl_lr_cosine)   */
+  float max_grad_norm;       /* > 0: clip each local step's gradient to this
+                                global norm (fl_local_step_clipped); 0: off */
 } fl_round_cfg;
 
 int fl_round(const fl_layout* layout, const fl_round_cfg* cfg, const uint16_t* const* grads,
@@ -239,6 +243,33 @@ int fl_round(const fl_layout* layout, const fl_round_cfg* cfg, const uint16_t* c
  * ---------------------------------------------------------------------- */
 float fl_lr_cosine(int64_t t, int64_t total_steps, int64_t warmup_steps, float lr_max,
                    float lr_min);
+
+/* ------------------------------------------------------------------------
+ * Global-norm gradient clipping of a local step (the rule of
+ * torch.nn.utils.clip_grad_norm_), driven by the sum of squares of the
+ * reduced gradient:
+ *     coef = (float)min(1, max_norm / (sqrt(total_sumsq) + 1e-6))   (double)
+ *     g[i] = (acc[i] * grad_scale) * coef, then AdamW as fl_local_step
+ * The norm is over the whole model, i.e. over every shard of the sharding
+ * group: a multi-GPU caller computes its shard's sum with fl_grad_sumsq,
+ * all-reduces it, then calls fl_local_step_clipped.  Within one GPU,
+ * fl_round_cfg.max_grad_norm does both for the local shard (the per-segment
+ * sums then report the unclipped gradient).  coef == 1 leaves the step
+ * bitwise equal to the unclipped one.
+ *
+ * fl_grad_sumsq: total_sumsq = sum_i (double)g[i]^2 of this shard's reduced
+ *   gradient (exact double squares, fixed-tree double sums), written to a
+ *   device double (8-byte aligned); seg_sumsq: NULL or n_seg floats as in
+ *   fl_shard_reduce.  Reads the R gradients once and writes no gradient.
+ * fl_local_step_clipped: fl_local_step with the coefficient above, from a
+ *   device double total_sumsq; max_norm > 0 and finite.
+ * ---------------------------------------------------------------------- */
+int fl_grad_sumsq(const fl_layout* layout, int R, const uint16_t* const* peer_grads,
+                  float grad_scale, double* total_sumsq, float* seg_sumsq, void* stream);
+int fl_local_step_clipped(const fl_layout* layout, const fl_adamw_hparams* h, int64_t step, int R,
+                          const uint16_t* const* peer_grads, float grad_scale,
+                          const double* total_sumsq, float max_norm, float* master, float* m,
+                          float* v, uint16_t* working, void* stream);
 
 /* ------------------------------------------------------------------------
  * Outer optimiser (Section 3: DiLoCo and Photon pair the inner AdamW with an
@@ -334,8 +365,10 @@ int fl_round_hsdp(const fl_layout* layout, const fl_round_cfg* cfg, const fl_hsd
 /* ------------------------------------------------------------------------
  * Launch-shape control, for tuning sweeps and for tests that check that
  * results do not depend on the launch shape.  blocks_per_cu > 0 caps the
- * grid of the streaming kernels at blocks_per_cu * (number of CUs); 0
- * restores the default.  Process-wide; returns the previous value.
+ * grid of every streaming kernel at blocks_per_cu * (number of CUs); 0
+ * restores the defaults (one workgroup per CU for the fused step and the
+ * FedAvg-side passes, more for the passes that only read the peer gradients,
+ * by R).  Process-wide; returns the previous value.
  * ---------------------------------------------------------------------- */
 int fl_set_blocks_per_cu(int blocks_per_cu);
 

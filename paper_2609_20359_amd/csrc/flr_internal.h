@@ -66,8 +66,10 @@ struct StepArgs {
   float* g_out;        // standalone reduce: fp32 reduced gradient
   const float* g_in;   // standalone AdamW: fp32 gradient
   uint16_t* wire_out;  // reduce to the bf16 wire format
-  float* partials;     // per-(piece, wave) sums of squares, kWaves per piece
+  double* partials;    // per-(piece, wave) sums of squares, kWaves per piece
                        // (null: not requested)
+  const double* clip_total;  // MODE 0: whole-shard sum of squares, clipping on
+  float clip_max;            // its max norm
 };
 
 struct FedArgs {
@@ -91,9 +93,12 @@ hipError_t launch_reduce_wire(const StepArgs& a, int grid, hipStream_t st);
 hipError_t launch_bcast_recv(int64_t n, const float* recv, float* master, uint16_t* working,
                              int grid, hipStream_t st);
 hipError_t launch_fedavg(const FedArgs& a, int grid, hipStream_t st);
-// Per-segment totals from the (piece, wave) partials; chunk_sums is a
-// temporary of L.n_chunks doubles.
-hipError_t launch_seg_finalize(const LayoutDev& L, const float* partials, double* chunk_sums,
-                               float* out, hipStream_t st);
+// Per-segment totals from the (piece, wave) partials: chunk_sums
+// (L.n_chunks doubles) and seg_dbl (L.n_seg doubles) are temporaries; out
+// (n_seg floats) and total (one double, the whole shard) may be null.
+hipError_t launch_seg_finalize(const LayoutDev& L, const double* partials, double* chunk_sums,
+                               double* seg_dbl, float* out, double* total, hipStream_t st);
+hipError_t launch_sumsq_only(const StepArgs& a, int grid, hipStream_t st);
+hipError_t launch_zero_total(double* total, hipStream_t st);
 
 }  // namespace flr

@@ -29,8 +29,20 @@ struct fl_layout {
 
 namespace {
 
-int g_blocks_per_cu = 0;  // 0: default
+int g_blocks_per_cu = 0;  // 0: the per-pass defaults below
+
+// Default workgroups per CU.  One 256-thread workgroup per CU keeps enough
+// 16-byte loads in flight for the passes that stream many arrays (the fused
+// step, FedAvg, the optimiser-only and broadcast passes).  A pass that only
+// reads the R peer gradients (the sum-of-squares pass, and the reductions when
+// R is small) has fewer loads in flight per thread and needs more workgroups
+// to cover HBM latency.  Chosen by occupancy sweeps on a 1.0e9-element shard.
 constexpr int kDefaultBlocksPerCu = 1;
+int sumsq_blocks_per_cu(int R) {
+  return R >= 8 ? 2 : R >= 4 ? 3 : R == 3 ? 4 : R == 2 ? 6 : 8;
+}
+int reduce_blocks_per_cu(int R) { return R >= 8 ? 1 : 2; }
+int wire_blocks_per_cu(int R) { return R >= 8 ? 1 : R >= 2 ? 2 : 4; }
 
 constexpr uint64_t kFnvOffset = 0xCBF29CE484222325ULL;
 constexpr uint64_t kFnvPrime = 0x100000001B3ULL;
@@ -119,6 +131,7 @@ fl_adamw_hparams step_hparams(const fl_round_cfg& c, int a) {
 }
 
 bool step_lrs_ok(const fl_round_cfg& c) {
+  if (!std::isfinite(c.max_grad_norm)) return false;
   if (!c.step_lr) return true;
   for (int a = 0; a < c.A; ++a)
     if (!std::isfinite(c.step_lr[a]) || !(c.step_lr[a] >= 0.f)) return false;
@@ -140,8 +153,8 @@ int check_device(const fl_layout* lay) {
   return dev == lay->device ? FL_OK : FL_ERR_DEVICE;
 }
 
-int grid_for(const fl_layout* lay, int64_t units) {
-  const int bpc = g_blocks_per_cu > 0 ? g_blocks_per_cu : kDefaultBlocksPerCu;
+int grid_for(const fl_layout* lay, int64_t units, int default_bpc = kDefaultBlocksPerCu) {
+  const int bpc = g_blocks_per_cu > 0 ? g_blocks_per_cu : default_bpc;
   int64_t cap = (int64_t)bpc * (int64_t)lay->num_cus;
   if (cap < 1) cap = 1;
   int64_t g = units < cap ? units : cap;
@@ -169,29 +182,32 @@ int check_peers(int R, const uint16_t* const* peers, int64_t n) {
 }
 
 // Stream-ordered temporary for the per-segment sums of squares: the
-// (piece, wave) partials (kWaves floats per piece) followed by one double
-// per finalize chunk.
+// (piece, wave) partials (kWaves doubles per piece), one double per finalize
+// chunk, one per segment, and the whole-shard total.
 struct Workspace {
-  float* p = nullptr;
+  double* p = nullptr;
   double* chunks = nullptr;
+  double* seg = nullptr;
+  double* total = nullptr;
   hipStream_t st = nullptr;
   int alloc(const flr::LayoutDev& L, hipStream_t stream) {
     st = stream;
-    size_t slots = (size_t)(L.n_pieces > 0 ? L.n_pieces : 1) * flr::kWaves;
-    slots = (slots + 3) & ~(size_t)3;  // keep the double region 16-byte aligned
-    const size_t bytes = slots * sizeof(float) + (size_t)(L.n_chunks > 0 ? L.n_chunks : 1) * sizeof(double);
+    const size_t slots = (size_t)(L.n_pieces > 0 ? L.n_pieces : 1) * flr::kWaves;
+    const size_t nch = (size_t)(L.n_chunks > 0 ? L.n_chunks : 1);
+    const size_t nseg = (size_t)(L.n_seg > 0 ? L.n_seg : 1);
     void* q = nullptr;
-    const hipError_t e = hipMallocAsync(&q, bytes, st);
+    const hipError_t e = hipMallocAsync(&q, (slots + nch + nseg + 1) * sizeof(double), st);
     if (e != hipSuccess) return status_of(e);
-    p = static_cast<float*>(q);
-    chunks = reinterpret_cast<double*>(p + slots);
+    p = static_cast<double*>(q);
+    chunks = p + slots;
+    seg = chunks + nch;
+    total = seg + nseg;
     return FL_OK;
   }
   int release() {
     if (!p) return FL_OK;
     const hipError_t e = hipFreeAsync(p, st);
-    p = nullptr;
-    chunks = nullptr;
+    p = chunks = seg = total = nullptr;
     return status_of(e);
   }
 };
@@ -204,23 +220,41 @@ flr::StepArgs step_args(const fl_layout* lay) {
 }
 
 // Enqueue one fused local step (and, with seg_sumsq, its per-segment sums).
+// With clip_max > 0 the step first runs a sum-of-squares pass over the same
+// inputs (whole-shard total and, if asked, the per-segment sums), then the
+// fused step with the gradient scaled by the clip coefficient.
 int enqueue_local_step(const fl_layout* lay, const fl_adamw_hparams& h, int64_t step, int R,
                        const uint16_t* const* peers, float grad_scale, float* master, float* m,
                        float* v, uint16_t* working, const Workspace& ws, float* seg_sumsq,
-                       hipStream_t st) {
+                       hipStream_t st, float clip_max = 0.f) {
   flr::StepArgs a = step_args(lay);
   for (int r = 0; r < R; ++r) a.grads[r] = peers[r];
   a.R = R;
   a.grad_scale = grad_scale;
+  const int grid = grid_for(lay, lay->L.n_tiles);
+  int rc = FL_OK;
+  if (clip_max > 0.f) {
+    a.partials = ws.p;
+    rc = status_of(flr::launch_sumsq_only(a, grid_for(lay, lay->L.n_tiles,
+                                                      sumsq_blocks_per_cu(R)), st));
+    if (rc == FL_OK)
+      rc = status_of(flr::launch_seg_finalize(lay->L, ws.p, ws.chunks, ws.seg, seg_sumsq,
+                                              ws.total, st));
+    a.partials = nullptr;
+    a.clip_total = ws.total;
+    a.clip_max = clip_max;
+    seg_sumsq = nullptr;
+  }
   a.s = adam_scalars(h, step);
   a.master = master;
   a.m = m;
   a.v = v;
   a.working = working;
-  a.partials = seg_sumsq ? ws.p : nullptr;
-  int rc = status_of(flr::launch_local_step(a, grid_for(lay, lay->L.n_tiles), st));
+  if (seg_sumsq) a.partials = ws.p;
+  if (rc == FL_OK) rc = status_of(flr::launch_local_step(a, grid, st));
   if (rc == FL_OK && seg_sumsq)
-    rc = status_of(flr::launch_seg_finalize(lay->L, ws.p, ws.chunks, seg_sumsq, st));
+    rc = status_of(flr::launch_seg_finalize(lay->L, ws.p, ws.chunks, ws.seg, seg_sumsq, nullptr,
+                                            st));
   return rc;
 }
 
@@ -270,7 +304,7 @@ const char* fl_status_string(int status) {
   }
 }
 
-int fl_version(void) { return (1 << 16) | 3; }
+int fl_version(void) { return (1 << 16) | 4; }
 
 float fl_lr_cosine(int64_t t, int64_t total_steps, int64_t warmup_steps, float lr_max,
                    float lr_min) {
@@ -453,9 +487,11 @@ int fl_shard_reduce(const fl_layout* layout, int R, const uint16_t* const* peer_
   a.grad_scale = grad_scale;
   a.g_out = grad_out;
   a.partials = ws.p;
-  rc = status_of(flr::launch_reduce(a, grid_for(layout, layout->L.n_tiles), st));
+  rc = status_of(flr::launch_reduce(a, grid_for(layout, layout->L.n_tiles,
+                                                reduce_blocks_per_cu(R)), st));
   if (rc == FL_OK && seg_sumsq)
-    rc = status_of(flr::launch_seg_finalize(layout->L, ws.p, ws.chunks, seg_sumsq, st));
+    rc = status_of(flr::launch_seg_finalize(layout->L, ws.p, ws.chunks, ws.seg, seg_sumsq,
+                                            nullptr, st));
   const int rc2 = ws.release();
   return rc != FL_OK ? rc : rc2;
 }
@@ -530,6 +566,67 @@ int fl_fedavg(const fl_layout* layout, int G, const uint16_t* const* replicas,
                         static_cast<hipStream_t>(stream));
 }
 
+int fl_grad_sumsq(const fl_layout* layout, int R, const uint16_t* const* peer_grads,
+                  float grad_scale, double* total_sumsq, float* seg_sumsq, void* stream) {
+  if (!layout || !total_sumsq) return FL_ERR_INVALID;
+  const int64_t n = layout->L.n;
+  int rc = check_peers(R, peer_grads, n);
+  if (rc != FL_OK) return rc;
+  if (!finite(grad_scale)) return FL_ERR_INVALID;
+  if (reinterpret_cast<uintptr_t>(total_sumsq) & 7u) return FL_ERR_ALIGN;
+  if (seg_sumsq && (reinterpret_cast<uintptr_t>(seg_sumsq) & 3u)) return FL_ERR_ALIGN;
+  if ((rc = check_device(layout)) != FL_OK) return rc;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  if (n == 0) return status_of(flr::launch_zero_total(total_sumsq, st));
+  Workspace ws;
+  if ((rc = ws.alloc(layout->L, st)) != FL_OK) return rc;
+  flr::StepArgs a = step_args(layout);
+  for (int r = 0; r < R; ++r) a.grads[r] = peer_grads[r];
+  a.R = R;
+  a.grad_scale = grad_scale;
+  a.partials = ws.p;
+  rc = status_of(flr::launch_sumsq_only(a, grid_for(layout, layout->L.n_tiles,
+                                                    sumsq_blocks_per_cu(R)), st));
+  if (rc == FL_OK)
+    rc = status_of(flr::launch_seg_finalize(layout->L, ws.p, ws.chunks, ws.seg, seg_sumsq,
+                                            total_sumsq, st));
+  const int rc2 = ws.release();
+  return rc != FL_OK ? rc : rc2;
+}
+
+int fl_local_step_clipped(const fl_layout* layout, const fl_adamw_hparams* h, int64_t step, int R,
+                          const uint16_t* const* peer_grads, float grad_scale,
+                          const double* total_sumsq, float max_norm, float* master, float* m,
+                          float* v, uint16_t* working, void* stream) {
+  if (!layout || !hparams_ok(h) || step < 1 || !finite(grad_scale) || !total_sumsq ||
+      !finite(max_norm) || !(max_norm > 0.f))
+    return FL_ERR_INVALID;
+  const int64_t n = layout->L.n;
+  int rc = check_peers(R, peer_grads, n);
+  if (rc != FL_OK) return rc;
+  if ((rc = dev_ptr(master, n)) != FL_OK) return rc;
+  if ((rc = dev_ptr(m, n)) != FL_OK) return rc;
+  if ((rc = dev_ptr(v, n)) != FL_OK) return rc;
+  if ((rc = dev_ptr(working, n)) != FL_OK) return rc;
+  if (reinterpret_cast<uintptr_t>(total_sumsq) & 7u) return FL_ERR_ALIGN;
+  if (n > 0 && (master == m || master == v || m == v)) return FL_ERR_INVALID;
+  if ((rc = check_device(layout)) != FL_OK) return rc;
+  if (n == 0) return FL_OK;
+  flr::StepArgs a = step_args(layout);
+  for (int r = 0; r < R; ++r) a.grads[r] = peer_grads[r];
+  a.R = R;
+  a.grad_scale = grad_scale;
+  a.s = adam_scalars(*h, step);
+  a.master = master;
+  a.m = m;
+  a.v = v;
+  a.working = working;
+  a.clip_total = total_sumsq;
+  a.clip_max = max_norm;
+  return status_of(flr::launch_local_step(a, grid_for(layout, layout->L.n_tiles),
+                                          static_cast<hipStream_t>(stream)));
+}
+
 int fl_shard_reduce_wire(const fl_layout* layout, int R, const uint16_t* const* peer_grads,
                          float grad_scale, uint16_t* wire_out, void* stream) {
   if (!layout) return FL_ERR_INVALID;
@@ -545,7 +642,8 @@ int fl_shard_reduce_wire(const fl_layout* layout, int R, const uint16_t* const* 
   a.R = R;
   a.grad_scale = grad_scale;
   a.wire_out = wire_out;
-  return status_of(flr::launch_reduce_wire(a, grid_for(layout, layout->L.n_tiles),
+  return status_of(flr::launch_reduce_wire(a, grid_for(layout, layout->L.n_tiles,
+                                                        wire_blocks_per_cu(R)),
                                            static_cast<hipStream_t>(stream)));
 }
 
@@ -630,7 +728,8 @@ int fl_round_hsdp(const fl_layout* layout, const fl_round_cfg* cfg, const fl_hsd
     return status_of(hipEventRecord(static_cast<hipEvent_t>(c.phase_events[k]), st));
   };
   Workspace ws;
-  if (n > 0 && seg_sumsq && (rc = ws.alloc(layout->L, st)) != FL_OK) return rc;
+  if (n > 0 && (seg_sumsq || c.max_grad_norm > 0.f) && (rc = ws.alloc(layout->L, st)) != FL_OK)
+    return rc;
   for (int a = 0; a < c.A && rc == FL_OK; ++a) {
     rc = record(a);
     if (rc != FL_OK || n == 0) continue;
@@ -638,7 +737,7 @@ int fl_round_hsdp(const fl_layout* layout, const fl_round_cfg* cfg, const fl_hsd
     const uint16_t* const* ga = grads + (size_t)a * (size_t)c.R;
     if (hc->H == 1) {
       rc = enqueue_local_step(layout, step_hparams(c, a), c.step0 + a, c.R, ga, c.grad_scale,
-                              master, m, v, working, ws, ss, st);
+                              master, m, v, working, ws, ss, st, c.max_grad_norm);
       continue;
     }
     // tier 1: the sharding group's reduction, in the bf16 wire format
@@ -647,7 +746,8 @@ int fl_round_hsdp(const fl_layout* layout, const fl_round_cfg* cfg, const fl_hsd
     t1.R = c.R;
     t1.grad_scale = c.grad_scale;
     t1.wire_out = wire;
-    rc = status_of(flr::launch_reduce_wire(t1, grid_for(layout, layout->L.n_tiles), st));
+    rc = status_of(flr::launch_reduce_wire(
+        t1, grid_for(layout, layout->L.n_tiles, wire_blocks_per_cu(c.R)), st));
     // tier 2: the replication group's average of the H wire shards, fused
     // with the optimiser step
     const uint16_t* wires[FL_MAX_PEERS];
@@ -655,7 +755,7 @@ int fl_round_hsdp(const fl_layout* layout, const fl_round_cfg* cfg, const fl_hsd
       wires[k] = (k == hc->replica) ? wire : replica_wires[(size_t)a * (size_t)hc->H + (size_t)k];
     if (rc == FL_OK)
       rc = enqueue_local_step(layout, step_hparams(c, a), c.step0 + a, hc->H, wires,
-                              hc->hsdp_scale, master, m, v, working, ws, ss, st);
+                              hc->hsdp_scale, master, m, v, working, ws, ss, st, c.max_grad_norm);
   }
   if (rc == FL_OK) rc = record(c.A);
   if (rc == FL_OK && n > 0) {
@@ -774,14 +874,15 @@ static int round_impl(const fl_layout* layout, const fl_round_cfg* cfg,
     return status_of(hipEventRecord(static_cast<hipEvent_t>(c.phase_events[k]), st));
   };
   Workspace ws;
-  if (n > 0 && seg_sumsq && (rc = ws.alloc(layout->L, st)) != FL_OK) return rc;
+  if (n > 0 && (seg_sumsq || c.max_grad_norm > 0.f) && (rc = ws.alloc(layout->L, st)) != FL_OK)
+    return rc;
   for (int a = 0; a < c.A && rc == FL_OK; ++a) {
     rc = record(a);
     if (rc == FL_OK && n > 0)
       rc = enqueue_local_step(layout, step_hparams(c, a), c.step0 + a, c.R,
                               grads + (size_t)a * (size_t)c.R, c.grad_scale, master, m, v, working, ws,
                               seg_sumsq ? seg_sumsq + (size_t)a * (size_t)layout->L.n_seg : nullptr,
-                              st);
+                              st, c.max_grad_norm);
   }
   if (rc == FL_OK) rc = record(c.A);
   if (rc == FL_OK && n > 0)

@@ -25,6 +25,7 @@ namespace {
 
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef double f64x2 __attribute__((ext_vector_type(2)));
 
 // Cache hints.  ld_once: streams read once per pass (peer gradients, FedAvg
 // replicas); ld: the read-modify-write state (master, m, v, fp32 gradient);
@@ -162,10 +163,17 @@ __device__ __forceinline__ void reduce_tail(const StepArgs& a, int64_t base, int
 
 // Fixed-tree sum over one wave64: butterfly exchange, after which every lane
 // holds the same bits (each step adds the same two partials in both lanes).
-__device__ __forceinline__ float wave_sum(float v) {
+__device__ __forceinline__ double wave_sum(double v) {
 #pragma unroll
   for (int off = 32; off >= 1; off >>= 1) v = v + __shfl_xor(v, off, 64);
   return v;
+}
+
+// Clip coefficient from the whole-shard sum of squares: min(1, max / (norm +
+// 1e-6)) in double, rounded once to float.
+__device__ __forceinline__ float clip_coef(const double* total, float max_norm) {
+  const double c = (double)max_norm / (__builtin_sqrt(*total) + 1e-6);
+  return (float)(c < 1.0 ? c : 1.0);
 }
 
 // Segment of element `i`, searching [lo, hi] (segments overlapping the tile).
@@ -177,12 +185,16 @@ __device__ __forceinline__ int find_seg(const int64_t* off, int lo, int hi, int6
   return lo;
 }
 
-// MODE 0: fused reduce + AdamW + working copy; 1: reduce only (g_out);
-// 2: AdamW only (g_in); 3: reduce to the bf16 wire format (wire_out).
-// SUMSQ: per-piece sums of squares of g.
+// MODE 0: fused reduce + AdamW + working copy (g scaled by the clip
+// coefficient when a.clip_total is set); 1: reduce only (g_out); 2: AdamW
+// only (g_in); 3: reduce to the bf16 wire format (wire_out); 4: reduce with
+// no output but the sums of squares.  SUMSQ: per-piece sums of squares of g
+// (before clipping).
 template <int RT, int MODE, bool SUMSQ>
 __global__ void __launch_bounds__(kBlock) k_step(const StepArgs a) {
   const int tid = threadIdx.x;
+  const bool clip = MODE == 0 && a.clip_total != nullptr;
+  const float coef = clip ? clip_coef(a.clip_total, a.clip_max) : 1.0f;
   for (int64_t t = blockIdx.x; t < a.L.n_tiles; t += gridDim.x) {
     const TileInfo ti = a.L.tiles[t];
     const int64_t base = t * kTile + (int64_t)tid * kVec;
@@ -227,7 +239,9 @@ __global__ void __launch_bounds__(kBlock) k_step(const StepArgs a) {
       }
     }
 
-    if constexpr (MODE == 1) {
+    if constexpr (MODE == 4) {
+      // sums of squares only
+    } else if constexpr (MODE == 1) {
       if (cnt == kVec) {
         store_f32x8(a.g_out + base, g);
       } else {
@@ -241,6 +255,9 @@ __global__ void __launch_bounds__(kBlock) k_step(const StepArgs a) {
       }
     } else {
       const AdamScalars& s = a.s;
+      float gc[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) gc[e] = clip ? g[e] * coef : g[e];
       float d[8];
       if (ti.nseg == 1) {
         const float du = ti.decay ? s.decay : 1.0f;
@@ -253,8 +270,8 @@ __global__ void __launch_bounds__(kBlock) k_step(const StepArgs a) {
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
         float pe = p[e] * d[e];
-        const float mn = (s.b1 * m[e]) + (s.omb1 * g[e]);
-        const float vn = (s.b2 * v[e]) + (s.omb2 * (g[e] * g[e]));
+        const float mn = (s.b1 * m[e]) + (s.omb1 * gc[e]);
+        const float vn = (s.b2 * v[e]) + (s.omb2 * (gc[e] * gc[e]));
         const float den = (__builtin_sqrtf(vn) / s.bc2_sqrt) + s.eps;
         pe = pe - (s.step_size * (mn / den));
         p[e] = pe; m[e] = mn; v[e] = vn;
@@ -275,22 +292,24 @@ __global__ void __launch_bounds__(kBlock) k_step(const StepArgs a) {
     }
 
     if constexpr (SUMSQ) {
-      // One partial per (piece, wave): the wave's share of the piece, summed
-      // in fp32 (8 elements in order, then the wave butterfly); no barrier.
+      // One partial per (piece, wave): the wave's share of the piece, the
+      // exact double squares of its 8 elements per lane summed in order, then
+      // the wave butterfly; no barrier.
       const int wid = tid >> 6;
       if (ti.nseg == 1) {
-        float acc = 0.f;
+        double acc = 0.0;
 #pragma unroll
-        for (int e = 0; e < 8; ++e) if (e < cnt) acc = acc + g[e] * g[e];
-        const float tot = wave_sum(acc);
+        for (int e = 0; e < 8; ++e) if (e < cnt) acc = acc + (double)g[e] * (double)g[e];
+        const double tot = wave_sum(acc);
         if ((tid & 63) == 0) a.partials[(int64_t)ti.piece0 * kWaves + wid] = tot;
       } else {
         for (int j = 0; j < ti.nseg; ++j) {
           const int sj = ti.seg0 + j;
-          float acc = 0.f;
+          double acc = 0.0;
 #pragma unroll
-          for (int e = 0; e < 8; ++e) if (e < cnt && seg[e] == sj) acc = acc + g[e] * g[e];
-          const float tot = wave_sum(acc);
+          for (int e = 0; e < 8; ++e)
+            if (e < cnt && seg[e] == sj) acc = acc + (double)g[e] * (double)g[e];
+          const double tot = wave_sum(acc);
           if ((tid & 63) == 0) a.partials[((int64_t)ti.piece0 + j) * kWaves + wid] = tot;
         }
       }
@@ -380,13 +399,14 @@ __global__ void __launch_bounds__(kBlock) k_fedavg(const FedArgs a) {
   }
 }
 
-// Per-segment totals of the (piece, wave) partials, in double, in two fixed
+// Per-segment totals of the (piece, wave) partials, in double, in fixed
 // trees that do not depend on the grid.  Stage 1: one workgroup per chunk of
 // up to kChunkPieces pieces of one segment; thread j folds pieces j, j+256,
 // ... (each piece's kWaves slots in order), then a wave64 butterfly and the 4
 // wave totals in order.  Stage 2: one thread per segment adds its chunks in
-// order.
-__global__ void __launch_bounds__(kBlock) k_seg_chunks(const LayoutDev L, const float* partials,
+// order (double per segment, and its float rounding if requested).  Stage 3
+// (whole-shard total, for clipping): one workgroup folds the segments.
+__global__ void __launch_bounds__(kBlock) k_seg_chunks(const LayoutDev L, const double* partials,
                                                        double* chunk_sums) {
   __shared__ double red[4];
   for (int64_t c = blockIdx.x; c < L.n_chunks; c += gridDim.x) {
@@ -394,14 +414,14 @@ __global__ void __launch_bounds__(kBlock) k_seg_chunks(const LayoutDev L, const 
     const int64_t p1 = L.chunk_p0[c + 1];
     double acc = 0.0;
     for (int64_t p = p0 + threadIdx.x; p < p1; p += kBlock) {
-      const f32x4 w = *reinterpret_cast<const f32x4*>(partials + p * kWaves);
-      acc = acc + (double)w.x;
-      acc = acc + (double)w.y;
-      acc = acc + (double)w.z;
-      acc = acc + (double)w.w;
+      const f64x2 w0 = *reinterpret_cast<const f64x2*>(partials + p * kWaves);
+      const f64x2 w1 = *reinterpret_cast<const f64x2*>(partials + p * kWaves + 2);
+      acc = acc + w0.x;
+      acc = acc + w0.y;
+      acc = acc + w1.x;
+      acc = acc + w1.y;
     }
-#pragma unroll
-    for (int off = 32; off >= 1; off >>= 1) acc = acc + __shfl_xor(acc, off, 64);
+    acc = wave_sum(acc);
     if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = acc;
     __syncthreads();
     if (threadIdx.x == 0) chunk_sums[c] = ((red[0] + red[1]) + red[2]) + red[3];
@@ -410,13 +430,25 @@ __global__ void __launch_bounds__(kBlock) k_seg_chunks(const LayoutDev L, const 
 }
 
 __global__ void __launch_bounds__(kBlock) k_seg_totals(const LayoutDev L, const double* chunk_sums,
-                                                       float* out) {
+                                                       double* seg_dbl, float* out) {
   const int64_t stride = (int64_t)gridDim.x * kBlock;
   for (int64_t s = (int64_t)blockIdx.x * kBlock + threadIdx.x; s < L.n_seg; s += stride) {
     double acc = 0.0;
     for (int64_t c = L.seg_chunk0[s]; c < L.seg_chunk0[s + 1]; ++c) acc = acc + chunk_sums[c];
-    out[s] = (float)acc;
+    seg_dbl[s] = acc;
+    if (out) out[s] = (float)acc;
   }
+}
+
+__global__ void __launch_bounds__(kBlock) k_total(const int64_t n_seg, const double* seg_dbl,
+                                                  double* total) {
+  __shared__ double red[4];
+  double acc = 0.0;
+  for (int64_t s = threadIdx.x; s < n_seg; s += kBlock) acc = acc + seg_dbl[s];
+  acc = wave_sum(acc);
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = acc;
+  __syncthreads();
+  if (threadIdx.x == 0) *total = ((red[0] + red[1]) + red[2]) + red[3];
 }
 
 // Broadcast receive: master = recv; working = bf16(recv).
@@ -504,8 +536,8 @@ hipError_t launch_fedavg(const FedArgs& a, int grid, hipStream_t st) {
   return a.prev ? dispatch_fedavg<true>(a, grid, st) : dispatch_fedavg<false>(a, grid, st);
 }
 
-hipError_t launch_seg_finalize(const LayoutDev& L, const float* partials, double* chunk_sums,
-                               float* out, hipStream_t st) {
+hipError_t launch_seg_finalize(const LayoutDev& L, const double* partials, double* chunk_sums,
+                               double* seg_dbl, float* out, double* total, hipStream_t st) {
   if (L.n_seg == 0) return hipSuccess;
   const int g1 = (int)(L.n_chunks < 65535 ? L.n_chunks : 65535);
   void* a1[] = {const_cast<LayoutDev*>(&L), &partials, &chunk_sums};
@@ -514,8 +546,23 @@ hipError_t launch_seg_finalize(const LayoutDev& L, const float* partials, double
   if (e != hipSuccess) return e;
   const int64_t b2 = (L.n_seg + kBlock - 1) / kBlock;
   const int g2 = (int)(b2 < 65535 ? b2 : 65535);
-  void* a2[] = {const_cast<LayoutDev*>(&L), &chunk_sums, &out};
-  return hipLaunchKernel((const void*)k_seg_totals, dim3((unsigned)g2), dim3(kBlock), a2, 0, st);
+  void* a2[] = {const_cast<LayoutDev*>(&L), &chunk_sums, &seg_dbl, &out};
+  e = hipLaunchKernel((const void*)k_seg_totals, dim3((unsigned)g2), dim3(kBlock), a2, 0, st);
+  if (e != hipSuccess || !total) return e;
+  int64_t n_seg = L.n_seg;
+  void* a3[] = {&n_seg, &seg_dbl, &total};
+  return hipLaunchKernel((const void*)k_total, dim3(1), dim3(kBlock), a3, 0, st);
+}
+
+hipError_t launch_zero_total(double* total, hipStream_t st) {
+  int64_t n_seg = 0;
+  const double* none = nullptr;
+  void* a3[] = {&n_seg, &none, &total};
+  return hipLaunchKernel((const void*)k_total, dim3(1), dim3(kBlock), a3, 0, st);
+}
+
+hipError_t launch_sumsq_only(const StepArgs& a, int grid, hipStream_t st) {
+  return dispatch_step<4, true>(a, grid, st);
 }
 
 }  // namespace flr

@@ -30,7 +30,7 @@ EXPORTS = ("fl_status_string", "fl_version", "fl_layout_create", "fl_layout_dest
            "fl_layout_fingerprint", "fl_shard_reduce", "fl_adamw_step", "fl_local_step",
            "fl_fedavg", "fl_round", "fl_set_blocks_per_cu", "fl_shard_reduce_wire",
            "fl_broadcast_recv", "fl_round_hsdp", "fl_fedopt", "fl_round_outer",
-           "fl_lr_cosine")
+           "fl_lr_cosine", "fl_grad_sumsq", "fl_local_step_clipped")
 
 _P = ctypes.c_void_p
 
@@ -53,7 +53,8 @@ class RoundCfg(ctypes.Structure):
                 ("weights", ctypes.POINTER(ctypes.c_float)),
                 ("replica_fp", ctypes.POINTER(ctypes.c_uint64)),
                 ("phase_events", ctypes.POINTER(ctypes.c_void_p)),
-                ("step_lr", ctypes.POINTER(ctypes.c_float))]
+                ("step_lr", ctypes.POINTER(ctypes.c_float)),
+                ("max_grad_norm", ctypes.c_float)]
 
 
 class OuterHparams(ctypes.Structure):
@@ -111,6 +112,10 @@ def lib():
                                 _P, _P, _P]
         L.fl_round_outer.argtypes = [_P, ctypes.POINTER(RoundCfg), ctypes.POINTER(OuterHparams),
                                      _P, _P, _P, _P, _P, _P, _P, _P, _P, _P]
+        L.fl_grad_sumsq.argtypes = [_P, ctypes.c_int, _P, ctypes.c_float, _P, _P, _P]
+        L.fl_local_step_clipped.argtypes = [_P, ctypes.POINTER(AdamwHparams), ctypes.c_int64,
+                                            ctypes.c_int, _P, ctypes.c_float, _P, ctypes.c_float,
+                                            _P, _P, _P, _P, _P]
         L.fl_lr_cosine.argtypes = [ctypes.c_int64, ctypes.c_int64, ctypes.c_int64, ctypes.c_float,
                                    ctypes.c_float]
         L.fl_lr_cosine.restype = ctypes.c_float
@@ -237,14 +242,14 @@ def fl_fedavg(layout, replicas, weights, master_out, working_out, replica_fp=Non
 
 
 def make_round_cfg(R, G, A, weights, hp, *, self_group=0, grad_scale=None, step0=1,
-                   replica_fp=None, phase_events=None, step_lr=None):
+                   replica_fp=None, phase_events=None, step_lr=None, max_grad_norm=0.0):
     """Build an fl_round_cfg; the returned object keeps its arrays alive."""
     w = (ctypes.c_float * G)(*[float(x) for x in weights])
     fp = None if replica_fp is None else (ctypes.c_uint64 * G)(*[int(x) for x in replica_fp])
     ev = None if phase_events is None else (ctypes.c_void_p * len(phase_events))(*phase_events)
     lrs = None if step_lr is None else (ctypes.c_float * len(step_lr))(*[float(x) for x in step_lr])
     cfg = RoundCfg(R, G, A, self_group, float(1.0 / R if grad_scale is None else grad_scale),
-                   hparams(hp), int(step0), w, fp, ev, lrs)
+                   hparams(hp), int(step0), w, fp, ev, lrs, float(max_grad_norm))
     cfg._keep = (w, fp, ev, lrs)
     return cfg
 
@@ -294,6 +299,23 @@ def fl_round_hsdp(layout, cfg, hcfg, grads, replica_wires, wire, replicas, bcast
                              _ptr(bcast_master), _ptr(master), _ptr(m), _ptr(v), _ptr(working),
                              _ptr(seg_sumsq), _stream(stream))
     _check(rc, "fl_round_hsdp")
+
+
+def fl_grad_sumsq(layout, peer_grads, grad_scale, total_sumsq, seg_sumsq=None, stream=None):
+    """total_sumsq: a CUDA float64 tensor of one element."""
+    rc = lib().fl_grad_sumsq(layout.handle, len(peer_grads), _ptr_array(peer_grads),
+                             float(grad_scale), _ptr(total_sumsq), _ptr(seg_sumsq), _stream(stream))
+    _check(rc, "fl_grad_sumsq")
+
+
+def fl_local_step_clipped(layout, hp, step, peer_grads, grad_scale, total_sumsq, max_norm, master,
+                          m, v, working, stream=None):
+    h = hparams(hp)
+    rc = lib().fl_local_step_clipped(layout.handle, ctypes.byref(h), int(step), len(peer_grads),
+                                     _ptr_array(peer_grads), float(grad_scale), _ptr(total_sumsq),
+                                     float(max_norm), _ptr(master), _ptr(m), _ptr(v),
+                                     _ptr(working), _stream(stream))
+    _check(rc, "fl_local_step_clipped")
 
 
 def fl_fedopt(layout, replicas, weights, outer, prev, buf, master_out, working_out,

@@ -121,6 +121,8 @@ class Workload:
     # outer optimiser (None: plain FedAvg): dict(lr, momentum, nesterov); the
     # outer state starts at prev = the initial master, buf = 0
     outer: Optional[dict] = None
+    # global-norm clipping of each local step's gradient (0: off)
+    max_grad_norm: float = 0.0
 
     def __post_init__(self):
         if self.grad_scale is None:
@@ -145,6 +147,8 @@ class Workload:
         base = 2 * self.R + 12 + 12 + 2
         if self.H > 1:
             base += 2 + 2 * self.H
+        if self.max_grad_norm > 0:
+            base += 2 * (self.H if self.H > 1 else self.R)   # the sum-of-squares pass
         return base
 
     def fedavg_bytes_per_param(self):
@@ -167,6 +171,8 @@ class Workload:
             d.update(H=self.H, replica=self.replica, fedavg_member=self.hsdp_member)
         if self.outer is not None:
             d.update(outer=self.outer)
+        if self.max_grad_norm > 0:
+            d.update(max_grad_norm=self.max_grad_norm)
         return d
 
 
@@ -188,7 +194,7 @@ def _normal_grads(n_arrays, seed, std=GRAD_STD):
 def make_workload(name, seg_sizes, seg_decay, R, G, A, *, weights=None, seed=0,
                   distinct_grads=True, student=False, own_drift=False, hp=None,
                   self_group=0, step0=1, grad_scale=None, note="", H=1, replica=0,
-                  hsdp_member=True, outer=None):
+                  hsdp_member=True, outer=None, max_grad_norm=0.0):
     """General constructor used by the named workloads and by the tests.
 
     distinct_grads: A*R distinct gradient arrays (else R arrays reused by
@@ -231,7 +237,8 @@ def make_workload(name, seg_sizes, seg_decay, R, G, A, *, weights=None, seed=0,
                     hp=dict(hp or ADAMW), self_group=self_group, step0=step0,
                     grad_scale=grad_scale, note=note, H=H, replica=replica,
                     hsdp_member=hsdp_member, wire_specs=wires, bcast_spec=bcast,
-                    outer=None if outer is None else dict(outer))
+                    outer=None if outer is None else dict(outer),
+                    max_grad_norm=float(max_grad_norm))
 
 
 def tiny(seed=0):
@@ -301,10 +308,18 @@ def llama8b_s8_outer(seed=0):
                          seed=seed, distinct_grads=False, outer=DILOCO_OUTER)
 
 
+def llama8b_s8_clip(seed=0):
+    """The Llama-3.1-8B S=8 round with every local step's gradient clipped to
+    global norm 1.0 (a sum-of-squares pass before each fused step)."""
+    sizes, dec = llama31_8b_segments(8)
+    return make_workload("llama31_8b_fsdp_s8_r8_g4_a8_clip1", sizes, dec, R=8, G=4, A=8,
+                         seed=seed, distinct_grads=False, max_grad_norm=1.0)
+
+
 ALL = dict(tiny=tiny, llama8b_s8=llama8b_s8, fedavg_heavy=fedavg_heavy, hsdp_s4=hsdp_s4,
            stress=stress, hsdp_s4_h2=hsdp_s4_h2,
            hsdp_s4_h2_recv=lambda seed=0: hsdp_s4_h2(seed, member=False),
-           llama8b_s8_outer=llama8b_s8_outer)
+           llama8b_s8_outer=llama8b_s8_outer, llama8b_s8_clip=llama8b_s8_clip)
 
 
 def sample_indices(w, n_random=1 << 16, seed=1, full_segments=4, max_full=4096):

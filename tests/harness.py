@@ -6,6 +6,7 @@ host values for the oracle side); expected values come only from the oracle.
 import numpy as np
 
 from synth.buffers import DeviceInputs, HostInputs, gather_f32, gather_u16, to_u16  # noqa: F401
+from synth import host_fill
 from synth.workloads import Workload
 
 TOL_F32_REL = 2e-6      # max relative error on fp32 master, m, v
@@ -42,30 +43,54 @@ def compact_layout(w: Workload, idx, full_segments=()):
 
 
 def oracle_round(orc, w: Workload, host: HostInputs, seg_off=None, seg_decay=None,
-                 want_sumsq=False):
+                 want_sumsq=False, clip_totals=None):
     """Run the oracle round (FL+FSDP, or FL+HSDP when w.H > 1) in place on host
-    arrays.  Returns the per-step per-segment sums of squares or None."""
+    arrays.  Returns the per-step per-segment sums of squares or None.
+    clip_totals: per-step whole-shard sums of squares to clip against when the
+    host arrays hold only a sample of the shard."""
     seg_off = w.seg_offsets if seg_off is None else seg_off
     seg_decay = w.seg_decay if seg_decay is None else seg_decay
     if w.outer is not None:
         return orc.round_outer(seg_off, seg_decay, w.R, w.G, w.A, w.self_group, w.grad_scale,
                                w.hp, w.step0, w.weights, w.outer, host.grads, host.replicas,
                                host.prev, host.buf, host.master, host.m, host.v, host.working,
-                               want_sumsq=want_sumsq)
+                               want_sumsq=want_sumsq, max_grad_norm=w.max_grad_norm,
+                               clip_totals=clip_totals)
     if w.H > 1:
         return orc.round_hsdp(seg_off, seg_decay, w.R, w.H, w.replica, 1.0 / w.H, w.hsdp_member,
                               w.G, w.A, w.self_group, w.grad_scale, w.hp, w.step0, w.weights,
                               host.grads, host.replica_wires, host.replicas, host.bcast,
-                              host.master, host.m, host.v, host.working, want_sumsq=want_sumsq)
+                              host.master, host.m, host.v, host.working, want_sumsq=want_sumsq,
+                              max_grad_norm=w.max_grad_norm, clip_totals=clip_totals)
     return orc.round(seg_off, seg_decay, w.R, w.G, w.A, w.self_group, w.grad_scale, w.hp,
                      w.step0, w.weights, host.grads, host.replicas, host.master, host.m, host.v,
-                     host.working, want_sumsq=want_sumsq)
+                     host.working, want_sumsq=want_sumsq, max_grad_norm=w.max_grad_norm,
+                     clip_totals=clip_totals)
+
+
+def clip_totals(orc, w: Workload, chunk=1 << 24, say=None):
+    """Whole-shard sum of squares of each local step's reduced gradient, in
+    index order, one chunk of host-regenerated peer gradients at a time (for a
+    clipped round whose oracle sees only a sample of the shard)."""
+    assert w.H == 1, "the FL+HSDP clip norm is that of the replica average"
+    steps = [tuple(w.grad_index[a * w.R:(a + 1) * w.R]) for a in range(w.A)]
+    done = {}
+    for key in dict.fromkeys(steps):
+        acc = 0.0
+        for c, lo in enumerate(range(0, w.n, chunk)):
+            k = min(chunk, w.n - lo)
+            acc = orc.grad_total([host_fill(w.grad_specs[j], lo, k) for j in key],
+                                 w.grad_scale, acc)
+            if say is not None and c % 16 == 15:
+                say("clip total: %d of %d elements" % (lo + k, w.n))
+        done[key] = acc
+    return [done[key] for key in steps]
 
 
 def round_cfg(P, w: Workload, step0=None, phase_events=None):
     return P.make_round_cfg(w.R, w.G, w.A, w.weights, w.hp, self_group=w.self_group,
                             grad_scale=w.grad_scale, step0=w.step0 if step0 is None else step0,
-                            phase_events=phase_events)
+                            phase_events=phase_events, max_grad_norm=w.max_grad_norm)
 
 
 def gpu_round(P, layout, w: Workload, dev: DeviceInputs, seg_sumsq=None, phase_events=None,

@@ -3,7 +3,9 @@ benchmark uses: one fl_round on the whole shard, then the oracle on sampled
 elements (every segment's first and last two elements, the tail, all of a few
 short segments, and uniform random draws), plus properties that hold at any
 size.  Sampled inputs are regenerated on the host by the same counter-based
-generator; expected values come only from the oracle."""
+generator; expected values come only from the oracle.  A clipped workload's
+coefficient depends on the whole shard, so the oracle first streams each
+step's whole-shard sum of squares over host-regenerated chunks."""
 import numpy as np
 import pytest
 
@@ -14,7 +16,7 @@ from synth import workloads as W
 pytestmark = pytest.mark.gpu
 
 WORKLOADS = ["llama8b_s8", "fedavg_heavy", "hsdp_s4", "stress", "hsdp_s4_h2", "hsdp_s4_h2_recv",
-             "llama8b_s8_outer"]
+             "llama8b_s8_outer", "llama8b_s8_clip"]
 
 
 def _say(*a):
@@ -64,9 +66,13 @@ def test_full_size_round_sampled(env, name):
     del dev
     torch.cuda.empty_cache()
 
+    totals = H.clip_totals(orc, w, say=lambda m: _say(name, m)) if w.max_grad_norm > 0 else None
+    if totals is not None:
+        _say(name, "clip coefficients", [orc.clip_coef(t, w.max_grad_norm) for t in totals[:1]])
     host = B.HostInputs(w, idx)
     off, dec, cmap = H.compact_layout(w, idx, full)
-    ss_ref = H.oracle_round(orc, w, host, seg_off=off, seg_decay=dec, want_sumsq=True)
+    ss_ref = H.oracle_round(orc, w, host, seg_off=off, seg_decay=dec, want_sumsq=True,
+                            clip_totals=totals)
     ref = dict(master=host.master, m=host.m, v=host.v, working=host.working)
     errs = H.assert_state_parity(name, got, ref, bitwise=True)
     if w.outer is not None:
