@@ -38,8 +38,22 @@ def env():
 
 @pytest.mark.parametrize("name", WORKLOADS)
 def test_full_size_round_sampled(env, name):
+    _sampled_parity(env, W.ALL[name](), name)
+
+
+def test_beyond_int32_element_indices(env):
+    """2^31 + 2053 elements: indices past the int32 range, a segment boundary
+    3 elements past 2^31 (inside a tile), a 5-element ragged tail, and a
+    short segment that straddles 2^31 itself."""
+    n = (1 << 31) + 2053
+    cuts = [0, 1 << 30, (1 << 31) - 700, (1 << 31) + 3, n]
+    w = W.make_workload("beyond_int32", np.diff(cuts), [1, 0, 1, 1], R=2, G=2, A=1, step0=3,
+                        weights=np.array([1.0, 3.0], np.float32))
+    _sampled_parity(env, w, "beyond_int32")
+
+
+def _sampled_parity(env, w, name):
     torch, P, orc = env["torch"], env["P"], env["orc"]
-    w = W.ALL[name]()
     _say(name, w.describe())
     lay = P.Layout(w.seg_offsets, w.seg_decay)
     dev = B.DeviceInputs(w)
