@@ -136,6 +136,28 @@ def summarize_trace(stats_csv, cmd, workload="llama8b_s8"):
     return "\n".join(lines)
 
 
+PROBE_FILE = os.path.join(ROOT, "profiles", "hbm_ceiling_probe.md")
+
+
+def probe_ceiling(w, achieved):
+    """The attainable rate of the local step's access pattern with no
+    arithmetic, from the committed ceiling-probe summary, where the probe
+    measured this workload's pattern (R = 8 peers, one replica, no clipping);
+    else None."""
+    if not (w.R == 8 and w.H == 1 and w.max_grad_norm <= 0) or not os.path.exists(PROBE_FILE):
+        return None
+    best = None
+    for line in open(PROBE_FILE):
+        cells = [c.strip() for c in line.strip().strip("|").split("|")]
+        if len(cells) >= 7 and cells[0] == "step_R8":
+            val = float(cells[6].split()[0])
+            best = val if best is None else max(best, val)
+    if best is None:
+        return None
+    return {"pattern": "step_R8 (11 read streams, 4 written; no arithmetic)", "gbs": best,
+            "frac": round(achieved / best, 4)}
+
+
 def step_label(w):
     """The kernels of one local step, as the roofline figure counts them."""
     fused = "k_step<%s=%d, fused, %s>" % ("R" if w.H == 1 else "H", w.R if w.H == 1 else w.H,
@@ -272,6 +294,9 @@ def main():
     wall = time.perf_counter() - t_wall
     total_ms = start.elapsed_time(stop)
     ms_round = total_ms / K
+    round_ms = sorted(events[k].elapsed_ms(0, w.A + 1) for k in range(K))
+    mid = K // 2
+    median_ms = round_ms[mid] if K % 2 else 0.5 * (round_ms[mid - 1] + round_ms[mid])
     step_ms = [events[k].elapsed_ms(a, a + 1) for k in range(K) for a in range(w.A)]
     fed_ms = [events[k].elapsed_ms(w.A, w.A + 1) for k in range(K)]
     avg_step = sum(step_ms) / len(step_ms)
@@ -306,6 +331,8 @@ def main():
         "params_per_s": round(w.n / (ms_round * 1e-3), 1),
         "phases_ms": dict(local_step=round(avg_step, 4), fedavg=round(avg_fed, 4),
                           fedavg_gbs=round(fed_bytes / (avg_fed * 1e-3) / 1e9, 2)),
+        "round_ms": dict(median=round(median_ms, 4),
+                         min=round(round_ms[0], 4), max=round(round_ms[-1], 4)),
         "roofline": {
             "bound": "hbm",
             "kernel": step_label(w),
@@ -316,6 +343,7 @@ def main():
             "traffic": traffic,
             "algorithmic_bytes": step_bytes,
             "kernel_source_hash": src_hash,
+            "probe_ceiling": probe_ceiling(w, achieved),
         },
     }
     del dev

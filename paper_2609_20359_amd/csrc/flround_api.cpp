@@ -7,6 +7,7 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <atomic>
 #include <cmath>
 #include <cstdint>
 #include <cstdlib>
@@ -29,7 +30,7 @@ struct fl_layout {
 
 namespace {
 
-int g_blocks_per_cu = 0;  // 0: the per-pass defaults below
+std::atomic<int> g_blocks_per_cu{0};  // 0: the per-pass defaults below
 
 // Default workgroups per CU.  One 256-thread workgroup per CU keeps enough
 // 16-byte loads in flight for the passes that stream many arrays (the fused
@@ -154,7 +155,8 @@ int check_device(const fl_layout* lay) {
 }
 
 int grid_for(const fl_layout* lay, int64_t units, int default_bpc = kDefaultBlocksPerCu) {
-  const int bpc = g_blocks_per_cu > 0 ? g_blocks_per_cu : default_bpc;
+  const int set = g_blocks_per_cu.load(std::memory_order_relaxed);
+  const int bpc = set > 0 ? set : default_bpc;
   int64_t cap = (int64_t)bpc * (int64_t)lay->num_cus;
   if (cap < 1) cap = 1;
   int64_t g = units < cap ? units : cap;
@@ -324,9 +326,7 @@ float fl_lr_cosine(int64_t t, int64_t total_steps, int64_t warmup_steps, float l
 }
 
 int fl_set_blocks_per_cu(int blocks_per_cu) {
-  const int prev = g_blocks_per_cu;
-  g_blocks_per_cu = blocks_per_cu > 0 ? blocks_per_cu : 0;
-  return prev;
+  return g_blocks_per_cu.exchange(blocks_per_cu > 0 ? blocks_per_cu : 0);
 }
 
 uint64_t fl_fingerprint(int64_t n, int64_t n_seg, const int64_t* seg_offsets,
