@@ -136,25 +136,31 @@ def summarize_trace(stats_csv, cmd, workload="llama8b_s8"):
     return "\n".join(lines)
 
 
-PROBE_FILE = os.path.join(ROOT, "profiles", "hbm_ceiling_probe.md")
+PROBE_FILES = {1003782144: os.path.join(ROOT, "profiles", "hbm_ceiling_probe_llama31_8b_s8.md"),
+               2007564288: os.path.join(ROOT, "profiles", "hbm_ceiling_probe_llama31_8b_s4.md")}
 
 
 def probe_ceiling(w, achieved):
     """The attainable rate of the local step's access pattern with no
-    arithmetic, from the committed ceiling-probe summary, where the probe
-    measured this workload's pattern (R = 8 peers, one replica, no clipping);
-    else None."""
-    if not (w.R == 8 and w.H == 1 and w.max_grad_norm <= 0) or not os.path.exists(PROBE_FILE):
+    arithmetic, from the committed ceiling-probe summary for this shard
+    length, where the probe measured the pattern (a plain fused step: one
+    replica, no clipping); else None."""
+    path = PROBE_FILES.get(w.n)
+    pattern = "step_R%d" % w.R
+    if not (w.H == 1 and w.max_grad_norm <= 0) or path is None or not os.path.exists(path):
         return None
     best = None
-    for line in open(PROBE_FILE):
+    for line in open(path):
         cells = [c.strip() for c in line.strip().strip("|").split("|")]
-        if len(cells) >= 7 and cells[0] == "step_R8":
-            val = float(cells[6].split()[0])
-            best = val if best is None else max(best, val)
+        if cells and cells[0] == pattern:
+            for c in cells:
+                if c.endswith("/CU)"):
+                    val = float(c.split()[0])
+                    best = val if best is None else max(best, val)
     if best is None:
         return None
-    return {"pattern": "step_R8 (11 read streams, 4 written; no arithmetic)", "gbs": best,
+    return {"pattern": "%s (%d bf16 streams read, 3 fp32 read and written, 1 bf16 written; "
+                       "no arithmetic)" % (pattern, w.R), "gbs": best,
             "frac": round(achieved / best, 4)}
 
 

@@ -10,12 +10,22 @@
 //   copy       1 read, 1 written
 //   step_R8    8 bf16 streams read, 3 fp32 streams read and written, 1 bf16
 //              stream written: the traffic of one fused local step (R = 8)
+//   step_R4, step_R2  the same with 4 and 2 peer streams (R = 4; the FL+HSDP
+//              second tier averages H = 2 bf16 wire shards, the R = 2 pattern)
+//   sumsq_R8, sumsq_R4  8 or 4 bf16 streams read, nothing written: the
+//              sum-of-squares pass before a clipped step
+//   wire_R4    4 bf16 streams read, 1 bf16 stream written: the FL+HSDP
+//              first-tier reduction to the wire format
 //   fedavg_G4  4 bf16 streams read, 1 fp32 and 1 bf16 stream written
+//   fedopt_G4  as fedavg_G4 plus 2 fp32 streams read and written (the outer
+//              step's round-start model and momentum buffer)
 //   step_R8_tiled  as step_R8, but the three fp32 state arrays interleaved per
 //              2048-element tile ([tile][master | m | v]), i.e. one 24 KB
 //              read-modify-write chunk per tile instead of three streams
-// each with plain and nontemporal stores, for 1..8 workgroups per CU.
-// Buffers are sized for the 1,003,782,144-element shard.
+// each with plain and nontemporal stores, for 1, 2, 3, 4 and 8 workgroups per CU.
+// Buffers are sized for the given element count (default: the
+// 1,003,782,144-element shard of Llama-3.1-8B at S = 8; the S = 4 shard has
+// 2,007,564,288 elements and needs about 120 GB).
 //
 // usage: hbm_probe [elements]
 #include <hip/hip_runtime.h>
@@ -78,7 +88,7 @@ void run_tiled(Streams s, int cus, long elems) {
     double best = 0.0;
     int best_bpc = 0;
     std::printf("| %-9s | %-5s |", "step_R8_tiled", nts ? "nt" : "plain");
-    for (int bpc : {1, 2, 4, 8}) {
+    for (int bpc : {1, 2, 3, 4, 8}) {
       const int grid = bpc * cus;
       float ms = nts ? time_ms([&] { k_step_tiled<true><<<grid, 256>>>(s); }, 5)
                      : time_ms([&] { k_step_tiled<false><<<grid, 256>>>(s); }, 5);
@@ -165,7 +175,7 @@ void run(const char* name, Streams s, int cus, long elems) {
     double best = 0.0;
     int best_bpc = 0;
     std::printf("| %-9s | %-5s |", name, nts ? "nt" : "plain");
-    for (int bpc : {1, 2, 4, 8}) {
+    for (int bpc : {1, 2, 3, 4, 8}) {
       const int grid = bpc * cus;
       float ms = nts ? time_ms([&] { k_pattern<NRD, NRMW, NWH, NWF, true><<<grid, 256>>>(s); }, 5)
                      : time_ms([&] { k_pattern<NRD, NRMW, NWH, NWF, false><<<grid, 256>>>(s); }, 5);
@@ -206,13 +216,19 @@ int main(int argc, char** argv) {
   std::printf("# HBM ceiling probe: %s, %d CUs, %ld-element streams\n\n", prop.gcnArchName, cus,
               elems);
   std::printf("GB/s by workgroups per CU; bytes = bytes the pattern moves; peak 8000 GB/s.\n\n");
-  std::printf("| pattern | stores | 1/CU | 2/CU | 4/CU | 8/CU | best | of peak |\n");
-  std::printf("|---|---|---|---|---|---|---|---|\n");
+  std::printf("| pattern | stores | 1/CU | 2/CU | 3/CU | 4/CU | 8/CU | best | of peak |\n");
+  std::printf("|---|---|---|---|---|---|---|---|---|\n");
   run<1, 0, 0, 0>("read1", s, cus, elems);
   run<0, 0, 1, 0>("write1", s, cus, elems);
   run<1, 0, 1, 0>("copy", s, cus, elems);
   run<8, 3, 1, 0>("step_R8", s, cus, elems);
+  run<4, 3, 1, 0>("step_R4", s, cus, elems);
+  run<2, 3, 1, 0>("step_R2", s, cus, elems);
+  run<8, 0, 0, 0>("sumsq_R8", s, cus, elems);
+  run<4, 0, 0, 0>("sumsq_R4", s, cus, elems);
+  run<4, 0, 1, 0>("wire_R4", s, cus, elems);
   run<4, 0, 1, 1>("fedavg_G4", s, cus, elems);
+  run<4, 2, 1, 1>("fedopt_G4", s, cus, elems);
   run_tiled(s, cus, elems);
   for (void* p : bufs) CK(hipFree(p));
   return 0;
