@@ -134,19 +134,53 @@ def _check(rc, where):
         raise FlError(rc, where)
 
 
-def _ptr(t):
-    """Device address of a tensor, or 0 for None."""
+_MAX_LIST = 1 << 20
+
+
+def _buf(t, n, esize, what):
+    """Device address of a tensor argument, after checking on the host what
+    the kernels assume of it: a contiguous CUDA tensor of exactly n elements
+    of esize bytes.  None gives NULL (the library decides whether that is
+    allowed); an int is taken as a raw device address."""
     if t is None:
         return None
     if isinstance(t, int):
         return t
+    if not getattr(t, "is_cuda", False):
+        raise ValueError("%s must be a CUDA tensor" % what)
     if not t.is_contiguous():
-        raise ValueError("tensors passed to libflround must be contiguous")
+        raise ValueError("%s must be contiguous" % what)
+    if t.element_size() != esize:
+        raise ValueError("%s has %d-byte elements; expected %d" % (what, t.element_size(), esize))
+    if t.numel() != n:
+        raise ValueError("%s has %d elements; expected %d" % (what, t.numel(), n))
     return t.data_ptr()
 
 
-def _ptr_array(ts):
-    return (ctypes.c_void_p * len(ts))(*[_ptr(t) for t in ts])
+def _bufs(ts, count, n, esize, what):
+    """Host array of the device addresses of `count` tensors (each checked as
+    in _buf).  A shorter list is padded with NULL, which the library rejects
+    with FL_ERR_INVALID; a longer one is an error.  When `count` is outside
+    what any call accepts, the list is passed as given for the library to
+    reject the configuration."""
+    ts = list(ts)
+    if 1 <= count <= _MAX_LIST:
+        if len(ts) > count:
+            raise ValueError("%s has %d entries; expected %d" % (what, len(ts), count))
+        size = count
+    else:
+        size = max(len(ts), 1)
+    arr = (ctypes.c_void_p * size)()
+    for i, t in enumerate(ts):
+        arr[i] = _buf(t, n, esize, "%s[%d]" % (what, i))
+    return arr
+
+
+def _host_list(xs, count, ctype, what):
+    xs = list(xs)
+    if len(xs) != count:
+        raise ValueError("%s has %d entries; expected %d" % (what, len(xs), count))
+    return (ctype * max(count, 1))(*xs)
 
 
 def _stream(stream):
@@ -211,43 +245,56 @@ class Layout:
 
 
 def fl_shard_reduce(layout, peer_grads, grad_scale, grad_out, seg_sumsq=None, stream=None):
-    rc = lib().fl_shard_reduce(layout.handle, len(peer_grads), _ptr_array(peer_grads),
-                               float(grad_scale), _ptr(grad_out), _ptr(seg_sumsq), _stream(stream))
+    n, R = layout.n, len(peer_grads)
+    rc = lib().fl_shard_reduce(layout.handle, R, _bufs(peer_grads, R, n, 2, "peer_grads"),
+                               float(grad_scale), _buf(grad_out, n, 4, "grad_out"),
+                               _buf(seg_sumsq, layout.n_seg, 4, "seg_sumsq"), _stream(stream))
     _check(rc, "fl_shard_reduce")
 
 
 def fl_adamw_step(layout, hp, step, grad, master, m, v, working=None, stream=None):
     h = hparams(hp)
-    rc = lib().fl_adamw_step(layout.handle, ctypes.byref(h), int(step), _ptr(grad), _ptr(master),
-                             _ptr(m), _ptr(v), _ptr(working), _stream(stream))
+    n = layout.n
+    rc = lib().fl_adamw_step(layout.handle, ctypes.byref(h), int(step), _buf(grad, n, 4, "grad"),
+                             _buf(master, n, 4, "master"), _buf(m, n, 4, "m"),
+                             _buf(v, n, 4, "v"), _buf(working, n, 2, "working"), _stream(stream))
     _check(rc, "fl_adamw_step")
 
 
 def fl_local_step(layout, hp, step, peer_grads, grad_scale, master, m, v, working,
                   seg_sumsq=None, stream=None):
     h = hparams(hp)
-    rc = lib().fl_local_step(layout.handle, ctypes.byref(h), int(step), len(peer_grads),
-                             _ptr_array(peer_grads), float(grad_scale), _ptr(master), _ptr(m),
-                             _ptr(v), _ptr(working), _ptr(seg_sumsq), _stream(stream))
+    n, R = layout.n, len(peer_grads)
+    rc = lib().fl_local_step(layout.handle, ctypes.byref(h), int(step), R,
+                             _bufs(peer_grads, R, n, 2, "peer_grads"), float(grad_scale),
+                             _buf(master, n, 4, "master"), _buf(m, n, 4, "m"), _buf(v, n, 4, "v"),
+                             _buf(working, n, 2, "working"),
+                             _buf(seg_sumsq, layout.n_seg, 4, "seg_sumsq"), _stream(stream))
     _check(rc, "fl_local_step")
 
 
 def fl_fedavg(layout, replicas, weights, master_out, working_out, replica_fp=None, stream=None):
-    G = len(replicas)
-    w = (ctypes.c_float * G)(*[float(x) for x in weights])
-    fp = None if replica_fp is None else (ctypes.c_uint64 * G)(*[int(x) for x in replica_fp])
-    rc = lib().fl_fedavg(layout.handle, G, _ptr_array(replicas), w, fp, _ptr(master_out),
-                         _ptr(working_out), _stream(stream))
+    n, G = layout.n, len(replicas)
+    w = _host_list([float(x) for x in weights], G, ctypes.c_float, "weights")
+    fp = None if replica_fp is None else _host_list([int(x) for x in replica_fp], G,
+                                                    ctypes.c_uint64, "replica_fp")
+    rc = lib().fl_fedavg(layout.handle, G, _bufs(replicas, G, n, 2, "replicas"), w, fp,
+                         _buf(master_out, n, 4, "master_out"),
+                         _buf(working_out, n, 2, "working_out"), _stream(stream))
     _check(rc, "fl_fedavg")
 
 
 def make_round_cfg(R, G, A, weights, hp, *, self_group=0, grad_scale=None, step0=1,
                    replica_fp=None, phase_events=None, step_lr=None, max_grad_norm=0.0):
-    """Build an fl_round_cfg; the returned object keeps its arrays alive."""
-    w = (ctypes.c_float * G)(*[float(x) for x in weights])
-    fp = None if replica_fp is None else (ctypes.c_uint64 * G)(*[int(x) for x in replica_fp])
-    ev = None if phase_events is None else (ctypes.c_void_p * len(phase_events))(*phase_events)
-    lrs = None if step_lr is None else (ctypes.c_float * len(step_lr))(*[float(x) for x in step_lr])
+    """Build an fl_round_cfg; the returned object keeps its arrays alive.
+    weights and replica_fp have G entries, step_lr A, phase_events A + 2."""
+    w = _host_list([float(x) for x in weights], G, ctypes.c_float, "weights")
+    fp = None if replica_fp is None else _host_list([int(x) for x in replica_fp], G,
+                                                    ctypes.c_uint64, "replica_fp")
+    ev = None if phase_events is None else _host_list(phase_events, A + 2, ctypes.c_void_p,
+                                                      "phase_events")
+    lrs = None if step_lr is None else _host_list([float(x) for x in step_lr], A, ctypes.c_float,
+                                                  "step_lr")
     cfg = RoundCfg(R, G, A, self_group, float(1.0 / R if grad_scale is None else grad_scale),
                    hparams(hp), int(step0), w, fp, ev, lrs, float(max_grad_norm))
     cfg._keep = (w, fp, ev, lrs)
@@ -263,20 +310,27 @@ def lr_cosine(t, total_steps, warmup_steps, lr_max, lr_min=0.0):
 def fl_round(layout, cfg, grads, replicas, master, m, v, working, seg_sumsq=None, stream=None):
     """grads: A*R tensors (step-major); replicas: G tensors or None (entry
     self_group is ignored)."""
-    rc = lib().fl_round(layout.handle, ctypes.byref(cfg), _ptr_array(grads),
-                        _ptr_array(replicas), _ptr(master), _ptr(m), _ptr(v), _ptr(working),
-                        _ptr(seg_sumsq), _stream(stream))
+    n = layout.n
+    rc = lib().fl_round(layout.handle, ctypes.byref(cfg),
+                        _bufs(grads, cfg.A * cfg.R, n, 2, "grads"),
+                        _bufs(replicas, cfg.G, n, 2, "replicas"), _buf(master, n, 4, "master"),
+                        _buf(m, n, 4, "m"), _buf(v, n, 4, "v"), _buf(working, n, 2, "working"),
+                        _buf(seg_sumsq, cfg.A * layout.n_seg, 4, "seg_sumsq"), _stream(stream))
     _check(rc, "fl_round")
 
 
 def fl_shard_reduce_wire(layout, peer_grads, grad_scale, wire_out, stream=None):
-    rc = lib().fl_shard_reduce_wire(layout.handle, len(peer_grads), _ptr_array(peer_grads),
-                                    float(grad_scale), _ptr(wire_out), _stream(stream))
+    n, R = layout.n, len(peer_grads)
+    rc = lib().fl_shard_reduce_wire(layout.handle, R, _bufs(peer_grads, R, n, 2, "peer_grads"),
+                                    float(grad_scale), _buf(wire_out, n, 2, "wire_out"),
+                                    _stream(stream))
     _check(rc, "fl_shard_reduce_wire")
 
 
 def fl_broadcast_recv(layout, recv_master, master, working, stream=None):
-    rc = lib().fl_broadcast_recv(layout.handle, _ptr(recv_master), _ptr(master), _ptr(working),
+    n = layout.n
+    rc = lib().fl_broadcast_recv(layout.handle, _buf(recv_master, n, 4, "recv_master"),
+                                 _buf(master, n, 4, "master"), _buf(working, n, 2, "working"),
                                  _stream(stream))
     _check(rc, "fl_broadcast_recv")
 
@@ -292,50 +346,67 @@ def fl_round_hsdp(layout, cfg, hcfg, grads, replica_wires, wire, replicas, bcast
     a*H + replica ignored), or None when H == 1; wire: bf16 scratch (H > 1);
     replicas: G tensors/None (FedAvg member) or None; bcast_master: fp32
     tensor (non-member) or None."""
-    rc = lib().fl_round_hsdp(layout.handle, ctypes.byref(cfg), ctypes.byref(hcfg),
-                             _ptr_array(grads),
-                             None if replica_wires is None else _ptr_array(replica_wires),
-                             _ptr(wire), None if replicas is None else _ptr_array(replicas),
-                             _ptr(bcast_master), _ptr(master), _ptr(m), _ptr(v), _ptr(working),
-                             _ptr(seg_sumsq), _stream(stream))
+    n = layout.n
+    rc = lib().fl_round_hsdp(
+        layout.handle, ctypes.byref(cfg), ctypes.byref(hcfg),
+        _bufs(grads, cfg.A * cfg.R, n, 2, "grads"),
+        None if replica_wires is None else _bufs(replica_wires, cfg.A * hcfg.H, n, 2,
+                                                 "replica_wires"),
+        _buf(wire, n, 2, "wire"),
+        None if replicas is None else _bufs(replicas, cfg.G, n, 2, "replicas"),
+        _buf(bcast_master, n, 4, "bcast_master"), _buf(master, n, 4, "master"),
+        _buf(m, n, 4, "m"), _buf(v, n, 4, "v"), _buf(working, n, 2, "working"),
+        _buf(seg_sumsq, cfg.A * layout.n_seg, 4, "seg_sumsq"), _stream(stream))
     _check(rc, "fl_round_hsdp")
 
 
 def fl_grad_sumsq(layout, peer_grads, grad_scale, total_sumsq, seg_sumsq=None, stream=None):
     """total_sumsq: a CUDA float64 tensor of one element."""
-    rc = lib().fl_grad_sumsq(layout.handle, len(peer_grads), _ptr_array(peer_grads),
-                             float(grad_scale), _ptr(total_sumsq), _ptr(seg_sumsq), _stream(stream))
+    n, R = layout.n, len(peer_grads)
+    rc = lib().fl_grad_sumsq(layout.handle, R, _bufs(peer_grads, R, n, 2, "peer_grads"),
+                             float(grad_scale), _buf(total_sumsq, 1, 8, "total_sumsq"),
+                             _buf(seg_sumsq, layout.n_seg, 4, "seg_sumsq"), _stream(stream))
     _check(rc, "fl_grad_sumsq")
 
 
 def fl_local_step_clipped(layout, hp, step, peer_grads, grad_scale, total_sumsq, max_norm, master,
                           m, v, working, stream=None):
     h = hparams(hp)
-    rc = lib().fl_local_step_clipped(layout.handle, ctypes.byref(h), int(step), len(peer_grads),
-                                     _ptr_array(peer_grads), float(grad_scale), _ptr(total_sumsq),
-                                     float(max_norm), _ptr(master), _ptr(m), _ptr(v),
-                                     _ptr(working), _stream(stream))
+    n, R = layout.n, len(peer_grads)
+    rc = lib().fl_local_step_clipped(layout.handle, ctypes.byref(h), int(step), R,
+                                     _bufs(peer_grads, R, n, 2, "peer_grads"), float(grad_scale),
+                                     _buf(total_sumsq, 1, 8, "total_sumsq"), float(max_norm),
+                                     _buf(master, n, 4, "master"), _buf(m, n, 4, "m"),
+                                     _buf(v, n, 4, "v"), _buf(working, n, 2, "working"),
+                                     _stream(stream))
     _check(rc, "fl_local_step_clipped")
 
 
 def fl_fedopt(layout, replicas, weights, outer, prev, buf, master_out, working_out,
               replica_fp=None, stream=None):
-    G = len(replicas)
-    w = (ctypes.c_float * G)(*[float(x) for x in weights])
-    fp = None if replica_fp is None else (ctypes.c_uint64 * G)(*[int(x) for x in replica_fp])
+    n, G = layout.n, len(replicas)
+    w = _host_list([float(x) for x in weights], G, ctypes.c_float, "weights")
+    fp = None if replica_fp is None else _host_list([int(x) for x in replica_fp], G,
+                                                    ctypes.c_uint64, "replica_fp")
     o = outer_hparams(outer)
-    rc = lib().fl_fedopt(layout.handle, G, _ptr_array(replicas), w, fp, ctypes.byref(o),
-                         _ptr(prev), _ptr(buf), _ptr(master_out), _ptr(working_out),
-                         _stream(stream))
+    rc = lib().fl_fedopt(layout.handle, G, _bufs(replicas, G, n, 2, "replicas"), w, fp,
+                         ctypes.byref(o), _buf(prev, n, 4, "prev"), _buf(buf, n, 4, "buf"),
+                         _buf(master_out, n, 4, "master_out"),
+                         _buf(working_out, n, 2, "working_out"), _stream(stream))
     _check(rc, "fl_fedopt")
 
 
 def fl_round_outer(layout, cfg, outer, grads, replicas, prev, buf, master, m, v, working,
                    seg_sumsq=None, stream=None):
     o = outer_hparams(outer)
+    n = layout.n
     rc = lib().fl_round_outer(layout.handle, ctypes.byref(cfg), ctypes.byref(o),
-                              _ptr_array(grads), _ptr_array(replicas), _ptr(prev), _ptr(buf),
-                              _ptr(master), _ptr(m), _ptr(v), _ptr(working), _ptr(seg_sumsq),
+                              _bufs(grads, cfg.A * cfg.R, n, 2, "grads"),
+                              _bufs(replicas, cfg.G, n, 2, "replicas"), _buf(prev, n, 4, "prev"),
+                              _buf(buf, n, 4, "buf"), _buf(master, n, 4, "master"),
+                              _buf(m, n, 4, "m"), _buf(v, n, 4, "v"),
+                              _buf(working, n, 2, "working"),
+                              _buf(seg_sumsq, cfg.A * layout.n_seg, 4, "seg_sumsq"),
                               _stream(stream))
     _check(rc, "fl_round_outer")
 

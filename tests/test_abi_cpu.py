@@ -114,3 +114,32 @@ def test_lr_cosine_matches_the_oracle_and_transformers():
             assert lib_lr == np.float32(opt.param_groups[0]["lr"])
             opt.step()
             sch.step()
+
+
+def test_binding_checks_host_lists_and_tensors_without_a_gpu():
+    """The binding checks every list length and tensor on the host before it
+    calls the library, so a mismatch never reaches a kernel."""
+    import pytest
+    import torch
+
+    hp = dict(lr=3e-4, beta1=0.9, beta2=0.95, eps=1e-8, weight_decay=0.1)
+    with pytest.raises(ValueError):
+        F.make_round_cfg(2, 3, 1, [1.0, 1.0], hp)                     # G weights
+    with pytest.raises(ValueError):
+        F.make_round_cfg(2, 2, 3, [1.0, 1.0], hp, step_lr=[1e-3, 1e-3])
+    with pytest.raises(ValueError):
+        F.make_round_cfg(2, 2, 1, [1.0, 1.0], hp, replica_fp=[1])
+    with pytest.raises(ValueError):
+        F.make_round_cfg(2, 2, 1, [1.0, 1.0], hp, phase_events=[0, 0])  # needs A + 2
+
+    class FakeLayout:  # a layout needs a GPU; the checks below come first
+        handle, n, n_seg = None, 16, 1
+
+    cfg = F.make_round_cfg(2, 2, 1, [1.0, 1.0], hp)
+    cpu = torch.zeros(16, dtype=torch.bfloat16)
+    with pytest.raises(ValueError, match="CUDA"):
+        F.fl_round(FakeLayout, cfg, [cpu, cpu], [None, cpu], None, None, None, None)
+    with pytest.raises(ValueError, match="entries"):
+        F.fl_round(FakeLayout, cfg, [None] * 3, [None, None], None, None, None, None)
+    with pytest.raises(ValueError, match="entries"):
+        F.fl_fedavg(FakeLayout, [None, None], [1.0], None, None)

@@ -177,3 +177,37 @@ def test_round_with_scheduled_learning_rates(env):
     with pytest.raises(P.FlError):
         H.gpu_round(P, lay, w, dev, cfg=bad)
     lay.close()
+
+
+def test_binding_rejects_mismatched_tensors(env):
+    """Tensors of the wrong length or element size, and lists of the wrong
+    length, are refused on the host before anything is enqueued; a list
+    shorter than the configuration asks for reaches the library as NULL
+    entries, which it rejects."""
+    torch, P = env["torch"], env["P"]
+    n = 4099
+    lay = P.Layout(np.array([0, 1000, n], np.int64), np.array([1, 0], np.uint8))
+    f32 = lambda k=n: torch.zeros(k, dtype=torch.float32, device="cuda")  # noqa: E731
+    bf = lambda k=n: torch.zeros(k, dtype=torch.bfloat16, device="cuda")  # noqa: E731
+    master, m, v, work = f32(), f32(), f32(), bf()
+    keep = master.clone()
+    grads = [bf(), bf()]
+    cfg = P.make_round_cfg(2, 2, 1, [1.0, 1.0], W.ADAMW)
+    run = lambda **k: P.fl_round(lay, cfg, k.get("g", grads), k.get("r", [None, bf()]),  # noqa: E731
+                                 k.get("p", master), m, v, work, seg_sumsq=k.get("ss"))
+    with pytest.raises(ValueError, match="elements"):
+        run(p=f32(n - 1))
+    with pytest.raises(ValueError, match="byte elements"):
+        run(g=[grads[0], f32()])
+    with pytest.raises(ValueError, match="entries"):
+        run(g=grads + [bf()])
+    with pytest.raises(ValueError, match="elements"):
+        run(ss=f32(lay.n_seg + 1))
+    with pytest.raises(ValueError, match="contiguous"):
+        run(p=torch.zeros(2 * n, device="cuda")[::2])
+    with pytest.raises(P.FlError) as e:
+        run(g=grads[:1])
+    assert e.value.status == -1
+    torch.cuda.synchronize()
+    assert torch.equal(master, keep), "a refused call changed the state"
+    lay.close()
