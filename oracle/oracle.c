@@ -63,7 +63,8 @@ double orc_total_sumsq(int64_t n, const float* g) {
 
 float orc_clip_coef(double total_sumsq, float max_norm) {
   const double c = (double)max_norm / (sqrt(total_sumsq) + 1e-6);
-  return (float)(c < 1.0 ? c : 1.0);
+  /* min(1, c) as torch's clamp takes it: a NaN norm gives a NaN coefficient */
+  return (float)(c >= 1.0 ? 1.0 : c);
 }
 
 double orc_grad_total(int64_t n, int R, const uint16_t* const* grads, float grad_scale,

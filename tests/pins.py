@@ -936,6 +936,23 @@ def pin_clip_vs_torch(orc):
         _check_close("clipped g", clipped, t.grad.numpy(), 4 * U * np.abs(t.grad.numpy()) + TINY)
 
 
+def pin_clip_nonfinite_norm_vs_torch(orc):
+    """A NaN or infinite gradient norm: the coefficient and the clipped
+    gradient are torch.nn.utils.clip_grad_norm_'s (NaN everywhere for a NaN
+    norm; zero, and NaN at an infinite entry, for an infinite norm)."""
+    for bad in (np.nan, np.inf):
+        g = np.array([1e-3, -2e-3, bad, 4e-3], np.float32)
+        t = torch.nn.Parameter(torch.zeros(g.size, dtype=torch.float64))
+        t.grad = torch.tensor(g.astype(np.float64))
+        torch.nn.utils.clip_grad_norm_([t], 1.0)
+        coef = orc.clip_coef(orc.total_sumsq(g), 1.0)
+        clipped = (g * np.float32(coef)).astype(np.float64)
+        want = t.grad.numpy()
+        assert np.array_equal(np.isnan(clipped), np.isnan(want)), (bad, clipped, want)
+        fin = ~np.isnan(want)
+        assert np.array_equal(clipped[fin], want[fin]), (bad, clipped, want)
+
+
 def _bf_clip(gsteps, max_norm):
     """Clipped per-step (g, bound) in float64 from unclipped ones."""
     out = []
@@ -1039,4 +1056,5 @@ ALL_PINS = [
     pin_round_clipped_brute_force,
     pin_clip_inactive_is_bitwise_unclipped,
     pin_grad_total_streams,
+    pin_clip_nonfinite_norm_vs_torch,
 ]

@@ -81,9 +81,10 @@ MUTANTS = {
     "lr_warmup_off_by_one": [("const double s = (double)(t - 1);", "const double s = (double)t;")],
     "lr_min_ignored": [("    f = f * (1.0 - rho) + rho;\n", "")],
     "lr_full_cosine_cycle": [("f = 0.5 * (1.0 + cos(M_PI * q));", "f = 0.5 * (1.0 + cos(2.0 * M_PI * q));")],
-    "clip_no_clamp": [("return (float)(c < 1.0 ? c : 1.0);", "return (float)c;")],
+    "clip_no_clamp": [("return (float)(c >= 1.0 ? 1.0 : c);", "return (float)c;")],
     "clip_no_eps": [("(sqrt(total_sumsq) + 1e-6)", "sqrt(total_sumsq)")],
     "clip_no_sqrt": [("(sqrt(total_sumsq) + 1e-6)", "(total_sumsq + 1e-6)")],
+    "clip_nan_norm_to_one": [("(float)(c >= 1.0 ? 1.0 : c)", "(float)(c < 1.0 ? c : 1.0)")],
     "clip_ignored": [("    if (rc == 0 && max_grad_norm > 0.0f)\n      orc_clip(n, g, max_grad_norm, clip_totals ? clip_totals + a : NULL);\n", "")],
     "clip_before_sumsq": [("    if (rc == 0 && seg_sumsq)\n      rc = orc_seg_sumsq(n_seg, seg_off, g, seg_sumsq + (size_t)a * (size_t)n_seg);\n    if (rc == 0 && max_grad_norm > 0.0f)\n      orc_clip(n, g, max_grad_norm, clip_totals ? clip_totals + a : NULL);",
                            "    if (rc == 0 && max_grad_norm > 0.0f)\n      orc_clip(n, g, max_grad_norm, clip_totals ? clip_totals + a : NULL);\n    if (rc == 0 && seg_sumsq)\n      rc = orc_seg_sumsq(n_seg, seg_off, g, seg_sumsq + (size_t)a * (size_t)n_seg);")],
