@@ -248,7 +248,8 @@ float fl_lr_cosine(int64_t t, int64_t total_steps, int64_t warmup_steps, float l
  * Global-norm gradient clipping of a local step (the rule of
  * torch.nn.utils.clip_grad_norm_), driven by the sum of squares of the
  * reduced gradient:
- *     coef = (float)min(1, max_norm / (sqrt(total_sumsq) + 1e-6))   (double)
+ *     coef = (float)min(1, max_norm / (sqrt(total_sumsq) + 1e-6))   (double;
+ *            a NaN total gives a NaN coef, as torch's clamp does)
  *     g[i] = (acc[i] * grad_scale) * coef, then AdamW as fl_local_step
  * The norm is over the whole model, i.e. over every shard of the sharding
  * group: a multi-GPU caller computes its shard's sum with fl_grad_sumsq,

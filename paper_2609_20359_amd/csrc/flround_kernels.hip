@@ -170,10 +170,11 @@ __device__ __forceinline__ double wave_sum(double v) {
 }
 
 // Clip coefficient from the whole-shard sum of squares: min(1, max / (norm +
-// 1e-6)) in double, rounded once to float.
+// 1e-6)) in double, rounded once to float; a NaN norm gives NaN, as torch's
+// clamp does.
 __device__ __forceinline__ float clip_coef(const double* total, float max_norm) {
   const double c = (double)max_norm / (__builtin_sqrt(*total) + 1e-6);
-  return (float)(c < 1.0 ? c : 1.0);
+  return (float)(c >= 1.0 ? 1.0 : c);
 }
 
 // Segment of element `i`, searching [lo, hi] (segments overlapping the tile).

@@ -68,6 +68,37 @@ def test_clipped_round_parity(env, n, R, A, max_norm, kind):
     lay.close()
 
 
+@pytest.mark.parametrize("bad", [0x7FC0, 0x7F80, 0xFF80])
+def test_clipped_round_with_a_nonfinite_gradient(env, bad):
+    """One NaN or infinite bf16 value in the first step's first peer
+    gradient: a NaN norm makes every clipped gradient NaN; an infinite norm
+    gives a zero coefficient (NaN at the infinite entry itself), as
+    clip_grad_norm_ does.  Compared with the oracle element by element (NaN
+    positions, all other bits)."""
+    torch, P, orc = env["torch"], env["P"], env["orc"]
+    w = _workload(5003, 2, 2, 0.01, seed=13)
+    tag = "clip nonfinite 0x%04X" % bad
+    _say(tag)
+    k = 1234
+    lay = P.Layout(w.seg_offsets, w.seg_decay)
+    dev = B.DeviceInputs(w)
+    dev.grad_arrays[w.grad_index[0]].view(torch.int16)[k] = bad - 0x10000 if bad > 0x7FFF else bad
+    ss = torch.full((w.A * w.n_seg,), -1.0, dtype=torch.float32, device="cuda")
+    H.gpu_round(P, lay, w, dev, seg_sumsq=ss)
+    torch.cuda.synchronize()
+    host = B.HostInputs(w)
+    host.grad_arrays[w.grad_index[0]][k] = bad
+    ss_ref = H.oracle_round(orc, w, host, want_sumsq=True)
+    got = dict(master=dev.master.cpu().numpy(), m=dev.m.cpu().numpy(), v=dev.v.cpu().numpy(),
+               working=H.to_u16(dev.working))
+    H.assert_state_parity(tag, got, dict(master=host.master, m=host.m, v=host.v,
+                                         working=host.working), bitwise=True)
+    H.assert_sumsq(tag, ss.cpu().numpy(), ss_ref.reshape(-1))
+    n_nan = int(np.isnan(got["master"]).sum())
+    assert n_nan == (w.n if bad == 0x7FC0 else 1), "%s: %d NaNs in master" % (tag, n_nan)
+    lay.close()
+
+
 def test_grad_sumsq_then_clipped_step_equals_round(env):
     """The two-call form (sum of squares, then the clipped step: what a
     multi-GPU caller does around its all-reduce) is bitwise fl_round's."""
