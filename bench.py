@@ -282,11 +282,12 @@ def main():
     # step's reduced gradient (A x n_seg floats)
     seg_sumsq = torch.empty(w.A * w.n_seg, dtype=torch.float32, device="cuda")
     for i in range(Wm):
-        H.gpu_round(P, lay, w, dev, seg_sumsq=seg_sumsq, cfg=H.round_cfg(P, w, w.step0 + w.A * i))
+        H.gpu_round(P, lay, w, dev, seg_sumsq=seg_sumsq,
+                    cfg=H.round_cfg(P, w, w.step0 + w.A * i, dev=dev))
     torch.cuda.synchronize()
     log("warmup done (%d rounds)" % Wm)
 
-    cfgs = [H.round_cfg(P, w, w.step0 + w.A * (Wm + k), phase_events=events[k].handles)
+    cfgs = [H.round_cfg(P, w, w.step0 + w.A * (Wm + k), phase_events=events[k].handles, dev=dev)
             for k in range(K)]
     start = torch.cuda.Event(enable_timing=True)
     stop = torch.cuda.Event(enable_timing=True)

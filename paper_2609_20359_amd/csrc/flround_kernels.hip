@@ -186,15 +186,15 @@ __device__ __forceinline__ int find_seg(const int64_t* off, int lo, int hi, int6
   return lo;
 }
 
-// MODE 0: fused reduce + AdamW + working copy (g scaled by the clip
-// coefficient when a.clip_total is set); 1: reduce only (g_out); 2: AdamW
-// only (g_in); 3: reduce to the bf16 wire format (wire_out); 4: reduce with
-// no output but the sums of squares.  SUMSQ: per-piece sums of squares of g
-// (before clipping).
+// MODE 0: fused reduce + AdamW + working copy; 1: reduce only (g_out); 2:
+// AdamW only (g_in); 3: reduce to the bf16 wire format (wire_out); 4: reduce
+// with no output but the sums of squares.  In MODE 0 and 2 the gradient is
+// scaled by the clip coefficient when a.clip_total is set.  SUMSQ: per-piece
+// sums of squares of g (before clipping).
 template <int RT, int MODE, bool SUMSQ>
 __global__ void __launch_bounds__(kBlock) k_step(const StepArgs a) {
   const int tid = threadIdx.x;
-  const bool clip = MODE == 0 && a.clip_total != nullptr;
+  const bool clip = (MODE == 0 || MODE == 2) && a.clip_total != nullptr;
   const float coef = clip ? clip_coef(a.clip_total, a.clip_max) : 1.0f;
   for (int64_t t = blockIdx.x; t < a.L.n_tiles; t += gridDim.x) {
     const TileInfo ti = a.L.tiles[t];

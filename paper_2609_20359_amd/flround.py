@@ -54,7 +54,8 @@ class RoundCfg(ctypes.Structure):
                 ("replica_fp", ctypes.POINTER(ctypes.c_uint64)),
                 ("phase_events", ctypes.POINTER(ctypes.c_void_p)),
                 ("step_lr", ctypes.POINTER(ctypes.c_float)),
-                ("max_grad_norm", ctypes.c_float)]
+                ("max_grad_norm", ctypes.c_float),
+                ("grad_scratch", ctypes.c_void_p)]
 
 
 class OuterHparams(ctypes.Structure):
@@ -285,9 +286,11 @@ def fl_fedavg(layout, replicas, weights, master_out, working_out, replica_fp=Non
 
 
 def make_round_cfg(R, G, A, weights, hp, *, self_group=0, grad_scale=None, step0=1,
-                   replica_fp=None, phase_events=None, step_lr=None, max_grad_norm=0.0):
+                   replica_fp=None, phase_events=None, step_lr=None, max_grad_norm=0.0,
+                   grad_scratch=None):
     """Build an fl_round_cfg; the returned object keeps its arrays alive.
-    weights and replica_fp have G entries, step_lr A, phase_events A + 2."""
+    weights and replica_fp have G entries, step_lr A, phase_events A + 2;
+    grad_scratch is None or a CUDA float32 tensor of the layout's length."""
     w = _host_list([float(x) for x in weights], G, ctypes.c_float, "weights")
     fp = None if replica_fp is None else _host_list([int(x) for x in replica_fp], G,
                                                     ctypes.c_uint64, "replica_fp")
@@ -295,10 +298,20 @@ def make_round_cfg(R, G, A, weights, hp, *, self_group=0, grad_scale=None, step0
                                                       "phase_events")
     lrs = None if step_lr is None else _host_list([float(x) for x in step_lr], A, ctypes.c_float,
                                                   "step_lr")
+    scratch = None if grad_scratch is None else _buf(grad_scratch, grad_scratch.numel(), 4,
+                                                     "grad_scratch")
     cfg = RoundCfg(R, G, A, self_group, float(1.0 / R if grad_scale is None else grad_scale),
-                   hparams(hp), int(step0), w, fp, ev, lrs, float(max_grad_norm))
-    cfg._keep = (w, fp, ev, lrs)
+                   hparams(hp), int(step0), w, fp, ev, lrs, float(max_grad_norm), scratch)
+    cfg._keep = (w, fp, ev, lrs, grad_scratch)
     return cfg
+
+
+def _check_cfg(layout, cfg):
+    """The round configuration's tensor fields against the layout."""
+    keep = getattr(cfg, "_keep", None)
+    scratch = keep[4] if keep is not None and len(keep) > 4 else None
+    if scratch is not None:
+        _buf(scratch, layout.n, 4, "grad_scratch")
 
 
 def lr_cosine(t, total_steps, warmup_steps, lr_max, lr_min=0.0):
@@ -311,6 +324,7 @@ def fl_round(layout, cfg, grads, replicas, master, m, v, working, seg_sumsq=None
     """grads: A*R tensors (step-major); replicas: G tensors or None (entry
     self_group is ignored)."""
     n = layout.n
+    _check_cfg(layout, cfg)
     rc = lib().fl_round(layout.handle, ctypes.byref(cfg),
                         _bufs(grads, cfg.A * cfg.R, n, 2, "grads"),
                         _bufs(replicas, cfg.G, n, 2, "replicas"), _buf(master, n, 4, "master"),
@@ -400,6 +414,7 @@ def fl_round_outer(layout, cfg, outer, grads, replicas, prev, buf, master, m, v,
                    seg_sumsq=None, stream=None):
     o = outer_hparams(outer)
     n = layout.n
+    _check_cfg(layout, cfg)
     rc = lib().fl_round_outer(layout.handle, ctypes.byref(cfg), ctypes.byref(o),
                               _bufs(grads, cfg.A * cfg.R, n, 2, "grads"),
                               _bufs(replicas, cfg.G, n, 2, "replicas"), _buf(prev, n, 4, "prev"),

@@ -39,12 +39,15 @@ class DeviceInputs:
         self.buf = torch.zeros(n, **f32) if w.outer else None
         self.bcast = None if w.bcast_spec is None else dev_fill(torch.empty(n, **f32),
                                                                  w.bcast_spec)
+        self.grad_scratch = (torch.empty(n, **f32)
+                             if w.max_grad_norm > 0 and w.clip_scratch and w.H == 1 else None)
 
     def bytes(self):
         t = [self.master, self.m, self.v, self.working] + self.grad_arrays + \
             [r for r in self.replicas if r is not None] + \
             list({id(r): r for r in (self.replica_wires or []) if r is not None}.values()) + \
-            [x for x in (self.wire, self.bcast, self.prev, self.buf) if x is not None]
+            [x for x in (self.wire, self.bcast, self.prev, self.buf, self.grad_scratch)
+             if x is not None]
         return sum(x.numel() * x.element_size() for x in t)
 
 

@@ -121,8 +121,10 @@ class Workload:
     # outer optimiser (None: plain FedAvg): dict(lr, momentum, nesterov); the
     # outer state starts at prev = the initial master, buf = 0
     outer: Optional[dict] = None
-    # global-norm clipping of each local step's gradient (0: off)
+    # global-norm clipping of each local step's gradient (0: off); with
+    # clip_scratch the round gets an N-float scratch for the reduced gradient
     max_grad_norm: float = 0.0
+    clip_scratch: bool = False
 
     def __post_init__(self):
         if self.grad_scale is None:
@@ -149,6 +151,10 @@ class Workload:
             base += 2 + 2 * self.H
         if self.max_grad_norm > 0:
             base += 2 * (self.H if self.H > 1 else self.R)   # the sum-of-squares pass
+            if self.H == 1 and self.clip_scratch:
+                # the first pass also writes the reduced gradient (4) and the
+                # step reads it back (4) instead of the R peer gradients
+                base += 8 - 2 * self.R
         return base
 
     def fedavg_bytes_per_param(self):
@@ -194,7 +200,7 @@ def _normal_grads(n_arrays, seed, std=GRAD_STD):
 def make_workload(name, seg_sizes, seg_decay, R, G, A, *, weights=None, seed=0,
                   distinct_grads=True, student=False, own_drift=False, hp=None,
                   self_group=0, step0=1, grad_scale=None, note="", H=1, replica=0,
-                  hsdp_member=True, outer=None, max_grad_norm=0.0):
+                  hsdp_member=True, outer=None, max_grad_norm=0.0, clip_scratch=False):
     """General constructor used by the named workloads and by the tests.
 
     distinct_grads: A*R distinct gradient arrays (else R arrays reused by
@@ -238,7 +244,7 @@ def make_workload(name, seg_sizes, seg_decay, R, G, A, *, weights=None, seed=0,
                     grad_scale=grad_scale, note=note, H=H, replica=replica,
                     hsdp_member=hsdp_member, wire_specs=wires, bcast_spec=bcast,
                     outer=None if outer is None else dict(outer),
-                    max_grad_norm=float(max_grad_norm))
+                    max_grad_norm=float(max_grad_norm), clip_scratch=bool(clip_scratch))
 
 
 def tiny(seed=0):
@@ -310,10 +316,11 @@ def llama8b_s8_outer(seed=0):
 
 def llama8b_s8_clip(seed=0):
     """The Llama-3.1-8B S=8 round with every local step's gradient clipped to
-    global norm 1.0 (a sum-of-squares pass before each fused step)."""
+    global norm 1.0: a pass that sums the squares of the reduced gradient and
+    stores it in an N-float scratch, then the AdamW pass over it."""
     sizes, dec = llama31_8b_segments(8)
     return make_workload("llama31_8b_fsdp_s8_r8_g4_a8_clip1", sizes, dec, R=8, G=4, A=8,
-                         seed=seed, distinct_grads=False, max_grad_norm=1.0)
+                         seed=seed, distinct_grads=False, max_grad_norm=1.0, clip_scratch=True)
 
 
 ALL = dict(tiny=tiny, llama8b_s8=llama8b_s8, fedavg_heavy=fedavg_heavy, hsdp_s4=hsdp_s4,

@@ -87,17 +87,21 @@ def clip_totals(orc, w: Workload, chunk=1 << 24, say=None):
     return [done[key] for key in steps]
 
 
-def round_cfg(P, w: Workload, step0=None, phase_events=None):
+def round_cfg(P, w: Workload, step0=None, phase_events=None, dev=None):
+    """The round configuration of workload w (with dev: its gradient scratch,
+    if the workload has one)."""
+    scratch = None if dev is None else getattr(dev, "grad_scratch", None)
     return P.make_round_cfg(w.R, w.G, w.A, w.weights, w.hp, self_group=w.self_group,
                             grad_scale=w.grad_scale, step0=w.step0 if step0 is None else step0,
-                            phase_events=phase_events, max_grad_norm=w.max_grad_norm)
+                            phase_events=phase_events, max_grad_norm=w.max_grad_norm,
+                            grad_scratch=scratch)
 
 
 def gpu_round(P, layout, w: Workload, dev: DeviceInputs, seg_sumsq=None, phase_events=None,
               cfg=None):
     """One fl_round (or fl_round_hsdp when w.H > 1) through the C ABI."""
     if cfg is None:
-        cfg = round_cfg(P, w, phase_events=phase_events)
+        cfg = round_cfg(P, w, phase_events=phase_events, dev=dev)
     if w.outer is not None:
         P.fl_round_outer(layout, cfg, w.outer, dev.grads, dev.replicas, dev.prev, dev.buf,
                          dev.master, dev.m, dev.v, dev.working, seg_sumsq=seg_sumsq)

@@ -40,15 +40,18 @@ def _workload(n, R, A, max_norm, seed, **kw):
 @pytest.mark.parametrize("n,R,A,max_norm,kind", [
     (1, 1, 1, 1e-5, "fsdp"), (2049, 3, 2, 1e-3, "fsdp"), (100_003, 4, 2, 0.05, "fsdp"),
     (100_003, 4, 2, 1e9, "fsdp"), (262_147, 8, 1, 0.02, "fsdp"), (50_001, 3, 2, 0.01, "hsdp"),
-    (50_001, 3, 2, 0.01, "outer"),
+    (50_001, 3, 2, 0.01, "outer"), (1, 1, 2, 1e-5, "scratch"), (262_147, 8, 2, 0.02, "scratch"),
+    (70_001, 16, 1, 1e9, "scratch"), (50_001, 6, 2, 0.01, "outer-scratch"),
 ])
 def test_clipped_round_parity(env, n, R, A, max_norm, kind):
     torch, P, orc = env["torch"], env["P"], env["orc"]
     kw = {}
     if kind == "hsdp":
         kw = dict(H=3, replica=1, hsdp_member=True)
-    elif kind == "outer":
+    if kind.startswith("outer"):
         kw = dict(outer=dict(lr=0.7, momentum=0.9, nesterov=True))
+    if kind.endswith("scratch"):
+        kw["clip_scratch"] = True
     w = _workload(n, R, A, max_norm, seed=n + R, **kw)
     tag = "clip %s n=%d R=%d A=%d max=%g" % (kind, n, R, A, max_norm)
     _say(tag)
@@ -96,6 +99,39 @@ def test_clipped_round_with_a_nonfinite_gradient(env, bad):
     H.assert_sumsq(tag, ss.cpu().numpy(), ss_ref.reshape(-1))
     n_nan = int(np.isnan(got["master"]).sum())
     assert n_nan == (w.n if bad == 0x7FC0 else 1), "%s: %d NaNs in master" % (tag, n_nan)
+    lay.close()
+
+
+@pytest.mark.parametrize("R", [1, 3, 8, 16])
+def test_scratch_path_is_bitwise_the_two_read_path(env, R):
+    """With a gradient scratch the round reads the peer gradients once and
+    takes the AdamW-only pass; state and per-segment sums equal the round
+    without it bit for bit."""
+    torch, P = env["torch"], env["P"]
+    w = _workload(200_011, R, 3, 0.03, seed=20 + R)
+    lay = P.Layout(w.seg_offsets, w.seg_decay)
+    a, b = B.DeviceInputs(w), B.DeviceInputs(w)
+    scratch = torch.empty(w.n, dtype=torch.float32, device="cuda")
+    ssa = torch.empty(w.A * w.n_seg, dtype=torch.float32, device="cuda")
+    ssb = torch.empty_like(ssa)
+    H.gpu_round(P, lay, w, a, seg_sumsq=ssa)
+    cfg = P.make_round_cfg(w.R, w.G, w.A, w.weights, w.hp, self_group=w.self_group,
+                           grad_scale=w.grad_scale, step0=w.step0,
+                           max_grad_norm=w.max_grad_norm, grad_scratch=scratch)
+    P.fl_round(lay, cfg, b.grads, b.replicas, b.master, b.m, b.v, b.working, seg_sumsq=ssb)
+    torch.cuda.synchronize()
+    for k in ("master", "m", "v", "working"):
+        assert torch.equal(getattr(a, k).view(torch.int16), getattr(b, k).view(torch.int16)), k
+    assert torch.equal(ssa.view(torch.int32), ssb.view(torch.int32)), "per-segment sums"
+    bad = P.make_round_cfg(w.R, w.G, w.A, w.weights, w.hp, max_grad_norm=w.max_grad_norm,
+                           grad_scratch=b.m)
+    with pytest.raises(P.FlError) as e:
+        P.fl_round(lay, bad, b.grads, b.replicas, b.master, b.m, b.v, b.working)
+    assert e.value.status == -1
+    short = P.make_round_cfg(w.R, w.G, w.A, w.weights, w.hp, max_grad_norm=w.max_grad_norm,
+                             grad_scratch=scratch[:-8])
+    with pytest.raises(ValueError):
+        P.fl_round(lay, short, b.grads, b.replicas, b.master, b.m, b.v, b.working)
     lay.close()
 
 
