@@ -16,6 +16,8 @@
 //              sum-of-squares pass before a clipped step
 //   wire_R4    4 bf16 streams read, 1 bf16 stream written: the FL+HSDP
 //              first-tier reduction to the wire format
+//   reduce_R8  8 bf16 streams read, 1 fp32 stream written: the reduction
+//              that stores the gradient of a clipped step in its scratch
 //   fedavg_G4  4 bf16 streams read, 1 fp32 and 1 bf16 stream written
 //   fedopt_G4  as fedavg_G4 plus 2 fp32 streams read and written (the outer
 //              step's round-start model and momentum buffer)
@@ -227,6 +229,7 @@ int main(int argc, char** argv) {
   run<8, 0, 0, 0>("sumsq_R8", s, cus, elems);
   run<4, 0, 0, 0>("sumsq_R4", s, cus, elems);
   run<4, 0, 1, 0>("wire_R4", s, cus, elems);
+  run<8, 0, 0, 1>("reduce_R8", s, cus, elems);
   run<4, 0, 1, 1>("fedavg_G4", s, cus, elems);
   run<4, 2, 1, 1>("fedopt_G4", s, cus, elems);
   run_tiled(s, cus, elems);
