@@ -43,7 +43,7 @@ def compact_layout(w: Workload, idx, full_segments=()):
 
 
 def oracle_round(orc, w: Workload, host: HostInputs, seg_off=None, seg_decay=None,
-                 want_sumsq=False, clip_totals=None):
+                 want_sumsq=False, clip_totals=None, step_lr=None):
     """Run the oracle round (FL+FSDP, or FL+HSDP when w.H > 1) in place on host
     arrays.  Returns the per-step per-segment sums of squares or None.
     clip_totals: per-step whole-shard sums of squares to clip against when the
@@ -55,17 +55,18 @@ def oracle_round(orc, w: Workload, host: HostInputs, seg_off=None, seg_decay=Non
                                w.hp, w.step0, w.weights, w.outer, host.grads, host.replicas,
                                host.prev, host.buf, host.master, host.m, host.v, host.working,
                                want_sumsq=want_sumsq, max_grad_norm=w.max_grad_norm,
-                               clip_totals=clip_totals)
+                               clip_totals=clip_totals, step_lr=step_lr)
     if w.H > 1:
         return orc.round_hsdp(seg_off, seg_decay, w.R, w.H, w.replica, 1.0 / w.H, w.hsdp_member,
                               w.G, w.A, w.self_group, w.grad_scale, w.hp, w.step0, w.weights,
                               host.grads, host.replica_wires, host.replicas, host.bcast,
                               host.master, host.m, host.v, host.working, want_sumsq=want_sumsq,
-                              max_grad_norm=w.max_grad_norm, clip_totals=clip_totals)
+                              max_grad_norm=w.max_grad_norm, clip_totals=clip_totals,
+                              step_lr=step_lr)
     return orc.round(seg_off, seg_decay, w.R, w.G, w.A, w.self_group, w.grad_scale, w.hp,
                      w.step0, w.weights, host.grads, host.replicas, host.master, host.m, host.v,
                      host.working, want_sumsq=want_sumsq, max_grad_norm=w.max_grad_norm,
-                     clip_totals=clip_totals)
+                     clip_totals=clip_totals, step_lr=step_lr)
 
 
 def clip_totals(orc, w: Workload, chunk=1 << 24, say=None):
@@ -87,14 +88,14 @@ def clip_totals(orc, w: Workload, chunk=1 << 24, say=None):
     return [done[key] for key in steps]
 
 
-def round_cfg(P, w: Workload, step0=None, phase_events=None, dev=None):
+def round_cfg(P, w: Workload, step0=None, phase_events=None, dev=None, step_lr=None):
     """The round configuration of workload w (with dev: its gradient scratch,
     if the workload has one)."""
     scratch = None if dev is None else getattr(dev, "grad_scratch", None)
     return P.make_round_cfg(w.R, w.G, w.A, w.weights, w.hp, self_group=w.self_group,
                             grad_scale=w.grad_scale, step0=w.step0 if step0 is None else step0,
                             phase_events=phase_events, max_grad_norm=w.max_grad_norm,
-                            grad_scratch=scratch)
+                            grad_scratch=scratch, step_lr=step_lr)
 
 
 def gpu_round(P, layout, w: Workload, dev: DeviceInputs, seg_sumsq=None, phase_events=None,
