@@ -32,10 +32,16 @@ def log(*a):
 
 
 def kernel_source_hash():
+    """Hash of the kernel sources with comments and whitespace removed, so
+    that it changes with the code the counters measured and not with its
+    commentary."""
     h = hashlib.sha256()
     for p in KERNEL_SOURCES:
-        with open(p, "rb") as f:
-            h.update(f.read())
+        with open(p) as f:
+            src = f.read()
+        src = re.sub(r"/\*.*?\*/", " ", src, flags=re.S)
+        src = re.sub(r"//[^\n]*", " ", src)
+        h.update(" ".join(src.split()).encode())
     return h.hexdigest()[:16]
 
 

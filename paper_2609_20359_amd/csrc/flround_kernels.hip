@@ -14,10 +14,11 @@
 //     -ffp-contract=off), so results are bitwise those of the definition and
 //     do not depend on the grid;
 //   * per-segment sums of squares use wave64 butterfly reductions only: each
-//     wave writes one fp32 partial per (tile, segment) piece it covers, with
-//     no workgroup barrier in the streaming loop, and a small two-stage
-//     finalize folds the partials per segment in double; only tiles that straddle a
-//     segment boundary (rare) resolve segments per element.
+//     lane squares its elements exactly in double, and each wave writes one
+//     double partial per (tile, segment) piece it covers, with no workgroup
+//     barrier in the streaming loop; a small finalize folds the partials per
+//     segment (and, for clipping, over the shard) in fixed trees; only tiles
+//     that straddle a segment boundary (rare) resolve segments per element.
 #include "flr_internal.h"
 
 namespace flr {
