@@ -119,9 +119,8 @@ typedef struct {
  * peer_grads: host array of R device pointers to N bf16 values (may repeat).
  * grad_out: device pointer, N floats (must not overlap an input).
  * seg_sumsq: NULL, or device pointer to n_seg floats receiving, per segment,
- *   the sum of grad_out[i]^2 (
- *   exact double squares, fixed-tree double sums, rounded once to float):
- *   per-layer gradient-norm telemetry.  Needs a stream-ordered temporary of
+ *   the sum of grad_out[i]^2 (exact double squares, fixed-tree double sums,
+ *   rounded once to float): per-layer gradient-norm telemetry.  Needs a stream-ordered temporary of
  *   32 bytes per (2048-element tile, segment) pair, allocated and freed on
  *   `stream`.
  * 1 <= R <= FL_MAX_PEERS; grad_scale finite.
@@ -199,6 +198,9 @@ int fl_fedavg(const fl_layout* layout, int G, const uint16_t* const* replicas,
  *   place and pairwise distinct.
  * seg_sumsq: NULL, or device pointer to A*n_seg floats (row a = local step a;
  *   see fl_shard_reduce).
+ * Allocation: with seg_sumsq or max_grad_norm > 0 the round takes one
+ *   stream-ordered temporary (as fl_shard_reduce) for all its steps;
+ *   otherwise it allocates nothing and may be captured in a HIP graph.
  * Configuration: 1 <= R <= FL_MAX_PEERS, 1 <= G <= FL_MAX_GROUPS, A >= 1,
  *   0 <= self_group < G, step0 >= 1, grad_scale finite, h and weights as
  *   above, replica_fp as in fl_fedavg, step_lr entries finite and >= 0,
