@@ -8,6 +8,7 @@
 //   read1      1 stream read
 //   write1     1 stream written
 //   copy       1 read, 1 written
+//   triad      2 read, 1 written (STREAM's triad traffic)
 //   step_R8    8 bf16 streams read, 3 fp32 streams read and written, 1 bf16
 //              stream written: the traffic of one fused local step (R = 8)
 //   step_R4, step_R2  the same with 4 and 2 peer streams (R = 4; the FL+HSDP
@@ -223,6 +224,7 @@ int main(int argc, char** argv) {
   run<1, 0, 0, 0>("read1", s, cus, elems);
   run<0, 0, 1, 0>("write1", s, cus, elems);
   run<1, 0, 1, 0>("copy", s, cus, elems);
+  run<2, 0, 1, 0>("triad", s, cus, elems);
   run<8, 3, 1, 0>("step_R8", s, cus, elems);
   run<4, 3, 1, 0>("step_R4", s, cus, elems);
   run<2, 3, 1, 0>("step_R2", s, cus, elems);
