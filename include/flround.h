@@ -160,9 +160,9 @@ int fl_local_step(const fl_layout* layout, const fl_adamw_hparams* h, int64_t st
 
 /* ------------------------------------------------------------------------
  * fl_fedavg -- FedAvg of G federation-group replicas of this shard
- * (Section 2, Federated Learning; Section 4.1 Eq. (3); Section 4.2: after
- * aggregation every shard equals the average of its corresponding shards,
- * so every group sums the same bf16 inputs in the same ascending order and
+ * (Section 2, Federated Learning; Section 4.1 Eq. (3); Section 4.2: once
+ * aggregated, a shard is the mean of the matching shards of all groups, so
+ * every group sums the same bf16 inputs in the same ascending order and
  * ends bit-identical):
  *     w'_g = w_g / sum_g w_g        (host, double, rounded to float)
  *     acc = 0; for g in 0..G-1: acc = acc + w'_g * f32(replicas[g][i])
@@ -242,8 +242,9 @@ int fl_round(const fl_layout* layout, const fl_round_cfg* cfg, const uint16_t* c
 
 /* ------------------------------------------------------------------------
  * fl_lr_cosine -- the learning rate of optimiser step t (1-based) under
- * cosine decay with linear warm-up (Section 5: cosine-decay scheduler with
- * 10 % warm-up steps), in double, rounded once to float; s = t - 1:
+ * cosine decay with linear warm-up (Section 5 decays the learning rate on a
+ * cosine after warming it up over the first tenth of the run), in double,
+ * rounded once to float; s = t - 1:
  *     s < warmup:  f = s / max(1, warmup)
  *     otherwise:   q = (s - warmup) / max(1, total - warmup);
  *                  f = 0.5 (1 + cos(pi q)); f = f (1 - lr_min/lr_max) + lr_min/lr_max;

@@ -32,14 +32,14 @@
  *         decay_s = 1 - lr * weight_decay if segment s decays, else 1.
  *  (a3) FedAvg: the weighted average of the G federation groups' replicas
  *       of the shard (Section 2, Federated Learning; Section 4.1, Eq. (3);
- *       Section 4.2, Eq. (4): after aggregation every shard equals the
- *       average of its corresponding shards):
+ *       Section 4.2, Eq. (4): once aggregated, a shard is the mean of the
+ *       matching shards of all groups):
  *         w_g' = w_g / sum_g w_g          (double, then float)
  *         acc = 0; for g = 0..G-1: acc = acc + w_g' * f32(rep_g[i])   (fp32)
  *         master = acc; working = bf16_rne(acc); m and v unchanged.
  *  (a4) one round: A local steps (a1 then a2 at step t = step0 + a), then
  *       FedAvg with the own replica taken from the bf16 working copy
- *       (Section 4.2: FedAvg after the local update every A steps).
+ *       (Section 4.2: groups aggregate once per A local optimiser steps).
  *  (a5) per-segment sum of squares of g for each local step, accumulated in
  *       double in index order.
  *  (n4) learning-rate schedule (Section 5: cosine decay with 10 % warm-up):

@@ -6,8 +6,8 @@ A local steps), the FedAvg weights, the AdamW hyperparameters and the
 generator specs of every input array.  Sizes and distributions follow the
 method's setting: Llama-3.1-8B trained in bf16 with AdamW at lr 3e-4 and an
 aggregation every 8 local steps (Section 5, experimental setup), sharded
-FSDP-style so that every layer is split equally over the S shards of a
-sharding group (Section 2, FSDP).
+FSDP-style, each layer cut into S equal slices, one per GPU of a sharding
+group (Section 2, FSDP).
 
 Stream ids: master 1; gradient array k -> 1000 + k; drift of group g ->
 2000 + g; layout and weight draws 3000..3009.
