@@ -62,8 +62,44 @@ def read_traffic(current_hash):
 
 
 LOCAL_STEP_KERNEL = "k_step<8, 0, true>"
-FEDAVG_KERNEL = "k_fedavg<4, false>"
 COPY_KERNEL = "__amd_rocclr_copyBuffer"
+
+
+def _rt(k):
+    """Template count of a dispatched kernel (the generic instance is 0)."""
+    return k if k in (1, 2, 4, 8, 16) else 0
+
+
+def round_kernels(w):
+    """(kernel name, algorithmic bytes read, bytes written) per launch for each
+    streaming kernel a round of workload w launches (bench.py asks for the
+    per-segment sums in every round)."""
+    n = w.n
+    ks = []
+    r = w.H if w.H > 1 else w.R
+    if w.H > 1:
+        ks.append(("k_step<%d, 3, false>" % _rt(w.R), 2 * w.R * n, 2 * n))
+    if w.max_grad_norm > 0 and w.H == 1 and w.clip_scratch:
+        ks.append(("k_step<%d, 1, true>" % _rt(w.R), 2 * w.R * n, 4 * n))
+        ks.append(("k_step<1, 2, false>", 16 * n, 14 * n))
+    elif w.max_grad_norm > 0:
+        ks.append(("k_step<%d, 4, true>" % _rt(r), 2 * r * n, 0))
+        ks.append(("k_step<%d, 0, false>" % _rt(r), (2 * r + 12) * n, 14 * n))
+    else:
+        ks.append(("k_step<%d, 0, true>" % _rt(r), (2 * r + 12) * n, 14 * n))
+    if w.H > 1 and not w.hsdp_member:
+        ks.append(("k_bcast_recv", 4 * n, 6 * n))
+    elif w.outer is not None:
+        ks.append(("k_fedavg<%d, true>" % _rt(w.G), (2 * w.G + 8) * n, 14 * n))
+    else:
+        ks.append(("k_fedavg<%d, false>" % _rt(w.G), 2 * w.G * n, 6 * n))
+    return ks
+
+
+def traffic_file(workload):
+    if workload == "llama8b_s8":
+        return TRAFFIC_FILE
+    return os.path.join(ROOT, "profiles", "traffic_%s.md" % W_ALL()[workload]().name)
 
 
 def _pmc_means(path):
@@ -77,16 +113,17 @@ def _pmc_means(path):
     return {k: (sum(v) / len(v), len(v)) for k, v in acc.items()}
 
 
-def summarize_pmc(fetch_csv, write_csv, copy_mib, cmd_fetch, cmd_write):
+def summarize_pmc(fetch_csv, write_csv, copy_mib, cmd_fetch, cmd_write, workload="llama8b_s8"):
     """Markdown summary of two counter passes (FETCH_SIZE, WRITE_SIZE, KiB per
     dispatch), scaled by what each counter reads for the plain copy of
-    copy_mib MiB that the same runs performed."""
-    w = W_ALL()["llama8b_s8"]()
+    copy_mib MiB that the same runs performed, for every streaming kernel a
+    round of the workload launches."""
+    w = W_ALL()[workload]()
     fetch, write = _pmc_means(fetch_csv), _pmc_means(write_csv)
 
-    def pick(table, name, grid=None):
+    def pick(table, name):
         for (k, g), v in table.items():
-            if name in k and (grid is None or g == grid):
+            if name in k:
                 return v
         raise KeyError(name)
 
@@ -95,7 +132,9 @@ def summarize_pmc(fetch_csv, write_csv, copy_mib, cmd_fetch, cmd_write):
     big = max(cands, key=lambda kg: fetch[kg][0])
     f_copy, w_copy = fetch[big][0], write[big][0]
     f_scale, w_scale = copy_kib / f_copy, copy_kib / w_copy
-    lines = ["# HBM traffic of the local-step and FedAvg kernels, Llama-3.1-8B shard (S=8)", "",
+    d = w.describe()
+    lines = ["# HBM traffic of the kernels of one round: %s" % d["workload"], "",
+             ", ".join("%s=%s" % (k, d[k]) for k in d if k != "workload"), "",
              "Counter passes (one counter per run, KiB per dispatch):", "",
              "    " + cmd_fetch, "    " + cmd_write, "",
              "Calibration: the same runs copy %d MiB with %s (reads and writes %d KiB)." % (
@@ -105,11 +144,8 @@ def summarize_pmc(fetch_csv, write_csv, copy_mib, cmd_fetch, cmd_write):
              "| kernel | dispatches | FETCH_SIZE KiB | WRITE_SIZE KiB | scaled read GB | "
              "scaled write GB | algorithmic read GB | algorithmic write GB | traffic / algorithmic |",
              "|---|---|---|---|---|---|---|---|---|"]
-    n = w.n
-    specs = [(LOCAL_STEP_KERNEL, (2 * w.R + 12) * n, 14 * n),
-             (FEDAVG_KERNEL, 2 * w.G * n, 6 * n)]
     out = {}
-    for name, alg_r, alg_w in specs:
+    for name, alg_r, alg_w in round_kernels(w):
         f, cnt = pick(fetch, name)
         wr, _ = pick(write, name)
         rb, wb = f * f_scale * 1024, wr * w_scale * 1024
@@ -118,9 +154,10 @@ def summarize_pmc(fetch_csv, write_csv, copy_mib, cmd_fetch, cmd_write):
             name, cnt, f, wr, rb / 1e9, wb / 1e9, alg_r / 1e9, alg_w / 1e9,
             (rb + wb) / (alg_r + alg_w)))
     lines += ["", "Values read by bench.py (roofline.traffic of the local-step kernel):", "",
-              "- kernel_source_hash: %s" % kernel_source_hash(),
-              "- hbm_bytes_per_launch: %.0f" % out[LOCAL_STEP_KERNEL],
-              "- fedavg_hbm_bytes_per_launch: %.0f" % out[FEDAVG_KERNEL], ""]
+              "- kernel_source_hash: %s" % kernel_source_hash()]
+    if LOCAL_STEP_KERNEL in out and workload == "llama8b_s8":
+        lines.append("- hbm_bytes_per_launch: %.0f" % out[LOCAL_STEP_KERNEL])
+    lines.append("")
     return "\n".join(lines)
 
 
@@ -238,7 +275,7 @@ def main():
     if args.summarize_pmc:
         cmds = args.cmd + ["", ""]
         print(summarize_pmc(args.summarize_pmc[0], args.summarize_pmc[1],
-                            args.copy_calibration or 1024, cmds[0], cmds[1]))
+                            args.copy_calibration or 1024, cmds[0], cmds[1], args.workload))
         return
     if args.summarize_trace:
         print(summarize_trace(args.summarize_trace, (args.cmd + [""])[0], args.workload))
