@@ -143,3 +143,15 @@ def test_binding_checks_host_lists_and_tensors_without_a_gpu():
         F.fl_round(FakeLayout, cfg, [None] * 3, [None, None], None, None, None, None)
     with pytest.raises(ValueError, match="entries"):
         F.fl_fedavg(FakeLayout, [None, None], [1.0], None, None)
+
+
+def test_binding_fails_loudly_without_the_library(monkeypatch, tmp_path):
+    """No fallback: with the library absent every call raises."""
+    import pytest
+
+    monkeypatch.setattr(F, "_lib", None)
+    monkeypatch.setattr(F, "LIB_PATH", str(tmp_path / "missing.so"))
+    with pytest.raises(RuntimeError, match="not built"):
+        F.lib()
+    with pytest.raises(RuntimeError, match="not built"):
+        F.lr_cosine(1, 10, 1, 1e-3)
