@@ -49,14 +49,17 @@ def _parity(env, w, tag):
     lay.close()
 
 
-def test_tiles_with_many_segments(env):
+@pytest.mark.parametrize("clip,scratch", [(0.0, False), (1e-3, False), (1e-3, True)])
+def test_tiles_with_many_segments(env, clip, scratch):
     """Runs of one-element and tiny segments, so single 2048-element tiles
-    hold hundreds of segments, between large ones."""
+    hold hundreds of segments, between large ones; unclipped, and clipped
+    through the sum-of-squares pass or the scratch pass."""
     sizes = [5000] + [1] * 700 + [3, 2, 1] * 100 + [4096, 1, 2047, 2049] + [7] * 300 + [10000]
     r = np.random.default_rng(21)
     flags = r.integers(0, 2, len(sizes)).astype(np.uint8)
-    w = W.make_workload("many_segments", sizes, flags, R=3, G=2, A=2)
-    _parity(env, w, "many_segments")
+    w = W.make_workload("many_segments", sizes, flags, R=3, G=2, A=2, max_grad_norm=clip,
+                        clip_scratch=scratch)
+    _parity(env, w, "many_segments clip=%g scratch=%s" % (clip, scratch))
 
 
 @pytest.mark.parametrize("hp,step0", [
