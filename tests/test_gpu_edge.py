@@ -214,3 +214,41 @@ def test_binding_rejects_mismatched_tensors(env):
     torch.cuda.synchronize()
     assert torch.equal(master, keep), "a refused call changed the state"
     lay.close()
+
+
+@pytest.mark.parametrize("kind", ["clip", "clip-scratch", "hsdp", "hsdp-recv", "outer"])
+def test_every_path_is_independent_of_the_launch_shape(env, kind):
+    """The same round under the default launch shapes and three forced ones
+    (1, 3 and 7 workgroups per CU for every pass) gives the same bits: state,
+    outer state and per-segment sums."""
+    torch, P = env["torch"], env["P"]
+    r = np.random.default_rng(26)
+    sizes = r.integers(1, 90_000, 17)
+    flags = r.integers(0, 2, sizes.size).astype(np.uint8)
+    kw = dict(clip=dict(max_grad_norm=0.01), hsdp=dict(H=3, replica=2),
+              outer=dict(outer=W.DILOCO_OUTER))
+    kw["clip-scratch"] = dict(max_grad_norm=0.01, clip_scratch=True)
+    kw["hsdp-recv"] = dict(H=2, replica=1, hsdp_member=False, max_grad_norm=0.01)
+    w = W.make_workload("shape_" + kind, sizes, flags, R=6, G=3, A=2, step0=4, **kw[kind])
+    lay = P.Layout(w.seg_offsets, w.seg_decay)
+    results = []
+    prev = P.set_blocks_per_cu(0)
+    try:
+        for bpc in (0, 1, 3, 7):
+            P.set_blocks_per_cu(bpc)
+            dev = B.DeviceInputs(w)
+            ss = torch.full((w.A * w.n_seg,), -1.0, dtype=torch.float32, device="cuda")
+            H.gpu_round(P, lay, w, dev, seg_sumsq=ss)
+            torch.cuda.synchronize()
+            keep = [dev.master, dev.m, dev.v, dev.working, ss]
+            if w.outer is not None:
+                keep += [dev.prev, dev.buf]
+            results.append([t.clone() for t in keep])
+            del dev
+    finally:
+        P.set_blocks_per_cu(prev)
+    for bpc, res in zip((1, 3, 7), results[1:]):
+        for a, b in zip(results[0], res):
+            assert torch.equal(a.view(torch.int16), b.view(torch.int16)), \
+                "%s differs at %d workgroups per CU" % (kind, bpc)
+    lay.close()
