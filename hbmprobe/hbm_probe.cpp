@@ -22,6 +22,8 @@
 //   fedavg_G4  4 bf16 streams read, 1 fp32 and 1 bf16 stream written
 //   fedopt_G4  as fedavg_G4 plus 2 fp32 streams read and written (the outer
 //              step's round-start model and momentum buffer)
+//   bcast      4 bytes read (two 2-byte streams), 1 fp32 and 1 bf16 stream
+//              written: the FL+HSDP broadcast receive
 //   step_R8_tiled  as step_R8, but the three fp32 state arrays interleaved per
 //              2048-element tile ([tile][master | m | v]), i.e. one 24 KB
 //              read-modify-write chunk per tile instead of three streams
@@ -234,6 +236,7 @@ int main(int argc, char** argv) {
   run<8, 0, 0, 1>("reduce_R8", s, cus, elems);
   run<4, 0, 1, 1>("fedavg_G4", s, cus, elems);
   run<4, 2, 1, 1>("fedopt_G4", s, cus, elems);
+  run<2, 0, 1, 1>("bcast", s, cus, elems);
   run_tiled(s, cus, elems);
   for (void* p : bufs) CK(hipFree(p));
   return 0;
