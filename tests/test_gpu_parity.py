@@ -7,6 +7,7 @@ import pytest
 import harness as H
 import synth
 import synth.buffers  # noqa: F401
+import synth.buffers as B
 from synth import workloads as W
 
 pytestmark = pytest.mark.gpu
@@ -336,3 +337,32 @@ def test_errors_are_returned_before_any_launch(env):
     torch.cuda.synchronize()
     lay.close()
     other.close()
+
+
+@pytest.mark.parametrize("kind", ["fsdp", "outer", "clip"])
+def test_many_rounds_stay_bitwise(env, kind):
+    """Twelve consecutive rounds on the same device state (step counter and
+    bias corrections advancing, the other groups' replicas fixed), compared
+    with the oracle after every round."""
+    torch, P, orc = env["torch"], env["P"], env["orc"]
+    r = np.random.default_rng(40)
+    sizes = r.integers(1, 40_000, 9)
+    flags = r.integers(0, 2, sizes.size).astype(np.uint8)
+    kw = dict(outer=dict(outer=W.DILOCO_OUTER), clip=dict(max_grad_norm=0.02), fsdp={})[kind]
+    w = W.make_workload("rounds_" + kind, sizes, flags, R=4, G=3, A=3, step0=1, **kw)
+    lay = P.Layout(w.seg_offsets, w.seg_decay)
+    dev = B.DeviceInputs(w)
+    host = B.HostInputs(w)
+    for rnd in range(12):
+        step0 = w.step0 + rnd * w.A
+        H.gpu_round(P, lay, w, dev, cfg=H.round_cfg(P, w, step0, dev=dev))
+        H.oracle_round(orc, W.Workload(**{**w.__dict__, "step0": step0}), host)
+        torch.cuda.synchronize()
+        got = dict(master=dev.master.cpu().numpy(), m=dev.m.cpu().numpy(),
+                   v=dev.v.cpu().numpy(), working=H.to_u16(dev.working))
+        H.assert_state_parity("%s round %d" % (kind, rnd), got,
+                              dict(master=host.master, m=host.m, v=host.v,
+                                   working=host.working), bitwise=True)
+        if w.outer is not None:
+            assert np.array_equal(dev.buf.cpu().numpy().view(np.uint32), host.buf.view(np.uint32))
+    lay.close()
