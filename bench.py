@@ -229,30 +229,56 @@ def W_ALL():
 
 
 def cpu_baseline(w, n_sample):
-    """The oracle as it stands, one thread, one full round on the first
-    n_sample elements of the same shard (same generator, same segments)."""
+    """The oracle as it stands, timed on the host's cores: one full round on
+    the first n_sample elements of the same shard (same generator, same
+    segments), split into one contiguous chunk per thread; every thread runs
+    the unchanged single-threaded oracle on its chunk (ctypes releases the
+    GIL).  Also the one-thread rate on the first chunk."""
+    import copy
+    from concurrent.futures import ThreadPoolExecutor
+
     import numpy as np
 
     import harness as H
     import oracle
     import synth.buffers as B
+    from synth import host_threads
 
     orc = oracle.Oracle()
     n_sample = min(n_sample, w.n)
-    idx = np.arange(n_sample, dtype=np.int64)
-    off = w.seg_offsets[w.seg_offsets < n_sample]
-    off = np.append(off, n_sample).astype(np.int64)
-    dec = w.seg_decay[:off.size - 1]
-    host = B.HostInputs(w, idx)
+    T = max(1, min(host_threads(), n_sample))
+    bounds = np.linspace(0, n_sample, T + 1).astype(np.int64)
+    jobs = []
+    for t in range(T):
+        lo, hi = int(bounds[t]), int(bounds[t + 1])
+        inner = w.seg_offsets[(w.seg_offsets > lo) & (w.seg_offsets < hi)]
+        off = np.concatenate([[lo], inner, [hi]]).astype(np.int64) - lo
+        first = int(np.searchsorted(w.seg_offsets, lo, side="right")) - 1
+        dec = w.seg_decay[first:first + off.size - 1]
+        jobs.append((B.HostInputs(w, span=(lo, hi)), off, dec))
+
+    def run(job):
+        host, off, dec = job
+        H.oracle_round(orc, w, host, seg_off=off, seg_decay=dec, want_sumsq=True)
+
+    per_param = w.A * w.step_bytes_per_param() + w.fedavg_bytes_per_param()
+    first = (copy.deepcopy(jobs[0][0]),) + jobs[0][1:]
     t0 = time.perf_counter()
-    H.oracle_round(orc, w, host, seg_off=off, seg_decay=dec, want_sumsq=True)
-    dt = time.perf_counter() - t0
-    bytes_round = n_sample * (w.A * w.step_bytes_per_param() + w.fedavg_bytes_per_param())
-    return dict(value=round(bytes_round / dt / 1e9, 4), unit="GB/s", cores=1, kind="oracle",
-                params_per_s=round(n_sample / dt, 1), seconds=round(dt, 3),
+    run(first)
+    dt1 = time.perf_counter() - t0
+    n1 = int(bounds[1] - bounds[0])
+    del first
+    with ThreadPoolExecutor(T) as ex:
+        t0 = time.perf_counter()
+        list(ex.map(run, jobs))
+        dt = time.perf_counter() - t0
+    return dict(value=round(n_sample * per_param / dt / 1e9, 4), unit="GB/s", cores=T,
+                kind="oracle", params_per_s=round(n_sample / dt, 1), seconds=round(dt, 3),
+                one_thread_gbs=round(n1 * per_param / dt1 / 1e9, 4),
                 sample="one round with per-segment sums (A=%d, R=%d, G=%d, H=%d) on the first "
-                       "%d elements of the same shard (%d segment(s)), single-threaded C "
-                       "oracle" % (w.A, w.R, w.G, w.H, n_sample, off.size - 1))
+                       "%d elements of the same shard, as %d contiguous chunks run concurrently, "
+                       "one thread each, by the single-threaded C oracle" % (
+                           w.A, w.R, w.G, w.H, n_sample, T))
 
 
 def main():

@@ -72,9 +72,14 @@ def gather_f32(t, idx_dev):
 class HostInputs:
     """The same inputs on the host, for all elements or at given indices."""
 
-    def __init__(self, w: Workload, idx=None):
+    def __init__(self, w: Workload, idx=None, span=None):
+        """idx: element indices (sorted), or span: a contiguous (lo, hi)
+        range; neither: the whole shard."""
         self.w = w
-        if idx is None:
+        if span is not None:
+            lo, hi = int(span[0]), int(span[1])
+            fill = lambda sp: host_fill(sp, lo, hi - lo)  # noqa: E731
+        elif idx is None:
             fill = lambda sp: host_fill(sp, 0, w.n)  # noqa: E731
         else:
             fill = lambda sp: host_gather(sp, idx)  # noqa: E731

@@ -89,3 +89,11 @@ def test_trace_summary_format(tmp_path):
     out = bench.summarize_trace(str(csv), "cmd", "llama8b_s8")
     assert "llama31_8b_fsdp_s8_r8_g4_a8" in out
     assert "| k_step<8, 0, true>(flr::StepArgs) | 8 | 8000.0 | 7900.0 | 8100.0 | 90.00 % |" in out
+
+
+def test_cpu_baseline_runs_the_oracle_on_host_threads():
+    sys.path.insert(0, os.path.join(ROOT, "tests"))
+    cb = bench.cpu_baseline(W.llama8b_s8(), 1 << 16)
+    assert cb["kind"] == "oracle" and cb["unit"] == "GB/s"
+    assert cb["cores"] >= 1 and cb["value"] > 0 and cb["one_thread_gbs"] > 0
+    assert "%d elements" % (1 << 16) in cb["sample"]
