@@ -66,7 +66,12 @@ typedef enum {
 /* Human-readable name of a status code (static storage). */
 const char* fl_status_string(int status);
 
-/* ABI version: (major << 16) | minor. */
+/* ABI version: (major << 16) | minor.  Minor versions add entry points or
+ * append fields to the end of a configuration struct; a caller built against
+ * minor k needs a library of minor >= k.  Minor 1: the FL+HSDP entry
+ * points; 2: the outer step; 3: fl_lr_cosine and fl_round_cfg.step_lr;
+ * 4: fl_round_cfg.max_grad_norm and the clipping entry points;
+ * 5: fl_round_cfg.grad_scratch. */
 int fl_version(void);
 
 /* ------------------------------------------------------------------------

@@ -329,7 +329,7 @@ const char* fl_status_string(int status) {
   }
 }
 
-int fl_version(void) { return (1 << 16) | 4; }
+int fl_version(void) { return (1 << 16) | 5; }
 
 float fl_lr_cosine(int64_t t, int64_t total_steps, int64_t warmup_steps, float lr_max,
                    float lr_min) {
