@@ -14,7 +14,7 @@ from synth import workloads as W
 
 pytestmark = pytest.mark.gpu
 
-N_CASES = 32
+N_CASES = 128
 
 
 def _say(*a):
