@@ -88,3 +88,50 @@ def test_random_round_configuration(env, k):
                               dict(master=host.prev, m=host.buf), bitwise=True)
     H.assert_sumsq(tag, ss.cpu().numpy(), ss_ref.reshape(-1))
     lay.close()
+
+
+def _large_case(k):
+    r = np.random.default_rng(90000 + k)
+    n = int(r.integers(2_000_000, 8_000_000))
+    nseg = int(r.integers(1, 400))
+    cuts = np.sort(r.choice(np.arange(1, n), size=nseg - 1, replace=False)) if nseg > 1 else []
+    off = np.concatenate([[0], cuts, [n]]).astype(np.int64)
+    flags = r.integers(0, 2, off.size - 1).astype(np.uint8)
+    R = int(r.choice([1, 3, 4, 8, 12, 16]))
+    G = int(r.integers(1, 8))
+    Hh = (1, 2, 1, 3)[k % 4]                    # FL+FSDP and FL+HSDP cases
+    outer = None if Hh > 1 or r.random() < 0.5 else W.DILOCO_OUTER
+    clip = 0.0 if r.random() < 0.5 else float(10 ** r.uniform(-3, 0))
+    return W.make_workload("large_%d" % k, np.diff(off), flags, R=R, G=G, A=int(r.integers(1, 3)),
+                           seed=k, weights=r.uniform(0.1, 5.0, G).astype(np.float32),
+                           self_group=int(r.integers(0, G)), step0=int(r.integers(1, 500)), H=Hh,
+                           replica=int(r.integers(0, Hh)),
+                           hsdp_member=bool(Hh == 1 or k % 4 == 1), outer=outer,
+                           max_grad_norm=clip, clip_scratch=bool(clip > 0 and r.random() < 0.5))
+
+
+@pytest.mark.parametrize("k", range(4))
+def test_random_large_configuration(env, k):
+    """Random configurations of 2-8 million elements and up to 400 segments,
+    compared with the oracle on the whole shard."""
+    torch, P, orc = env["torch"], env["P"], env["orc"]
+    w = _large_case(k)
+    tag = "large case %d %s" % (k, w.describe())
+    _say(tag)
+    lay = P.Layout(w.seg_offsets, w.seg_decay)
+    dev = B.DeviceInputs(w)
+    ss = torch.full((w.A * w.n_seg,), -1.0, dtype=torch.float32, device="cuda")
+    H.gpu_round(P, lay, w, dev, seg_sumsq=ss)
+    torch.cuda.synchronize()
+    host = B.HostInputs(w)
+    ss_ref = H.oracle_round(orc, w, host, want_sumsq=True)
+    got = dict(master=dev.master.cpu().numpy(), m=dev.m.cpu().numpy(), v=dev.v.cpu().numpy(),
+               working=H.to_u16(dev.working))
+    H.assert_state_parity(tag, got, dict(master=host.master, m=host.m, v=host.v,
+                                         working=host.working), bitwise=True)
+    if w.outer is not None:
+        H.assert_state_parity(tag + " outer state", dict(master=dev.prev.cpu().numpy(),
+                                                         m=dev.buf.cpu().numpy()),
+                              dict(master=host.prev, m=host.buf), bitwise=True)
+    H.assert_sumsq(tag, ss.cpu().numpy(), ss_ref.reshape(-1))
+    lay.close()
