@@ -252,3 +252,14 @@ def test_every_path_is_independent_of_the_launch_shape(env, kind):
             assert torch.equal(a.view(torch.int16), b.view(torch.int16)), \
                 "%s differs at %d workgroups per CU" % (kind, bpc)
     lay.close()
+
+
+def test_hundreds_of_thousands_of_segments(env):
+    """300,000 segments of 1-8 elements: every tile straddles segments, and
+    the finalize folds 300,000 per-segment sums (clipped round, so the
+    whole-shard total too)."""
+    r = np.random.default_rng(27)
+    sizes = r.integers(1, 9, 300_000)
+    flags = r.integers(0, 2, sizes.size).astype(np.uint8)
+    w = W.make_workload("many_many_segments", sizes, flags, R=2, G=2, A=2, max_grad_norm=0.01)
+    _parity(env, w, "300k segments")
