@@ -238,7 +238,7 @@ typedef struct {
                                 2R + 34 bytes per element instead of 4R + 26
                                 (faster for R >= 6).  Same results bit for
                                 bit.  Ignored without clipping and by
-                                fl_round_hsdp.                              */
+                                fl_round_hsdp with H > 1.                   */
 } fl_round_cfg;
 
 int fl_round(const fl_layout* layout, const fl_round_cfg* cfg, const uint16_t* const* grads,

@@ -740,6 +740,15 @@ int fl_round_hsdp(const fl_layout* layout, const fl_round_cfg* cfg, const fl_hsd
   if (n > 0 && (master == m || master == v || m == v)) return FL_ERR_INVALID;
   if (n > 0 && hc->H > 1 && (wire == working)) return FL_ERR_INVALID;
   if (seg_sumsq && (reinterpret_cast<uintptr_t>(seg_sumsq) & 3u)) return FL_ERR_ALIGN;
+  // the gradient scratch of a clipped step pays off only for the R-peer
+  // reduction, i.e. with one replica
+  float* g_scratch = (c.max_grad_norm > 0.f && hc->H == 1) ? c.grad_scratch : nullptr;
+  if (g_scratch) {
+    if ((rc = dev_ptr(g_scratch, n)) != FL_OK) return rc;
+    const void* others[] = {master, m, v, working};
+    for (const void* o : others)
+      if (n > 0 && o == g_scratch) return FL_ERR_INVALID;
+  }
   if (c.phase_events)
     for (int k = 0; k < c.A + 2; ++k)
       if (!c.phase_events[k]) return FL_ERR_INVALID;
@@ -760,7 +769,7 @@ int fl_round_hsdp(const fl_layout* layout, const fl_round_cfg* cfg, const fl_hsd
     const uint16_t* const* ga = grads + (size_t)a * (size_t)c.R;
     if (hc->H == 1) {
       rc = enqueue_local_step(layout, step_hparams(c, a), c.step0 + a, c.R, ga, c.grad_scale,
-                              master, m, v, working, ws, ss, st, c.max_grad_norm);
+                              master, m, v, working, ws, ss, st, c.max_grad_norm, g_scratch);
       continue;
     }
     // tier 1: the sharding group's reduction, in the bf16 wire format

@@ -361,6 +361,7 @@ def fl_round_hsdp(layout, cfg, hcfg, grads, replica_wires, wire, replicas, bcast
     replicas: G tensors/None (FedAvg member) or None; bcast_master: fp32
     tensor (non-member) or None."""
     n = layout.n
+    _check_cfg(layout, cfg)
     rc = lib().fl_round_hsdp(
         layout.handle, ctypes.byref(cfg), ctypes.byref(hcfg),
         _bufs(grads, cfg.A * cfg.R, n, 2, "grads"),

@@ -81,6 +81,28 @@ def test_one_replica_is_fl_fsdp(env):
     lay.close()
 
 
+def test_one_replica_clipped_with_scratch_is_fl_fsdp(env):
+    """With one replica, a clipped FL+HSDP round with the gradient scratch is
+    bitwise the clipped fl_round with the scratch."""
+    torch, P = env["torch"], env["P"]
+    w = _workload(70_001, 8, 1, 2, 1, seed=7)
+    lay = P.Layout(w.seg_offsets, w.seg_decay)
+    a, b = B.DeviceInputs(w), B.DeviceInputs(w)
+    sa = torch.empty(w.n, dtype=torch.float32, device="cuda")
+    sb = torch.empty_like(sa)
+    mk = lambda s: P.make_round_cfg(w.R, w.G, w.A, w.weights, w.hp,  # noqa: E731
+                                    self_group=w.self_group, grad_scale=w.grad_scale,
+                                    step0=w.step0, max_grad_norm=0.01, grad_scratch=s)
+    P.fl_round_hsdp(lay, mk(sa), P.make_hsdp_cfg(1, 0, 1.0, True), a.grads, None, None,
+                    a.replicas, None, a.master, a.m, a.v, a.working)
+    P.fl_round(lay, mk(sb), b.grads, b.replicas, b.master, b.m, b.v, b.working)
+    torch.cuda.synchronize()
+    for k in ("master", "m", "v", "working"):
+        assert torch.equal(getattr(a, k).view(torch.int16), getattr(b, k).view(torch.int16)), k
+    assert torch.equal(sa.view(torch.int32), sb.view(torch.int32)), "scratch not used alike"
+    lay.close()
+
+
 def test_wire_reduce_and_broadcast_receive(env):
     torch, P, orc = env["torch"], env["P"], env["orc"]
     w = _workload(123_457, 6, 2, 1, 0, seed=4)
