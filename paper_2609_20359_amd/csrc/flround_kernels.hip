@@ -406,10 +406,15 @@ __global__ void __launch_bounds__(kBlock) k_fedavg(const FedArgs a) {
 // up to kChunkPieces pieces of one segment; thread j folds pieces j, j+256,
 // ... (each piece's kWaves slots in order), then a wave64 butterfly and the 4
 // wave totals in order.  Stage 2: one thread per segment adds its chunks in
-// order (double per segment, and its float rounding if requested).  Stage 3
-// (whole-shard total, for clipping): one workgroup folds the segments.
+// order (double per segment, and its float rounding if requested); skipped
+// when every segment is one chunk.  Stage 3 (whole-shard total, for
+// clipping): one workgroup folds the segments.
+// DIRECT (every segment is a single chunk, so chunk c is segment c): the
+// chunk sum is the segment's total; write it, and its float rounding if
+// requested, in place of stage 2 (which would add it to 0.0: the same bits).
+template <bool DIRECT>
 __global__ void __launch_bounds__(kBlock) k_seg_chunks(const LayoutDev L, const double* partials,
-                                                       double* chunk_sums) {
+                                                       double* chunk_sums, float* out) {
   __shared__ double red[4];
   for (int64_t c = blockIdx.x; c < L.n_chunks; c += gridDim.x) {
     const int64_t p0 = L.chunk_p0[c];
@@ -426,7 +431,11 @@ __global__ void __launch_bounds__(kBlock) k_seg_chunks(const LayoutDev L, const 
     acc = wave_sum(acc);
     if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = acc;
     __syncthreads();
-    if (threadIdx.x == 0) chunk_sums[c] = ((red[0] + red[1]) + red[2]) + red[3];
+    if (threadIdx.x == 0) {
+      const double sum = ((red[0] + red[1]) + red[2]) + red[3];
+      chunk_sums[c] = sum;
+      if (DIRECT && out) out[c] = (float)sum;
+    }
     __syncthreads();
   }
 }
@@ -542,10 +551,19 @@ hipError_t launch_seg_finalize(const LayoutDev& L, const double* partials, doubl
                                double* seg_dbl, float* out, double* total, hipStream_t st) {
   if (L.n_seg == 0) return hipSuccess;
   const int g1 = (int)(L.n_chunks < 65535 ? L.n_chunks : 65535);
-  void* a1[] = {const_cast<LayoutDev*>(&L), &partials, &chunk_sums};
-  hipError_t e = hipLaunchKernel((const void*)k_seg_chunks, dim3((unsigned)g1), dim3(kBlock), a1,
-                                 0, st);
+  const bool direct = L.n_chunks == L.n_seg;
+  double* stage1 = direct ? seg_dbl : chunk_sums;
+  void* a1[] = {const_cast<LayoutDev*>(&L), &partials, &stage1, &out};
+  hipError_t e = hipLaunchKernel(direct ? (const void*)k_seg_chunks<true>
+                                        : (const void*)k_seg_chunks<false>,
+                                 dim3((unsigned)g1), dim3(kBlock), a1, 0, st);
   if (e != hipSuccess) return e;
+  if (direct) {
+    if (!total) return hipSuccess;
+    int64_t n_seg = L.n_seg;
+    void* a3[] = {&n_seg, &seg_dbl, &total};
+    return hipLaunchKernel((const void*)k_total, dim3(1), dim3(kBlock), a3, 0, st);
+  }
   const int64_t b2 = (L.n_seg + kBlock - 1) / kBlock;
   const int g2 = (int)(b2 < 65535 ? b2 : 65535);
   void* a2[] = {const_cast<LayoutDev*>(&L), &chunk_sums, &seg_dbl, &out};
