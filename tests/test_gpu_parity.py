@@ -95,6 +95,7 @@ def test_round_stress_shaped_small(env):
 @pytest.mark.parametrize("n,R,G,A", [
     (1, 1, 1, 1), (7, 3, 2, 1), (8, 2, 3, 2), (9, 5, 1, 1), (2047, 4, 4, 1), (2048, 8, 8, 1),
     (2049, 16, 16, 1), (6143, 17, 17, 2), (100_003, 6, 5, 3), (262_147, 64, 64, 1),
+    (5003, 2, 2, 32),
 ])
 def test_round_ragged_shapes(env, n, R, G, A):
     r = np.random.default_rng(n + 31 * R + 7 * G)
