@@ -51,3 +51,28 @@ def test_sampled_oracle_matches_whole_shard(orc, clip, outer):
         host2 = B.HostInputs(w, idx)
         H.oracle_round(orc, w, host2, seg_off=off, seg_decay=dec)
         assert not np.array_equal(host2.master, host.master)
+
+
+@pytest.mark.parametrize("threads", [2, 5])
+def test_oracle_in_concurrent_chunks_matches_one_pass(orc, threads):
+    """The oracle run as contiguous chunks on several threads at once (as the
+    benchmark's CPU baseline runs it) gives the whole-shard pass's state bit
+    for bit: the path is elementwise, so the thread count changes nothing."""
+    from concurrent.futures import ThreadPoolExecutor
+
+    w = _workload(0.0, outer=W.DILOCO_OUTER)
+    whole = B.HostInputs(w)
+    H.oracle_round(orc, w, whole)
+    bounds = np.linspace(0, w.n, threads + 1).astype(np.int64)
+    parts = []
+    for t in range(threads):
+        lo, hi = int(bounds[t]), int(bounds[t + 1])
+        inner = w.seg_offsets[(w.seg_offsets > lo) & (w.seg_offsets < hi)]
+        off = np.concatenate([[lo], inner, [hi]]).astype(np.int64) - lo
+        first = int(np.searchsorted(w.seg_offsets, lo, side="right")) - 1
+        parts.append((B.HostInputs(w, span=(lo, hi)), off, w.seg_decay[first:first + off.size - 1]))
+    with ThreadPoolExecutor(threads) as ex:
+        list(ex.map(lambda p: H.oracle_round(orc, w, p[0], seg_off=p[1], seg_decay=p[2]), parts))
+    for name in ("master", "m", "v", "working", "prev", "buf"):
+        got = np.concatenate([getattr(p[0], name) for p in parts])
+        assert np.array_equal(got, getattr(whole, name)), name
