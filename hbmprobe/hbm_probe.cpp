@@ -238,6 +238,19 @@ int main(int argc, char** argv) {
   run<4, 2, 1, 1>("fedopt_G4", s, cus, elems);
   run<2, 0, 1, 1>("bcast", s, cus, elems);
   run_tiled(s, cus, elems);
+
+  // the runtime's own device-to-device copy of one fp32 stream, as a vendor
+  // reference point for the copy pattern (bytes read + written)
+  {
+    void* src = static_cast<void*>(s.rmw[0]);
+    void* dst = static_cast<void*>(s.wr[0]);
+    const size_t bytes = (size_t)elems * 4;
+    const float ms =
+        time_ms([&] { CK(hipMemcpyAsync(dst, src, bytes, hipMemcpyDeviceToDevice, 0)); }, 5);
+    const double gbs = 2.0 * (double)bytes / (ms * 1e-3) / 1e9;
+    std::printf("\nhipMemcpyAsync device to device, %zu bytes: %.3f ms, %.1f GB/s moved "
+                "(%.1f %% of peak)\n", bytes, ms, gbs, 100.0 * gbs / 8000.0);
+  }
   for (void* p : bufs) CK(hipFree(p));
   return 0;
 }
