@@ -78,7 +78,8 @@ def round_kernels(w):
     ks = []
     r = w.H if w.H > 1 else w.R
     if w.H > 1:
-        ks.append(("k_step<%d, 3, false>" % _rt(w.R), 2 * w.R * n, 2 * n))
+        wire = "k_wire<%d>" % w.R if _rt(w.R) else "k_step<0, 3, false>"
+        ks.append((wire, 2 * w.R * n, 2 * n))
     if w.max_grad_norm > 0 and w.H == 1 and w.clip_scratch:
         ks.append(("k_step<%d, 1, true>" % _rt(w.R), 2 * w.R * n, 4 * n))
         ks.append(("k_step<1, 2, false>", 16 * n, 14 * n))
@@ -214,7 +215,7 @@ def step_label(w):
                                          "per-segment sums")
     parts = []
     if w.H > 1:
-        parts.append("k_step<R=%d, wire>" % w.R)
+        parts.append("k_wire<R=%d>" % w.R)
     if w.max_grad_norm > 0:
         parts.append("k_step<%s=%d, sum of squares> + finalize" % (
             "R" if w.H == 1 else "H", w.R if w.H == 1 else w.H))

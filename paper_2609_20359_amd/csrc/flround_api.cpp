@@ -43,7 +43,11 @@ int sumsq_blocks_per_cu(int R) {
   return R >= 8 ? 2 : R >= 4 ? 3 : R == 3 ? 4 : R == 2 ? 6 : 8;
 }
 int reduce_blocks_per_cu(int R) { return R >= 8 ? 1 : 2; }
-int wire_blocks_per_cu(int R) { return R >= 8 ? 1 : R >= 2 ? 2 : 4; }
+int wire_blocks_per_cu(int R) {
+  const bool two_vector_kernel = R == 1 || R == 2 || R == 4 || R == 8 || R == 16;
+  if (two_vector_kernel) return R <= 2 ? 2 : 1;
+  return R >= 8 ? 1 : 2;
+}
 
 constexpr uint64_t kFnvOffset = 0xCBF29CE484222325ULL;
 constexpr uint64_t kFnvPrime = 0x100000001B3ULL;

@@ -319,6 +319,57 @@ __global__ void __launch_bounds__(kBlock) k_step(const StepArgs a) {
   }
 }
 
+// Reduction to the bf16 wire format with compile-time R (MODE 3 of k_step
+// for other R).  It needs no segment data, so it strides over 8-element
+// vectors and takes two per thread per iteration, issuing all 2R loads before
+// the arithmetic of either: a read-mostly pass needs that many loads in
+// flight to cover HBM latency at one workgroup per CU.  Same arithmetic and
+// bits as MODE 3.
+template <int RT>
+__global__ void __launch_bounds__(kBlock) k_wire(const StepArgs a) {
+  const int64_t nvec = (a.L.n + kVec - 1) / kVec;
+  const int64_t stride = (int64_t)gridDim.x * kBlock;
+  for (int64_t v0 = (int64_t)blockIdx.x * kBlock + threadIdx.x; v0 < nvec; v0 += 2 * stride) {
+    const int64_t v1 = v0 + stride;
+    const int64_t b0 = v0 * kVec, b1 = v1 * kVec;
+    if (b1 + kVec <= a.L.n) {  // both vectors full (b0 < b1)
+      u32x4 w0[RT], w1[RT];
+#pragma unroll
+      for (int r = 0; r < RT; ++r) w0[r] = ld_once(reinterpret_cast<const u32x4*>(a.grads[r] + b0));
+#pragma unroll
+      for (int r = 0; r < RT; ++r) w1[r] = ld_once(reinterpret_cast<const u32x4*>(a.grads[r] + b1));
+      float g0[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+      float g1[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int r = 0; r < RT; ++r) add_bf16x8(g0, w0[r]);
+#pragma unroll
+      for (int r = 0; r < RT; ++r) add_bf16x8(g1, w1[r]);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        g0[e] = g0[e] * a.grad_scale;
+        g1[e] = g1[e] * a.grad_scale;
+      }
+      st(reinterpret_cast<u32x4*>(a.wire_out + b0), pack_bf16x8(g0));
+      st(reinterpret_cast<u32x4*>(a.wire_out + b1), pack_bf16x8(g1));
+      continue;
+    }
+    for (int k = 0; k < 2; ++k) {  // the last vectors of the shard
+      const int64_t vi = k == 0 ? v0 : v1;
+      if (vi >= nvec) break;
+      const int64_t base = vi * kVec;
+      const int64_t left = a.L.n - base;
+      float g[8];
+      if (left >= kVec) {
+        reduce_vec<RT>(a, base, g);
+        st(reinterpret_cast<u32x4*>(a.wire_out + base), pack_bf16x8(g));
+      } else {
+        reduce_tail(a, base, (int)left, g);
+        for (int e = 0; e < (int)left; ++e) a.wire_out[base + e] = (uint16_t)to_bf16(g[e]);
+      }
+    }
+  }
+}
+
 // FedAvg: master = sum_g w_g * f32(rep_g), ascending g; working = bf16(master).
 // OUTER: the outer optimiser step on that average instead:
 //   delta = prev - xbar; buf = mu * buf + delta;
@@ -517,7 +568,14 @@ hipError_t launch_reduce(const StepArgs& a, int grid, hipStream_t st) {
 }
 
 hipError_t launch_reduce_wire(const StepArgs& a, int grid, hipStream_t st) {
-  return dispatch_step<3, false>(a, grid, st);
+  switch (a.R) {
+    case 1: return launch((const void*)k_wire<1>, a, grid, st);
+    case 2: return launch((const void*)k_wire<2>, a, grid, st);
+    case 4: return launch((const void*)k_wire<4>, a, grid, st);
+    case 8: return launch((const void*)k_wire<8>, a, grid, st);
+    case 16: return launch((const void*)k_wire<16>, a, grid, st);
+    default: return dispatch_step<3, false>(a, grid, st);
+  }
 }
 
 hipError_t launch_bcast_recv(int64_t n, const float* recv, float* master, uint16_t* working,
