@@ -240,7 +240,6 @@ def cpu_baseline(w, n_sample):
 
     import numpy as np
 
-    import harness as H
     import oracle
     import synth.buffers as B
     from synth import host_threads
@@ -252,15 +251,12 @@ def cpu_baseline(w, n_sample):
     jobs = []
     for t in range(T):
         lo, hi = int(bounds[t]), int(bounds[t + 1])
-        inner = w.seg_offsets[(w.seg_offsets > lo) & (w.seg_offsets < hi)]
-        off = np.concatenate([[lo], inner, [hi]]).astype(np.int64) - lo
-        first = int(np.searchsorted(w.seg_offsets, lo, side="right")) - 1
-        dec = w.seg_decay[first:first + off.size - 1]
+        off, dec, _ = w.span_layout(lo, hi)
         jobs.append((B.HostInputs(w, span=(lo, hi)), off, dec))
 
     def run(job):
         host, off, dec = job
-        H.oracle_round(orc, w, host, seg_off=off, seg_decay=dec, want_sumsq=True)
+        oracle.workload_round(orc, w, host, seg_off=off, seg_decay=dec, want_sumsq=True)
 
     per_param = w.A * w.step_bytes_per_param() + w.fedavg_bytes_per_param()
     first = (copy.deepcopy(jobs[0][0]),) + jobs[0][1:]
@@ -290,6 +286,8 @@ def main():
     ap.add_argument("--workload", default="llama8b_s8")
     ap.add_argument("--cpu-sample", type=int, default=64 << 20)
     ap.add_argument("--no-cpu", action="store_true")
+    ap.add_argument("--blocks-per-cu", type=int, default=0,
+                    help="workgroups per CU for every kernel (0: the library's defaults)")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="first run one plain torch copy of MIB MiB (reference kernel of "
                          "known traffic for counter runs)")
@@ -319,14 +317,15 @@ def main():
     import synth.buffers as B
     from synth import workloads as W
 
-    sys.path.insert(0, os.path.join(ROOT, "tests"))
-    import harness as H
+    from paper_2609_20359_amd import runner
 
     if not torch.cuda.is_available():
         print("bench.py needs a GPU", file=sys.stderr)
         sys.exit(1)
     torch.cuda.set_device(0)
     P.lib()
+    if args.blocks_per_cu:
+        P.set_blocks_per_cu(args.blocks_per_cu)
     w = W.ALL[args.workload]()
     log("workload", w.describe())
     lay = P.Layout(w.seg_offsets, w.seg_decay)
@@ -352,20 +351,20 @@ def main():
     # step's reduced gradient (A x n_seg floats)
     seg_sumsq = torch.empty(w.A * w.n_seg, dtype=torch.float32, device="cuda")
     for i in range(Wm):
-        H.gpu_round(P, lay, w, dev, seg_sumsq=seg_sumsq,
-                    cfg=H.round_cfg(P, w, w.step0 + w.A * i, dev=dev))
+        runner.gpu_round(lay, w, dev, seg_sumsq=seg_sumsq,
+                         cfg=runner.round_cfg(w, w.step0 + w.A * i, dev=dev))
     torch.cuda.synchronize()
     log("warmup done (%d rounds)" % Wm)
 
-    cfgs = [H.round_cfg(P, w, w.step0 + w.A * (Wm + k), phase_events=events[k].handles, dev=dev)
-            for k in range(K)]
+    cfgs = [runner.round_cfg(w, w.step0 + w.A * (Wm + k), phase_events=events[k].handles,
+                             dev=dev) for k in range(K)]
     start = torch.cuda.Event(enable_timing=True)
     stop = torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     t_wall = time.perf_counter()
     start.record(stream)
     for k in range(K):
-        H.gpu_round(P, lay, w, dev, seg_sumsq=seg_sumsq, cfg=cfgs[k])
+        runner.gpu_round(lay, w, dev, seg_sumsq=seg_sumsq, cfg=cfgs[k])
     stop.record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t_wall

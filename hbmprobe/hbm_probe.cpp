@@ -24,19 +24,26 @@
 //              step's round-start model and momentum buffer)
 //   bcast      4 bytes read (two 2-byte streams), 1 fp32 and 1 bf16 stream
 //              written: the FL+HSDP broadcast receive
+//   rmw3       3 fp32 streams read and written in place: the optimiser state
+//              of the fused step alone
 //   step_R8_tiled  as step_R8, but the three fp32 state arrays interleaved per
 //              2048-element tile ([tile][master | m | v]), i.e. one 24 KB
 //              read-modify-write chunk per tile instead of three streams
-// each with plain and nontemporal stores, for 1, 2, 3, 4 and 8 workgroups per CU.
+// each with plain and nontemporal stores, for 1, 2, 3, 4 and 8 workgroups per CU
+// (or the one count given).
 // Buffers are sized for the given element count (default: the
 // 1,003,782,144-element shard of Llama-3.1-8B at S = 8; the S = 4 shard has
 // 2,007,564,288 elements and needs about 120 GB).
 //
-// usage: hbm_probe [elements]
+// usage: hbm_probe [elements [pattern[,pattern...] [workgroups per CU]]]
+//   with a pattern list only those patterns run (the runtime copy line is
+//   printed only without a list); a counter run names one pattern and one
+//   workgroup count so that every dispatch of the run is that pattern.
 #include <hip/hip_runtime.h>
 
 #include <cstdio>
 #include <cstdlib>
+#include <string>
 #include <vector>
 
 typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
@@ -52,6 +59,17 @@ typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
 
 template <typename F>
 float time_ms(F launch, int reps);
+
+// Patterns and workgroup counts selected on the command line (empty: all).
+static std::vector<std::string> g_only;
+static std::vector<int> g_bpc = {1, 2, 3, 4, 8};
+
+static bool selected(const char* name) {
+  if (g_only.empty()) return true;
+  for (const std::string& o : g_only)
+    if (o == name) return true;
+  return false;
+}
 
 struct Streams {
   const u32x4* rd[12];  // read-only 16-byte streams, in units of u32x4
@@ -88,12 +106,13 @@ __global__ void __launch_bounds__(256) k_step_tiled(Streams s) {
 }
 
 void run_tiled(Streams s, int cus, long elems) {
+  if (!selected("step_R8_tiled")) return;
   const double bytes = (double)elems * 42.0;
   for (int nts = 0; nts < 2; ++nts) {
     double best = 0.0;
     int best_bpc = 0;
     std::printf("| %-9s | %-5s |", "step_R8_tiled", nts ? "nt" : "plain");
-    for (int bpc : {1, 2, 3, 4, 8}) {
+    for (int bpc : g_bpc) {
       const int grid = bpc * cus;
       float ms = nts ? time_ms([&] { k_step_tiled<true><<<grid, 256>>>(s); }, 5)
                      : time_ms([&] { k_step_tiled<false><<<grid, 256>>>(s); }, 5);
@@ -175,12 +194,13 @@ float time_ms(F launch, int reps) {
 
 template <int NRD, int NRMW, int NWH, int NWF>
 void run(const char* name, Streams s, int cus, long elems) {
+  if (!selected(name)) return;
   const double bytes = (double)elems * (2.0 * NRD + 8.0 * NRMW + 2.0 * NWH + 4.0 * NWF);
   for (int nts = 0; nts < 2; ++nts) {
     double best = 0.0;
     int best_bpc = 0;
     std::printf("| %-9s | %-5s |", name, nts ? "nt" : "plain");
-    for (int bpc : {1, 2, 3, 4, 8}) {
+    for (int bpc : g_bpc) {
       const int grid = bpc * cus;
       float ms = nts ? time_ms([&] { k_pattern<NRD, NRMW, NWH, NWF, true><<<grid, 256>>>(s); }, 5)
                      : time_ms([&] { k_pattern<NRD, NRMW, NWH, NWF, false><<<grid, 256>>>(s); }, 5);
@@ -200,6 +220,25 @@ void run(const char* name, Streams s, int cus, long elems) {
 int main(int argc, char** argv) {
   long elems = argc > 1 ? std::atol(argv[1]) : 1003782144L;
   elems -= elems % 8;
+  if (argc > 2) {
+    std::string list = argv[2];
+    size_t pos = 0;
+    while (pos <= list.size()) {
+      const size_t c = list.find(',', pos);
+      const std::string item = list.substr(pos, c == std::string::npos ? std::string::npos : c - pos);
+      if (!item.empty()) g_only.push_back(item);
+      if (c == std::string::npos) break;
+      pos = c + 1;
+    }
+  }
+  if (argc > 3) {
+    const int b = std::atoi(argv[3]);
+    if (b < 1 || b > 16) {
+      std::printf("workgroups per CU must be 1..16\n");
+      return 2;
+    }
+    g_bpc = {b};
+  }
   int cus = 0;
   CK(hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, 0));
   hipDeviceProp_t prop;
@@ -221,8 +260,11 @@ int main(int argc, char** argv) {
   std::printf("# HBM ceiling probe: %s, %d CUs, %ld-element streams\n\n", prop.gcnArchName, cus,
               elems);
   std::printf("GB/s by workgroups per CU; bytes = bytes the pattern moves; peak 8000 GB/s.\n\n");
-  std::printf("| pattern | stores | 1/CU | 2/CU | 3/CU | 4/CU | 8/CU | best | of peak |\n");
-  std::printf("|---|---|---|---|---|---|---|---|---|\n");
+  std::printf("| pattern | stores |");
+  for (int b : g_bpc) std::printf(" %d/CU |", b);
+  std::printf(" best | of peak |\n|---|---|");
+  for (size_t k = 0; k < g_bpc.size(); ++k) std::printf("---|");
+  std::printf("---|---|\n");
   run<1, 0, 0, 0>("read1", s, cus, elems);
   run<0, 0, 1, 0>("write1", s, cus, elems);
   run<1, 0, 1, 0>("copy", s, cus, elems);
@@ -237,11 +279,12 @@ int main(int argc, char** argv) {
   run<4, 0, 1, 1>("fedavg_G4", s, cus, elems);
   run<4, 2, 1, 1>("fedopt_G4", s, cus, elems);
   run<2, 0, 1, 1>("bcast", s, cus, elems);
+  run<0, 3, 0, 0>("rmw3", s, cus, elems);
   run_tiled(s, cus, elems);
 
   // the runtime's own device-to-device copy of one fp32 stream, as a vendor
   // reference point for the copy pattern (bytes read + written)
-  {
+  if (g_only.empty()) {
     void* src = static_cast<void*>(s.rmw[0]);
     void* dst = static_cast<void*>(s.wr[0]);
     const size_t bytes = (size_t)elems * 4;

@@ -95,27 +95,28 @@ def _ptr_array(arrays):
     return (ctypes.c_void_p * len(arrays))(*[a.ctypes.data for a in arrays])
 
 
-_keep = []
-
-
-def _lr_ptr(step_lr, A):
+def _lr_arr(step_lr, A):
+    """The per-step learning rates as a float32 array (or None); the caller
+    holds it for the duration of the oracle call."""
     if step_lr is None:
         return None
     a = np.ascontiguousarray(step_lr, dtype=np.float32)
     assert a.size == A, "step_lr needs one value per local step"
-    _keep.append(a)
-    del _keep[:-4]
-    return a.ctypes.data
+    return a
 
 
-def _tot_ptr(totals, A):
+def _tot_arr(totals, A):
+    """The per-step whole-shard sums of squares as a float64 array (or
+    None); the caller holds it for the duration of the oracle call."""
     if totals is None:
         return None
     a = np.ascontiguousarray(totals, dtype=np.float64)
     assert a.size == A, "clip_totals needs one value per local step"
-    _keep.append(a)
-    del _keep[:-4]
-    return a.ctypes.data
+    return a
+
+
+def _ptr(a):
+    return None if a is None else a.ctypes.data
 
 
 def hparams(hp):
@@ -222,6 +223,7 @@ class Oracle:
         w = _c(weights if weights is not None else [1.0], np.float32)
         bc = None if bcast is None else _c(bcast, np.float32)
         h = hparams(hp)
+        lr_a, tot_a = _lr_arr(step_lr, A), _tot_arr(clip_totals, A)
         ss = np.empty(A * n_seg, np.float64) if want_sumsq else None
         rc = self.L.orc_round_hsdp(n_seg, seg_off.ctypes.data, seg_decay.ctypes.data, R, H, replica,
                                    hsdp_scale, 1 if member else 0, G, A, self_group, grad_scale,
@@ -230,8 +232,8 @@ class Oracle:
                                    _ptr_array(reps) if reps else None,
                                    None if bc is None else bc.ctypes.data, master.ctypes.data,
                                    m.ctypes.data, v.ctypes.data, working.ctypes.data,
-                                   None if ss is None else ss.ctypes.data, _lr_ptr(step_lr, A),
-                                   max_grad_norm, _tot_ptr(clip_totals, A))
+                                   None if ss is None else ss.ctypes.data, _ptr(lr_a),
+                                   max_grad_norm, _ptr(tot_a))
         if rc:
             raise ValueError("orc_round_hsdp: %d" % rc)
         return None if ss is None else ss.reshape(A, n_seg)
@@ -262,14 +264,15 @@ class Oracle:
         w = _c(weights, np.float32)
         h = hparams(hp)
         o = outer(oh)
+        lr_a, tot_a = _lr_arr(step_lr, A), _tot_arr(clip_totals, A)
         ss = np.empty(A * n_seg, np.float64) if want_sumsq else None
         rc = self.L.orc_round_outer(n_seg, seg_off.ctypes.data, seg_decay.ctypes.data, R, G, A,
                                     self_group, grad_scale, ctypes.byref(h), step0, w.ctypes.data,
                                     ctypes.byref(o), _ptr_array(grads), _ptr_array(reps),
                                     prev.ctypes.data, buf.ctypes.data, master.ctypes.data,
                                     m.ctypes.data, v.ctypes.data, working.ctypes.data,
-                                    None if ss is None else ss.ctypes.data, _lr_ptr(step_lr, A),
-                                    max_grad_norm, _tot_ptr(clip_totals, A))
+                                    None if ss is None else ss.ctypes.data, _ptr(lr_a),
+                                    max_grad_norm, _ptr(tot_a))
         if rc:
             raise ValueError("orc_round_outer: %d" % rc)
         return None if ss is None else ss.reshape(A, n_seg)
@@ -302,13 +305,44 @@ class Oracle:
         reps = [working if r is None else _c(r, np.uint16) for r in replicas]
         w = _c(weights, np.float32)
         h = hparams(hp)
+        lr_a, tot_a = _lr_arr(step_lr, A), _tot_arr(clip_totals, A)
         ss = np.empty(A * n_seg, np.float64) if want_sumsq else None
         rc = self.L.orc_round(n_seg, seg_off.ctypes.data, seg_decay.ctypes.data, R, G, A,
                               self_group, grad_scale, ctypes.byref(h), step0, w.ctypes.data,
                               _ptr_array(grads), _ptr_array(reps), master.ctypes.data,
                               m.ctypes.data, v.ctypes.data, working.ctypes.data,
-                              None if ss is None else ss.ctypes.data, _lr_ptr(step_lr, A),
-                              max_grad_norm, _tot_ptr(clip_totals, A))
+                              None if ss is None else ss.ctypes.data, _ptr(lr_a),
+                              max_grad_norm, _ptr(tot_a))
         if rc:
             raise ValueError("orc_round: %d" % rc)
         return None if ss is None else ss.reshape(A, n_seg)
+
+
+def workload_round(orc, w, host, seg_off=None, seg_decay=None, want_sumsq=False,
+                   clip_totals=None, step_lr=None):
+    """Run the oracle round of workload w (FL+FSDP, FL+HSDP when w.H > 1, or
+    the outer step) in place on the host arrays of `host` (a
+    synth.buffers.HostInputs or a view of one).  seg_off / seg_decay: the
+    layout of the arrays held (default: the workload's whole shard).
+    clip_totals: per-step whole-shard sums of squares to clip against when
+    the arrays hold only part of the shard.  Returns the per-step
+    per-segment sums of squares (A x n_seg, double) or None."""
+    seg_off = w.seg_offsets if seg_off is None else seg_off
+    seg_decay = w.seg_decay if seg_decay is None else seg_decay
+    if w.outer is not None:
+        return orc.round_outer(seg_off, seg_decay, w.R, w.G, w.A, w.self_group, w.grad_scale,
+                               w.hp, w.step0, w.weights, w.outer, host.grads, host.replicas,
+                               host.prev, host.buf, host.master, host.m, host.v, host.working,
+                               want_sumsq=want_sumsq, max_grad_norm=w.max_grad_norm,
+                               clip_totals=clip_totals, step_lr=step_lr)
+    if w.H > 1:
+        return orc.round_hsdp(seg_off, seg_decay, w.R, w.H, w.replica, 1.0 / w.H, w.hsdp_member,
+                              w.G, w.A, w.self_group, w.grad_scale, w.hp, w.step0, w.weights,
+                              host.grads, host.replica_wires, host.replicas, host.bcast,
+                              host.master, host.m, host.v, host.working, want_sumsq=want_sumsq,
+                              max_grad_norm=w.max_grad_norm, clip_totals=clip_totals,
+                              step_lr=step_lr)
+    return orc.round(seg_off, seg_decay, w.R, w.G, w.A, w.self_group, w.grad_scale, w.hp,
+                     w.step0, w.weights, host.grads, host.replicas, host.master, host.m, host.v,
+                     host.working, want_sumsq=want_sumsq, max_grad_norm=w.max_grad_norm,
+                     clip_totals=clip_totals, step_lr=step_lr)

@@ -170,6 +170,14 @@ class Workload:
     def round_bytes(self):
         return self.n * (self.A * self.step_bytes_per_param() + self.fedavg_bytes_per_param())
 
+    def span_layout(self, lo, hi):
+        """The segments of elements lo..hi-1 as a layout of their own:
+        (offsets relative to lo, decay flags, index of the first segment)."""
+        inner = self.seg_offsets[(self.seg_offsets > lo) & (self.seg_offsets < hi)]
+        off = np.concatenate([[lo], inner, [hi]]).astype(np.int64) - lo
+        first = int(np.searchsorted(self.seg_offsets, lo, side="right")) - 1
+        return off, self.seg_decay[first:first + off.size - 1].copy(), first
+
     def describe(self):
         d = dict(workload=self.name, n=self.n, n_seg=self.n_seg, R=self.R, G=self.G,
                  A=self.A, distinct_grad_arrays=len(self.grad_specs))

@@ -44,43 +44,29 @@ def compact_layout(w: Workload, idx, full_segments=()):
 
 def oracle_round(orc, w: Workload, host: HostInputs, seg_off=None, seg_decay=None,
                  want_sumsq=False, clip_totals=None, step_lr=None):
-    """Run the oracle round (FL+FSDP, or FL+HSDP when w.H > 1) in place on host
-    arrays.  Returns the per-step per-segment sums of squares or None.
-    clip_totals: per-step whole-shard sums of squares to clip against when the
-    host arrays hold only a sample of the shard."""
-    seg_off = w.seg_offsets if seg_off is None else seg_off
-    seg_decay = w.seg_decay if seg_decay is None else seg_decay
-    if w.outer is not None:
-        return orc.round_outer(seg_off, seg_decay, w.R, w.G, w.A, w.self_group, w.grad_scale,
-                               w.hp, w.step0, w.weights, w.outer, host.grads, host.replicas,
-                               host.prev, host.buf, host.master, host.m, host.v, host.working,
-                               want_sumsq=want_sumsq, max_grad_norm=w.max_grad_norm,
-                               clip_totals=clip_totals, step_lr=step_lr)
-    if w.H > 1:
-        return orc.round_hsdp(seg_off, seg_decay, w.R, w.H, w.replica, 1.0 / w.H, w.hsdp_member,
-                              w.G, w.A, w.self_group, w.grad_scale, w.hp, w.step0, w.weights,
-                              host.grads, host.replica_wires, host.replicas, host.bcast,
-                              host.master, host.m, host.v, host.working, want_sumsq=want_sumsq,
-                              max_grad_norm=w.max_grad_norm, clip_totals=clip_totals,
-                              step_lr=step_lr)
-    return orc.round(seg_off, seg_decay, w.R, w.G, w.A, w.self_group, w.grad_scale, w.hp,
-                     w.step0, w.weights, host.grads, host.replicas, host.master, host.m, host.v,
-                     host.working, want_sumsq=want_sumsq, max_grad_norm=w.max_grad_norm,
-                     clip_totals=clip_totals, step_lr=step_lr)
+    """The oracle round of workload w in place on host arrays (see
+    oracle.workload_round)."""
+    import oracle
+
+    return oracle.workload_round(orc, w, host, seg_off=seg_off, seg_decay=seg_decay,
+                                 want_sumsq=want_sumsq, clip_totals=clip_totals,
+                                 step_lr=step_lr)
 
 
-def clip_totals(orc, w: Workload, chunk=1 << 24, say=None):
+def clip_totals(orc, w: Workload, chunk=1 << 24, say=None, fill=None):
     """Whole-shard sum of squares of each local step's reduced gradient, in
-    index order, one chunk of host-regenerated peer gradients at a time (for a
-    clipped round whose oracle sees only a sample of the shard)."""
+    index order, one chunk of regenerated peer gradients at a time (for a
+    clipped round whose oracle sees only part of the shard).  fill(spec, lo,
+    k): the k values from index lo (default: the host generator)."""
     assert w.H == 1, "the FL+HSDP clip norm is that of the replica average"
+    fill = host_fill if fill is None else fill
     steps = [tuple(w.grad_index[a * w.R:(a + 1) * w.R]) for a in range(w.A)]
     done = {}
     for key in dict.fromkeys(steps):
         acc = 0.0
         for c, lo in enumerate(range(0, w.n, chunk)):
             k = min(chunk, w.n - lo)
-            acc = orc.grad_total([host_fill(w.grad_specs[j], lo, k) for j in key],
+            acc = orc.grad_total([fill(w.grad_specs[j], lo, k) for j in key],
                                  w.grad_scale, acc)
             if say is not None and c % 16 == 15:
                 say("clip total: %d of %d elements" % (lo + k, w.n))
@@ -88,34 +74,111 @@ def clip_totals(orc, w: Workload, chunk=1 << 24, say=None):
     return [done[key] for key in steps]
 
 
+def _bits_equal(got, ref):
+    """Every element bitwise equal (a fast whole-array check; NaNs compare as
+    bits here, the detailed comparison below tolerates payload differences)."""
+    g, r = np.asarray(got), np.asarray(ref)
+    if g.shape != r.shape or g.dtype.itemsize != r.dtype.itemsize:
+        return False
+    u = np.uint32 if g.dtype.itemsize == 4 else np.uint16
+    return bool(np.array_equal(g.view(u), r.view(u)))
+
+
+def assert_state_parity_fast(tag, gpu, ref):
+    """assert_state_parity(bitwise=True) with a fast path: arrays that are
+    bitwise equal (the expected case) are not examined further; any other
+    array goes through the detailed comparison, which reports the errors and
+    raises unless only NaN payloads differ."""
+    slow = {k: gpu[k] for k in ref if not _bits_equal(gpu[k], ref[k])}
+    errs = {k: 0.0 for k in ("master", "m", "v") if k in ref}
+    if "working" in ref:
+        errs["working_ulp"] = 0
+    if slow:
+        errs.update(assert_state_parity(tag, slow, {k: ref[k] for k in slow}, bitwise=True))
+    return errs
+
+
+def whole_shard_parity(orc, w: Workload, state, ss_gpu, inputs, chunk=1 << 26, threads=None,
+                       clip_totals=None, say=None):
+    """Compare every element of a GPU round's result with the oracle.
+
+    state(name, lo, hi) -> host copy of the GPU's array `name` (master, m, v,
+    working; prev and buf with an outer step) over elements lo..hi-1;
+    ss_gpu: the GPU's A x n_seg sums of squares; inputs(lo, hi) -> the
+    HostInputs of that span.  Each chunk of `chunk` elements is split into
+    one contiguous sub-span per thread, each with the segments it holds as
+    its own layout, and the unchanged oracle runs on every sub-span (ctypes
+    releases the GIL; the oracle is elementwise, so sub-spans give the whole
+    shard's values).  While the oracle threads work on one chunk, the calling
+    thread fetches the next chunk's inputs.  master, m, v and working (and
+    the outer state) must be bitwise equal; each segment's sum of squares is
+    the sum of its pieces' oracle sums in index order, within TOL_SUMSQ_REL.
+    Returns the largest errors seen."""
+    from concurrent.futures import ThreadPoolExecutor
+
+    from synth import host_threads
+    from synth.buffers import HostView
+
+    T = threads or host_threads()
+    seg_acc = np.zeros((w.A, w.n_seg), np.float64)
+    worst = {}
+    starts = list(range(0, w.n, chunk))
+
+    def run(job):
+        view, off, dec, first = job
+        return first, oracle_round(orc, w, view, seg_off=off, seg_decay=dec, want_sumsq=True,
+                                   clip_totals=clip_totals)
+
+    with ThreadPoolExecutor(T) as ex:
+        nxt = inputs(starts[0], min(w.n, starts[0] + chunk)) if starts else None
+        for c, lo in enumerate(starts):
+            hi = min(w.n, lo + chunk)
+            host, nxt = nxt, None
+            bounds = np.linspace(0, hi - lo, T + 1).astype(np.int64)
+            jobs = []
+            for t in range(T):
+                a, b = int(bounds[t]), int(bounds[t + 1])
+                if b > a:
+                    off, dec, first = w.span_layout(lo + a, lo + b)
+                    jobs.append((HostView(host, a, b), off, dec, first))
+            futs = [ex.submit(run, j) for j in jobs]
+            got = {k: state(k, lo, hi) for k in ("master", "m", "v", "working")}
+            if w.outer is not None:
+                got_outer = dict(master=state("prev", lo, hi), m=state("buf", lo, hi))
+            if c + 1 < len(starts):
+                nxt = inputs(starts[c + 1], min(w.n, starts[c + 1] + chunk))
+            for f in futs:                                   # in index order
+                first, ss = f.result()
+                seg_acc[:, first:first + ss.shape[1]] += ss
+            ref = dict(master=host.master, m=host.m, v=host.v, working=host.working)
+            errs = assert_state_parity_fast("%s [%d, %d)" % (w.name, lo, hi), got, ref)
+            if w.outer is not None:
+                assert_state_parity_fast("%s outer state [%d, %d)" % (w.name, lo, hi), got_outer,
+                                         dict(master=host.prev, m=host.buf))
+            for k, e in errs.items():
+                worst[k] = max(worst.get(k, 0), e)
+            del host, got, ref
+            if say is not None:
+                say("chunk %d/%d: elements [%d, %d) bitwise equal" % (c + 1, len(starts), lo, hi))
+    worst["sumsq_rel"] = assert_sumsq(w.name, np.asarray(ss_gpu).reshape(w.A, w.n_seg), seg_acc)
+    return worst
+
+
 def round_cfg(P, w: Workload, step0=None, phase_events=None, dev=None, step_lr=None):
-    """The round configuration of workload w (with dev: its gradient scratch,
-    if the workload has one)."""
-    scratch = None if dev is None else getattr(dev, "grad_scratch", None)
-    return P.make_round_cfg(w.R, w.G, w.A, w.weights, w.hp, self_group=w.self_group,
-                            grad_scale=w.grad_scale, step0=w.step0 if step0 is None else step0,
-                            phase_events=phase_events, max_grad_norm=w.max_grad_norm,
-                            grad_scratch=scratch, step_lr=step_lr)
+    """The round configuration of workload w (P: the package, kept for the
+    callers' signature; see paper_2609_20359_amd.runner)."""
+    from paper_2609_20359_amd import runner
+
+    return runner.round_cfg(w, step0=step0, phase_events=phase_events, dev=dev, step_lr=step_lr)
 
 
 def gpu_round(P, layout, w: Workload, dev: DeviceInputs, seg_sumsq=None, phase_events=None,
               cfg=None):
-    """One fl_round (or fl_round_hsdp when w.H > 1) through the C ABI."""
-    if cfg is None:
-        cfg = round_cfg(P, w, phase_events=phase_events, dev=dev)
-    if w.outer is not None:
-        P.fl_round_outer(layout, cfg, w.outer, dev.grads, dev.replicas, dev.prev, dev.buf,
-                         dev.master, dev.m, dev.v, dev.working, seg_sumsq=seg_sumsq)
-    elif w.H > 1:
-        hc = P.make_hsdp_cfg(w.H, w.replica, 1.0 / w.H, w.hsdp_member)
-        P.fl_round_hsdp(layout, cfg, hc, dev.grads, dev.replica_wires, dev.wire,
-                        dev.replicas if w.hsdp_member else None,
-                        None if w.hsdp_member else dev.bcast, dev.master, dev.m, dev.v,
-                        dev.working, seg_sumsq=seg_sumsq)
-    else:
-        P.fl_round(layout, cfg, dev.grads, dev.replicas, dev.master, dev.m, dev.v, dev.working,
-                   seg_sumsq=seg_sumsq)
-    return cfg
+    """One fl_round (or fl_round_hsdp / fl_round_outer) through the C ABI."""
+    from paper_2609_20359_amd import runner
+
+    return runner.gpu_round(layout, w, dev, seg_sumsq=seg_sumsq, phase_events=phase_events,
+                            cfg=cfg)
 
 
 # ---- comparisons -----------------------------------------------------------

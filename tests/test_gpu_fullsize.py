@@ -1,11 +1,23 @@
 """GPU parity at the workloads' full sizes, in the launch configuration the
-benchmark uses: one fl_round on the whole shard, then the oracle on sampled
-elements (every segment's first and last two elements, the tail, all of a few
-short segments, and uniform random draws), plus properties that hold at any
-size.  Sampled inputs are regenerated on the host by the same counter-based
-generator; expected values come only from the oracle.  A clipped workload's
-coefficient depends on the whole shard, so the oracle first streams each
-step's whole-shard sum of squares over host-regenerated chunks."""
+benchmark uses: one round on the whole shard, then every element of the
+result compared with the oracle.
+
+The oracle runs chunk by chunk (64 Mi elements) on the host's threads.  Each
+chunk's inputs are the generator's values for that span: produced by the
+generator's device build into a scratch tensor that the library never
+touches, copied to the host, and spot-checked against the host build at
+random indices of every array of every chunk (the two builds evaluate one
+source; test_gpu_parity.test_generator_device_matches_host compares them
+element by element).  Expected values
+come only from the oracle.  A clipped round's coefficient depends on the
+whole shard, so the oracle first streams each step's whole-shard sum of
+squares the same way.
+
+Every test writes one progress line per chunk to gpurun_out/ so that a long
+comparison is visibly alive."""
+import os
+import time
+
 import numpy as np
 import pytest
 
@@ -17,10 +29,19 @@ pytestmark = pytest.mark.gpu
 
 WORKLOADS = ["llama8b_s8", "fedavg_heavy", "hsdp_s4", "stress", "hsdp_s4_h2", "hsdp_s4_h2_recv",
              "llama8b_s8_outer", "llama8b_s8_clip"]
+CHUNK = 1 << 26
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 
 
 def _say(*a):
-    print("[gpu-fullsize]", *a, flush=True)
+    msg = " ".join(str(x) for x in a)
+    print("[gpu-fullsize]", msg, flush=True)
+    try:
+        os.makedirs(os.path.join(ROOT, "gpurun_out"), exist_ok=True)
+        with open(os.path.join(ROOT, "gpurun_out", "progress_fullsize.log"), "a") as f:
+            f.write("%s %s\n" % (time.strftime("%H:%M:%S"), msg))
+    except OSError:
+        pass
 
 
 @pytest.fixture(scope="module")
@@ -36,11 +57,13 @@ def env():
     return dict(torch=torch, P=P, orc=oracle.Oracle())
 
 
+@pytest.mark.timeout(900)
 @pytest.mark.parametrize("name", WORKLOADS)
-def test_full_size_round_sampled(env, name):
-    _sampled_parity(env, W.ALL[name](), name)
+def test_full_size_round_whole_shard(env, name):
+    _whole_shard(env, W.ALL[name](), name)
 
 
+@pytest.mark.timeout(900)
 def test_beyond_int32_element_indices(env):
     """2^31 + 2053 elements: indices past the int32 range, a segment boundary
     3 elements past 2^31 (inside a tile), a 5-element ragged tail, and a
@@ -49,10 +72,10 @@ def test_beyond_int32_element_indices(env):
     cuts = [0, 1 << 30, (1 << 31) - 700, (1 << 31) + 3, n]
     w = W.make_workload("beyond_int32", np.diff(cuts), [1, 0, 1, 1], R=2, G=2, A=1, step0=3,
                         weights=np.array([1.0, 3.0], np.float32))
-    _sampled_parity(env, w, "beyond_int32")
+    _whole_shard(env, w, "beyond_int32")
 
 
-def _sampled_parity(env, w, name):
+def _whole_shard(env, w, name):
     torch, P, orc = env["torch"], env["P"], env["orc"]
     _say(name, w.describe())
     lay = P.Layout(w.seg_offsets, w.seg_decay)
@@ -61,38 +84,30 @@ def _sampled_parity(env, w, name):
     H.gpu_round(P, lay, w, dev, seg_sumsq=ss)
     torch.cuda.synchronize()
     _say(name, "gpu round done")
-
-    # properties at full size
-    assert torch.equal(dev.master.to(torch.bfloat16).view(torch.int16),
-                       dev.working.view(torch.int16)), "working != bf16(master)"
-    for t in (dev.master, dev.m, dev.v):
-        assert bool(torch.isfinite(t).all()), "non-finite state"
-    assert bool((dev.v >= 0).all()), "negative second moment"
+    ss_gpu = ss.cpu().numpy()
     assert bool((ss >= 0).all()), "negative or unwritten per-segment sum of squares"
+    lay.close()
 
-    idx, full = W.sample_indices(w, n_random=1 << 16)
-    idx_dev = torch.from_numpy(idx).cuda()
-    got = dict(master=H.gather_f32(dev.master, idx_dev), m=H.gather_f32(dev.m, idx_dev),
-               v=H.gather_f32(dev.v, idx_dev), working=H.gather_u16(dev.working, idx_dev))
+    # keep only the results; the inputs are regenerated per chunk
+    keep = dict(master=dev.master, m=dev.m, v=dev.v, working=dev.working)
     if w.outer is not None:
-        got_outer = dict(master=H.gather_f32(dev.prev, idx_dev), m=H.gather_f32(dev.buf, idx_dev))
-    ss_gpu = ss.cpu().numpy().reshape(w.A, w.n_seg)
+        keep.update(prev=dev.prev, buf=dev.buf)
     del dev
     torch.cuda.empty_cache()
 
-    totals = H.clip_totals(orc, w, say=lambda m: _say(name, m)) if w.max_grad_norm > 0 else None
-    if totals is not None:
+    def state(k, lo, hi):
+        t = keep[k][lo:hi]
+        return H.to_u16(t) if k == "working" else t.cpu().numpy()
+
+    filler = B.DeviceSpanFiller(min(CHUNK, w.n))
+    totals = None
+    if w.max_grad_norm > 0:
+        totals = H.clip_totals(orc, w, chunk=CHUNK, say=lambda m: _say(name, m),
+                               fill=lambda sp, lo, k: filler.fill(sp, lo, lo + k))
         _say(name, "clip coefficients", [orc.clip_coef(t, w.max_grad_norm) for t in totals[:1]])
-    host = B.HostInputs(w, idx)
-    off, dec, cmap = H.compact_layout(w, idx, full)
-    ss_ref = H.oracle_round(orc, w, host, seg_off=off, seg_decay=dec, want_sumsq=True,
-                            clip_totals=totals)
-    ref = dict(master=host.master, m=host.m, v=host.v, working=host.working)
-    errs = H.assert_state_parity(name, got, ref, bitwise=True)
-    if w.outer is not None:
-        H.assert_state_parity(name + " outer state", got_outer,
-                              dict(master=host.prev, m=host.buf), bitwise=True)
-    for s, cs in cmap.items():
-        H.assert_sumsq("%s seg %d" % (name, s), ss_gpu[:, s], ss_ref[:, cs])
-    lay.close()
-    _say(name, "ok: %d sampled elements, %d full segments, errors %s" % (idx.size, len(cmap), errs))
+    t0 = time.time()
+    worst = H.whole_shard_parity(orc, w, state, ss_gpu, lambda lo, hi: filler.host_inputs(w, lo, hi),
+                                 chunk=CHUNK, clip_totals=totals, say=lambda m: _say(name, m))
+    _say(name, "ok: all %d elements bitwise equal to the oracle (%.1f s; %d generator values "
+         "spot-checked against the host build); largest errors %s"
+         % (w.n, time.time() - t0, filler.checked, worst))
