@@ -85,9 +85,17 @@ int fl_version(void);
  *   for n == 0); seg_offsets: host array of n_seg + 1 values, [0] == 0,
  *   strictly increasing, [n_seg] == n; seg_decay: host array of n_seg flags,
  *   or NULL for "every segment decays".  Uploads small per-segment and
- *   per-tile tables (about 16 bytes per 2048 elements) to the current device;
- *   returns FL_ERR_NOMEM / FL_ERR_HIP if that fails.  *out receives an
- *   immutable handle that may be used from several streams at once.
+ *   per-tile tables (about 16 bytes per 2048 elements) to the current device,
+ *   and allocates the workspace of the per-segment sums of squares (32 bytes
+ *   per (2048-element tile, segment) pair, plus 8 per segment; zeroed once);
+ *   returns FL_ERR_NOMEM / FL_ERR_HIP if that fails.  *out receives a handle
+ *   that may be used from several streams at once.
+ *   The workspace serves the calls of one stream at a time: a call that needs
+ *   it (seg_sumsq given, or clipping) uses it when it is free and the last
+ *   call that used it was on the same stream (the two are then ordered);
+ *   otherwise -- another stream, two host threads at once, or a stream being
+ *   captured into a HIP graph -- the call takes a stream-ordered temporary of
+ *   the same size instead, allocated and freed on its stream.
  * fl_layout_destroy: frees the handle and its device tables (NULL is OK).
  *   The caller must ensure no enqueued call still uses it.
  * ---------------------------------------------------------------------- */
@@ -125,9 +133,11 @@ typedef struct {
  * grad_out: device pointer, N floats (must not overlap an input).
  * seg_sumsq: NULL, or device pointer to n_seg floats receiving, per segment,
  *   the sum of grad_out[i]^2 (exact double squares, fixed-tree double sums,
- *   rounded once to float): per-layer gradient-norm telemetry.  Needs a stream-ordered temporary of
- *   32 bytes per (2048-element tile, segment) pair, allocated and freed on
- *   `stream`.
+ *   rounded once to float): per-layer gradient-norm telemetry.  Uses the
+ *   layout's workspace (see fl_layout_create).  When every segment spans at
+ *   most 1024 tiles and there are at most 8 segments, the workgroup of the
+ *   pass that finishes last computes the per-segment totals (the same fixed
+ *   trees, the same bits) in place of a separate finalize launch.
  * 1 <= R <= FL_MAX_PEERS; grad_scale finite.
  * ---------------------------------------------------------------------- */
 int fl_shard_reduce(const fl_layout* layout, int R, const uint16_t* const* peer_grads,
@@ -203,9 +213,11 @@ int fl_fedavg(const fl_layout* layout, int G, const uint16_t* const* replicas,
  *   place and pairwise distinct.
  * seg_sumsq: NULL, or device pointer to A*n_seg floats (row a = local step a;
  *   see fl_shard_reduce).
- * Allocation: with seg_sumsq or max_grad_norm > 0 the round takes one
- *   stream-ordered temporary (as fl_shard_reduce) for all its steps;
- *   otherwise it allocates nothing and may be captured in a HIP graph.
+ * Allocation: with seg_sumsq or max_grad_norm > 0 the round uses the
+ *   layout's workspace for all its steps, or one stream-ordered temporary
+ *   when that is not available to this stream (see fl_layout_create); under
+ *   graph capture the temporary becomes a graph allocation.  Without them it
+ *   allocates nothing.
  * Configuration: 1 <= R <= FL_MAX_PEERS, 1 <= G <= FL_MAX_GROUPS, A >= 1,
  *   0 <= self_group < G, step0 >= 1, grad_scale finite, h and weights as
  *   above, replica_fp as in fl_fedavg, step_lr entries finite and >= 0,

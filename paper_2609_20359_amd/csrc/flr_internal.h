@@ -12,6 +12,7 @@ constexpr int kVec = 8;                // elements per thread per tile (16 B of 
 constexpr int kTile = kBlock * kVec;   // elements per tile: 2048
 constexpr int kWaves = kBlock / 64;    // wave64s per workgroup: one partial slot each
 constexpr int kChunkPieces = 1024;    // pieces folded by one workgroup in the finalize
+constexpr int kFoldMaxChunks = 8;     // finalize folded into the pass up to this many chunks
 constexpr int kMaxPeers = 64;
 constexpr int kMaxGroups = 64;
 
@@ -70,6 +71,15 @@ struct StepArgs {
                        // (null: not requested)
   const double* clip_total;  // MODE 0: whole-shard sum of squares, clipping on
   float clip_max;            // its max norm
+  // Finalize folded into the pass (null: separate finalize kernels).  Only
+  // for layouts whose every segment is one finalize chunk and that have at
+  // most kFoldMaxChunks of them.  fold_counter must read 0 when the pass
+  // starts; the workgroup that finishes last folds the partials exactly as
+  // k_seg_chunks and k_total do and sets it back to 0.
+  unsigned* fold_counter;
+  double* fold_seg;     // n_seg doubles: per-segment totals
+  float* fold_out;      // n_seg floats (may be null)
+  double* fold_total;   // whole-shard total (may be null)
 };
 
 struct FedArgs {

@@ -21,11 +21,21 @@
 using flr::kTile;
 
 struct fl_layout {
-  int device;
-  int num_cus;
-  uint64_t fingerprint;
-  void* dev_mem;  // one allocation holding all device tables
-  flr::LayoutDev L;
+  int device = 0;
+  int num_cus = 0;
+  uint64_t fingerprint = 0;
+  void* dev_mem = nullptr;  // one allocation holding all device tables
+  flr::LayoutDev L{};
+  // Workspace of the per-segment sums of squares (see Workspace below),
+  // allocated with the layout and zeroed once.  It serves the calls of one
+  // stream at a time: the stream of the last call that used it (ws_stream,
+  // its kernels followed by ws_done); a call on another stream, or one being
+  // captured into a graph, takes a stream-ordered allocation of its own.
+  void* ws_mem = nullptr;
+  std::atomic<bool> ws_busy{false};
+  hipStream_t ws_stream = nullptr;
+  hipEvent_t ws_done = nullptr;
+  bool ws_recorded = false;
 };
 
 namespace {
@@ -158,8 +168,15 @@ int check_device(const fl_layout* lay) {
   return dev == lay->device ? FL_OK : FL_ERR_DEVICE;
 }
 
+// Workgroups of a pass over `units` tiles or vector groups: a grid-stride
+// loop over a grid of bpc workgroups per CU; a shard whose units all fit on
+// the chip at once (at most kResidentPerCu per CU) gets one workgroup per unit
+// instead, so that a small shard is not spread over fewer workgroups than it
+// has tiles.  An explicit fl_set_blocks_per_cu applies to every pass.
+constexpr int kResidentPerCu = 4;
 int grid_for(const fl_layout* lay, int64_t units, int default_bpc = kDefaultBlocksPerCu) {
   const int set = g_blocks_per_cu.load(std::memory_order_relaxed);
+  if (set <= 0 && units <= (int64_t)kResidentPerCu * lay->num_cus) return (int)(units < 1 ? 1 : units);
   const int bpc = set > 0 ? set : default_bpc;
   int64_t cap = (int64_t)bpc * (int64_t)lay->num_cus;
   if (cap < 1) cap = 1;
@@ -187,36 +204,109 @@ int check_peers(int R, const uint16_t* const* peers, int64_t n) {
   return FL_OK;
 }
 
-// Stream-ordered temporary for the per-segment sums of squares: the
-// (piece, wave) partials (kWaves doubles per piece), one double per finalize
-// chunk, one per segment, and the whole-shard total.
+// Workspace of the per-segment sums of squares: the (piece, wave) partials
+// (kWaves doubles per piece), one double per finalize chunk, one per segment,
+// the whole-shard total, and the counter of a finalize folded into the pass.
+size_t ws_slots(const flr::LayoutDev& L) {
+  return (size_t)(L.n_pieces > 0 ? L.n_pieces : 1) * flr::kWaves;
+}
+size_t ws_bytes(const flr::LayoutDev& L) {
+  const size_t nch = (size_t)(L.n_chunks > 0 ? L.n_chunks : 1);
+  const size_t nseg = (size_t)(L.n_seg > 0 ? L.n_seg : 1);
+  return (ws_slots(L) + nch + nseg + 1 + 1) * sizeof(double);
+}
+
 struct Workspace {
   double* p = nullptr;
   double* chunks = nullptr;
   double* seg = nullptr;
   double* total = nullptr;
+  unsigned* counter = nullptr;  // null: no folded finalize
   hipStream_t st = nullptr;
-  int alloc(const flr::LayoutDev& L, hipStream_t stream) {
+  fl_layout* owner = nullptr;   // the layout whose workspace this is (or null)
+  void* own = nullptr;          // a stream-ordered allocation of this call
+
+  void carve(const flr::LayoutDev& L, void* mem) {
+    p = static_cast<double*>(mem);
+    chunks = p + ws_slots(L);
+    seg = chunks + (L.n_chunks > 0 ? L.n_chunks : 1);
+    total = seg + (L.n_seg > 0 ? L.n_seg : 1);
+    counter = reinterpret_cast<unsigned*>(total + 1);
+  }
+
+  // The layout's workspace when this stream may use it, else a stream-ordered
+  // allocation (without the fold counter, which would need zeroing).
+  int acquire(const fl_layout* layc, hipStream_t stream) {
+    fl_layout* lay = const_cast<fl_layout*>(layc);
     st = stream;
-    const size_t slots = (size_t)(L.n_pieces > 0 ? L.n_pieces : 1) * flr::kWaves;
-    const size_t nch = (size_t)(L.n_chunks > 0 ? L.n_chunks : 1);
-    const size_t nseg = (size_t)(L.n_seg > 0 ? L.n_seg : 1);
-    void* q = nullptr;
-    const hipError_t e = hipMallocAsync(&q, (slots + nch + nseg + 1) * sizeof(double), st);
-    if (e != hipSuccess) return status_of(e);
-    p = static_cast<double*>(q);
-    chunks = p + slots;
-    seg = chunks + nch;
-    total = seg + nseg;
+    hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
+    if (hipStreamIsCapturing(stream, &cs) != hipSuccess) return FL_ERR_HIP;
+    bool expected = false;
+    if (cs == hipStreamCaptureStatusNone && lay->ws_mem &&
+        lay->ws_busy.compare_exchange_strong(expected, true, std::memory_order_acquire)) {
+      if (!lay->ws_recorded || lay->ws_stream == stream) {
+        if (lay->ws_recorded && hipStreamWaitEvent(stream, lay->ws_done, 0) != hipSuccess) {
+          lay->ws_busy.store(false, std::memory_order_release);
+          return FL_ERR_HIP;
+        }
+        owner = lay;
+        carve(lay->L, lay->ws_mem);
+        return FL_OK;
+      }
+      lay->ws_busy.store(false, std::memory_order_release);
+    }
+    const hipError_t e = hipMallocAsync(&own, ws_bytes(lay->L), st);
+    if (e != hipSuccess) {
+      own = nullptr;
+      return status_of(e);
+    }
+    carve(lay->L, own);
+    counter = nullptr;
     return FL_OK;
   }
+
   int release() {
-    if (!p) return FL_OK;
-    const hipError_t e = hipFreeAsync(p, st);
+    int rc = FL_OK;
+    if (owner) {
+      if (hipEventRecord(owner->ws_done, st) == hipSuccess) {
+        owner->ws_stream = st;
+        owner->ws_recorded = true;
+      } else {
+        // the next call must not assume this one's kernels are ordered
+        owner->ws_recorded = true;
+        owner->ws_stream = nullptr;
+        rc = FL_ERR_HIP;
+      }
+      owner->ws_busy.store(false, std::memory_order_release);
+      owner = nullptr;
+    } else if (own) {
+      rc = status_of(hipFreeAsync(own, st));
+      own = nullptr;
+    }
     p = chunks = seg = total = nullptr;
-    return status_of(e);
+    counter = nullptr;
+    return rc;
   }
 };
+
+// Whether a pass with per-segment sums folds its finalize (every segment one
+// finalize chunk, few of them, and a zeroed counter to count workgroups).
+bool fold_ok(const flr::LayoutDev& L, const Workspace& ws) {
+  return ws.counter != nullptr && L.n_chunks == L.n_seg && L.n_chunks >= 1 &&
+         L.n_chunks <= flr::kFoldMaxChunks;
+}
+
+// Point a pass with per-segment sums at its finalize outputs: folded into the
+// pass when fold_ok, else left to launch_seg_finalize (returns false).
+bool set_fold(flr::StepArgs& a, const fl_layout* lay, const Workspace& ws, float* out,
+              bool total) {
+  if (!fold_ok(lay->L, ws)) return false;
+  a.fold_counter = ws.counter;
+  a.fold_seg = ws.seg;
+  a.fold_out = out;
+  a.fold_total = total ? ws.total : nullptr;
+  return true;
+}
 
 flr::StepArgs step_args(const fl_layout* lay) {
   flr::StepArgs a;
@@ -245,9 +335,10 @@ int enqueue_local_step(const fl_layout* lay, const fl_adamw_hparams& h, int64_t 
   if (clip_max > 0.f && g_scratch) {
     a.partials = ws.p;
     a.g_out = g_scratch;
+    const bool folded = set_fold(a, lay, ws, seg_sumsq, true);
     rc = status_of(flr::launch_reduce(a, grid_for(lay, lay->L.n_tiles, reduce_blocks_per_cu(R)),
                                       st));
-    if (rc == FL_OK)
+    if (rc == FL_OK && !folded)
       rc = status_of(flr::launch_seg_finalize(lay->L, ws.p, ws.chunks, ws.seg, seg_sumsq,
                                               ws.total, st));
     flr::StepArgs b = step_args(lay);
@@ -264,12 +355,14 @@ int enqueue_local_step(const fl_layout* lay, const fl_adamw_hparams& h, int64_t 
   }
   if (clip_max > 0.f) {
     a.partials = ws.p;
+    const bool folded = set_fold(a, lay, ws, seg_sumsq, true);
     rc = status_of(flr::launch_sumsq_only(a, grid_for(lay, lay->L.n_tiles,
                                                       sumsq_blocks_per_cu(R)), st));
-    if (rc == FL_OK)
+    if (rc == FL_OK && !folded)
       rc = status_of(flr::launch_seg_finalize(lay->L, ws.p, ws.chunks, ws.seg, seg_sumsq,
                                               ws.total, st));
     a.partials = nullptr;
+    a.fold_counter = nullptr;
     a.clip_total = ws.total;
     a.clip_max = clip_max;
     seg_sumsq = nullptr;
@@ -279,9 +372,13 @@ int enqueue_local_step(const fl_layout* lay, const fl_adamw_hparams& h, int64_t 
   a.m = m;
   a.v = v;
   a.working = working;
-  if (seg_sumsq) a.partials = ws.p;
+  bool folded = false;
+  if (seg_sumsq) {
+    a.partials = ws.p;
+    folded = set_fold(a, lay, ws, seg_sumsq, false);
+  }
   if (rc == FL_OK) rc = status_of(flr::launch_local_step(a, grid, st));
-  if (rc == FL_OK && seg_sumsq)
+  if (rc == FL_OK && seg_sumsq && !folded)
     rc = status_of(flr::launch_seg_finalize(lay->L, ws.p, ws.chunks, ws.seg, seg_sumsq, nullptr,
                                             st));
   return rc;
@@ -407,9 +504,8 @@ int fl_layout_create(int64_t n, int64_t n_seg, const int64_t* seg_offsets,
   std::vector<uint8_t> decay((size_t)n_seg);
   for (int64_t k = 0; k < n_seg; ++k) decay[(size_t)k] = (seg_decay == nullptr || seg_decay[k]) ? 1 : 0;
 
-  fl_layout* lay = new (std::nothrow) fl_layout;
+  fl_layout* lay = new (std::nothrow) fl_layout();
   if (!lay) return FL_ERR_NOMEM;
-  std::memset(lay, 0, sizeof *lay);
   if (hipGetDevice(&lay->device) != hipSuccess) {
     delete lay;
     return FL_ERR_HIP;
@@ -429,19 +525,31 @@ int fl_layout_create(int64_t n, int64_t n_seg, const int64_t* seg_offsets,
   lay->L.n_chunks = n_chunks;
 
   // One device allocation:
-  // [seg_off | seg_piece0 | seg_chunk0 | chunk_p0 | tiles | seg_decay].
+  // [seg_off | seg_piece0 | seg_chunk0 | chunk_p0 | tiles | seg_decay | workspace].
   const size_t b_off = sizeof(int64_t) * (size_t)(n_seg + 1);
   const size_t b_pp = sizeof(int64_t) * (size_t)(n_seg + 1);
   const size_t b_sc = sizeof(int64_t) * (size_t)(n_seg + 1);
   const size_t b_cp = sizeof(int64_t) * (size_t)(n_chunks + 1);
   const size_t b_tiles = sizeof(flr::TileInfo) * (size_t)n_tiles;
   const size_t b_dec = (size_t)n_seg;
-  const size_t total = b_off + b_pp + b_sc + b_cp + b_tiles + b_dec + 64;
+  const size_t b_tables = (b_off + b_pp + b_sc + b_cp + b_tiles + b_dec + 255) & ~(size_t)255;
+  const size_t b_ws = n > 0 ? ws_bytes(lay->L) : 0;
+  const size_t total = b_tables + b_ws + 64;
   void* mem = nullptr;
   hipError_t e = hipMalloc(&mem, total);
   if (e != hipSuccess) {
     delete lay;
     return status_of(e);
+  }
+  if (b_ws) {
+    e = hipMemset(static_cast<char*>(mem) + b_tables, 0, b_ws);
+    if (e == hipSuccess) e = hipEventCreateWithFlags(&lay->ws_done, hipEventDisableTiming);
+    if (e != hipSuccess) {
+      (void)hipFree(mem);
+      delete lay;
+      return status_of(e);
+    }
+    lay->ws_mem = static_cast<char*>(mem) + b_tables;
   }
   char* base = static_cast<char*>(mem);
   char* p_off = base;
@@ -457,6 +565,7 @@ int fl_layout_create(int64_t n, int64_t n_seg, const int64_t* seg_offsets,
   if (e == hipSuccess && b_tiles) e = hipMemcpy(p_tiles, tiles.data(), b_tiles, hipMemcpyHostToDevice);
   if (e == hipSuccess && b_dec) e = hipMemcpy(p_dec, decay.data(), b_dec, hipMemcpyHostToDevice);
   if (e != hipSuccess) {
+    if (lay->ws_done) (void)hipEventDestroy(lay->ws_done);
     (void)hipFree(mem);
     delete lay;
     return status_of(e);
@@ -479,6 +588,7 @@ int fl_layout_destroy(fl_layout* layout) {
     int cur = -1;
     (void)hipGetDevice(&cur);
     if (cur != layout->device) (void)hipSetDevice(layout->device);
+    if (layout->ws_done && hipEventDestroy(layout->ws_done) != hipSuccess) rc = FL_ERR_HIP;
     if (hipFree(layout->dev_mem) != hipSuccess) rc = FL_ERR_HIP;
     if (cur >= 0 && cur != layout->device) (void)hipSetDevice(cur);
   }
@@ -507,16 +617,17 @@ int fl_shard_reduce(const fl_layout* layout, int R, const uint16_t* const* peer_
   if (n == 0) return FL_OK;
   hipStream_t st = static_cast<hipStream_t>(stream);
   Workspace ws;
-  if (seg_sumsq && (rc = ws.alloc(layout->L, st)) != FL_OK) return rc;
+  if (seg_sumsq && (rc = ws.acquire(layout, st)) != FL_OK) return rc;
   flr::StepArgs a = step_args(layout);
   for (int r = 0; r < R; ++r) a.grads[r] = peer_grads[r];
   a.R = R;
   a.grad_scale = grad_scale;
   a.g_out = grad_out;
   a.partials = ws.p;
+  const bool folded = seg_sumsq && set_fold(a, layout, ws, seg_sumsq, false);
   rc = status_of(flr::launch_reduce(a, grid_for(layout, layout->L.n_tiles,
                                                 reduce_blocks_per_cu(R)), st));
-  if (rc == FL_OK && seg_sumsq)
+  if (rc == FL_OK && seg_sumsq && !folded)
     rc = status_of(flr::launch_seg_finalize(layout->L, ws.p, ws.chunks, ws.seg, seg_sumsq,
                                             nullptr, st));
   const int rc2 = ws.release();
@@ -565,7 +676,7 @@ int fl_local_step(const fl_layout* layout, const fl_adamw_hparams* h, int64_t st
   if (n == 0) return FL_OK;
   hipStream_t st = static_cast<hipStream_t>(stream);
   Workspace ws;
-  if (seg_sumsq && (rc = ws.alloc(layout->L, st)) != FL_OK) return rc;
+  if (seg_sumsq && (rc = ws.acquire(layout, st)) != FL_OK) return rc;
   rc = enqueue_local_step(layout, *h, step, R, peer_grads, grad_scale, master, m, v, working, ws,
                           seg_sumsq, st);
   const int rc2 = ws.release();
@@ -606,15 +717,17 @@ int fl_grad_sumsq(const fl_layout* layout, int R, const uint16_t* const* peer_gr
   hipStream_t st = static_cast<hipStream_t>(stream);
   if (n == 0) return status_of(flr::launch_zero_total(total_sumsq, st));
   Workspace ws;
-  if ((rc = ws.alloc(layout->L, st)) != FL_OK) return rc;
+  if ((rc = ws.acquire(layout, st)) != FL_OK) return rc;
   flr::StepArgs a = step_args(layout);
   for (int r = 0; r < R; ++r) a.grads[r] = peer_grads[r];
   a.R = R;
   a.grad_scale = grad_scale;
   a.partials = ws.p;
+  const bool folded = set_fold(a, layout, ws, seg_sumsq, true);
+  if (folded) a.fold_total = total_sumsq;
   rc = status_of(flr::launch_sumsq_only(a, grid_for(layout, layout->L.n_tiles,
                                                     sumsq_blocks_per_cu(R)), st));
-  if (rc == FL_OK)
+  if (rc == FL_OK && !folded)
     rc = status_of(flr::launch_seg_finalize(layout->L, ws.p, ws.chunks, ws.seg, seg_sumsq,
                                             total_sumsq, st));
   const int rc2 = ws.release();
@@ -764,7 +877,7 @@ int fl_round_hsdp(const fl_layout* layout, const fl_round_cfg* cfg, const fl_hsd
     return status_of(hipEventRecord(static_cast<hipEvent_t>(c.phase_events[k]), st));
   };
   Workspace ws;
-  if (n > 0 && (seg_sumsq || c.max_grad_norm > 0.f) && (rc = ws.alloc(layout->L, st)) != FL_OK)
+  if (n > 0 && (seg_sumsq || c.max_grad_norm > 0.f) && (rc = ws.acquire(layout, st)) != FL_OK)
     return rc;
   for (int a = 0; a < c.A && rc == FL_OK; ++a) {
     rc = record(a);
@@ -917,7 +1030,7 @@ static int round_impl(const fl_layout* layout, const fl_round_cfg* cfg,
     return status_of(hipEventRecord(static_cast<hipEvent_t>(c.phase_events[k]), st));
   };
   Workspace ws;
-  if (n > 0 && (seg_sumsq || c.max_grad_norm > 0.f) && (rc = ws.alloc(layout->L, st)) != FL_OK)
+  if (n > 0 && (seg_sumsq || c.max_grad_norm > 0.f) && (rc = ws.acquire(layout, st)) != FL_OK)
     return rc;
   for (int a = 0; a < c.A && rc == FL_OK; ++a) {
     rc = record(a);

@@ -187,6 +187,99 @@ __device__ __forceinline__ int find_seg(const int64_t* off, int lo, int hi, int6
   return lo;
 }
 
+// A (piece, wave) partial: stored at device (agent) scope, so that it goes to
+// the device's coherence point instead of staying in one XCD's L2, where the
+// folded finalize of another workgroup could not see it.
+__device__ __forceinline__ void put_partial(double* p, double v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// Fixed-tree total of the (piece, wave) partials of finalize chunk c: thread
+// j folds pieces j, j + 256, ... (each piece's kWaves slots in order), a
+// wave64 butterfly, then the 4 wave totals in order.  Called by all threads
+// of the workgroup; the result is valid in thread 0.  COHERENT: read the
+// partials at device scope (the folded finalize, which runs in the pass
+// that wrote them); otherwise they were written by an earlier kernel.
+template <bool COHERENT>
+__device__ __forceinline__ double chunk_fold(const LayoutDev& L, const double* partials,
+                                             int64_t c, double* red) {
+  const int64_t p0 = L.chunk_p0[c];
+  const int64_t p1 = L.chunk_p0[c + 1];
+  double acc = 0.0;
+  for (int64_t p = p0 + threadIdx.x; p < p1; p += kBlock) {
+    const double* q = partials + p * kWaves;
+    if constexpr (COHERENT) {
+#pragma unroll
+      for (int k = 0; k < kWaves; ++k)
+        acc = acc + __hip_atomic_load(q + k, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    } else {
+      const f64x2 w0 = *reinterpret_cast<const f64x2*>(q);
+      const f64x2 w1 = *reinterpret_cast<const f64x2*>(q + 2);
+      acc = acc + w0.x;
+      acc = acc + w0.y;
+      acc = acc + w1.x;
+      acc = acc + w1.y;
+    }
+  }
+  acc = wave_sum(acc);
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = acc;
+  __syncthreads();
+  const double sum = ((red[0] + red[1]) + red[2]) + red[3];
+  __syncthreads();
+  return sum;
+}
+
+// Fixed-tree total of n_seg per-segment values: thread t adds values t,
+// t + 256, ... in order, a wave64 butterfly, then the 4 wave totals in order.
+// Called by all threads; the result is valid in thread 0.
+template <typename Get>
+__device__ __forceinline__ double total_fold(int64_t n_seg, Get get, double* red) {
+  double acc = 0.0;
+  for (int64_t s = threadIdx.x; s < n_seg; s += kBlock) acc = acc + get(s);
+  acc = wave_sum(acc);
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = acc;
+  __syncthreads();
+  const double sum = ((red[0] + red[1]) + red[2]) + red[3];
+  __syncthreads();
+  return sum;
+}
+
+// The finalize of a pass with few single-chunk segments, run by the
+// workgroup that finishes the pass last (see StepArgs::fold_counter): every
+// workgroup waits until its partials (device-scope stores) are complete and
+// then counts itself in with a device-scope atomic; the one that counts last
+// reads all partials at device scope and writes the per-segment totals (and
+// their float roundings, and the whole-shard total), with the trees of
+// k_seg_chunks and k_total, so the bits equal those of the separate finalize
+// kernels.  No fence flushes the L2s: only the partials cross workgroups.
+__device__ void fold_finalize(const StepArgs& a) {
+  __shared__ double red[4];
+  __shared__ double segs[kFoldMaxChunks];
+  __shared__ int last;
+  __builtin_amdgcn_s_waitcnt(0);  // this wave's partial stores have completed
+  __syncthreads();
+  if (threadIdx.x == 0)
+    last = __hip_atomic_fetch_add(a.fold_counter, 1u, __ATOMIC_RELAXED,
+                                  __HIP_MEMORY_SCOPE_AGENT) == gridDim.x - 1;
+  __syncthreads();
+  if (!last) return;
+  for (int64_t c = 0; c < a.L.n_chunks; ++c) {
+    const double sum = chunk_fold<true>(a.L, a.partials, c, red);
+    if (threadIdx.x == 0) {
+      segs[c] = sum;
+      a.fold_seg[c] = sum;
+      if (a.fold_out) a.fold_out[c] = (float)sum;
+    }
+  }
+  __syncthreads();
+  if (a.fold_total) {
+    const double tot = total_fold(a.L.n_seg, [&](int64_t s) { return segs[s]; }, red);
+    if (threadIdx.x == 0) *a.fold_total = tot;
+  }
+  if (threadIdx.x == 0)
+    __hip_atomic_store(a.fold_counter, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
 // MODE 0: fused reduce + AdamW + working copy; 1: reduce only (g_out); 2:
 // AdamW only (g_in); 3: reduce to the bf16 wire format (wire_out); 4: reduce
 // with no output but the sums of squares.  In MODE 0 and 2 the gradient is
@@ -303,7 +396,7 @@ __global__ void __launch_bounds__(kBlock) k_step(const StepArgs a) {
 #pragma unroll
         for (int e = 0; e < 8; ++e) if (e < cnt) acc = acc + (double)g[e] * (double)g[e];
         const double tot = wave_sum(acc);
-        if ((tid & 63) == 0) a.partials[(int64_t)ti.piece0 * kWaves + wid] = tot;
+        if ((tid & 63) == 0) put_partial(a.partials + (int64_t)ti.piece0 * kWaves + wid, tot);
       } else {
         for (int j = 0; j < ti.nseg; ++j) {
           const int sj = ti.seg0 + j;
@@ -312,10 +405,13 @@ __global__ void __launch_bounds__(kBlock) k_step(const StepArgs a) {
           for (int e = 0; e < 8; ++e)
             if (e < cnt && seg[e] == sj) acc = acc + (double)g[e] * (double)g[e];
           const double tot = wave_sum(acc);
-          if ((tid & 63) == 0) a.partials[((int64_t)ti.piece0 + j) * kWaves + wid] = tot;
+          if ((tid & 63) == 0) put_partial(a.partials + ((int64_t)ti.piece0 + j) * kWaves + wid, tot);
         }
       }
     }
+  }
+  if constexpr (SUMSQ) {
+    if (a.fold_counter) fold_finalize(a);
   }
 }
 
@@ -468,26 +564,11 @@ __global__ void __launch_bounds__(kBlock) k_seg_chunks(const LayoutDev L, const 
                                                        double* chunk_sums, float* out) {
   __shared__ double red[4];
   for (int64_t c = blockIdx.x; c < L.n_chunks; c += gridDim.x) {
-    const int64_t p0 = L.chunk_p0[c];
-    const int64_t p1 = L.chunk_p0[c + 1];
-    double acc = 0.0;
-    for (int64_t p = p0 + threadIdx.x; p < p1; p += kBlock) {
-      const f64x2 w0 = *reinterpret_cast<const f64x2*>(partials + p * kWaves);
-      const f64x2 w1 = *reinterpret_cast<const f64x2*>(partials + p * kWaves + 2);
-      acc = acc + w0.x;
-      acc = acc + w0.y;
-      acc = acc + w1.x;
-      acc = acc + w1.y;
-    }
-    acc = wave_sum(acc);
-    if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = acc;
-    __syncthreads();
+    const double sum = chunk_fold<false>(L, partials, c, red);
     if (threadIdx.x == 0) {
-      const double sum = ((red[0] + red[1]) + red[2]) + red[3];
       chunk_sums[c] = sum;
       if (DIRECT && out) out[c] = (float)sum;
     }
-    __syncthreads();
   }
 }
 
@@ -505,12 +586,8 @@ __global__ void __launch_bounds__(kBlock) k_seg_totals(const LayoutDev L, const 
 __global__ void __launch_bounds__(kBlock) k_total(const int64_t n_seg, const double* seg_dbl,
                                                   double* total) {
   __shared__ double red[4];
-  double acc = 0.0;
-  for (int64_t s = threadIdx.x; s < n_seg; s += kBlock) acc = acc + seg_dbl[s];
-  acc = wave_sum(acc);
-  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = acc;
-  __syncthreads();
-  if (threadIdx.x == 0) *total = ((red[0] + red[1]) + red[2]) + red[3];
+  const double tot = total_fold(n_seg, [&](int64_t s) { return seg_dbl[s]; }, red);
+  if (threadIdx.x == 0) *total = tot;
 }
 
 // Broadcast receive: master = recv; working = bf16(recv).

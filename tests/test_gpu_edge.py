@@ -263,3 +263,96 @@ def test_hundreds_of_thousands_of_segments(env):
     flags = r.integers(0, 2, sizes.size).astype(np.uint8)
     w = W.make_workload("many_many_segments", sizes, flags, R=2, G=2, A=2, max_grad_norm=0.01)
     _parity(env, w, "300k segments")
+
+
+def _twin_rounds(env, w, cfg_step0=1):
+    """The same round on two streams: the first stream to ask takes the
+    layout's workspace (finalize folded into the pass where the layout
+    allows it), the second a stream-ordered temporary (separate finalize
+    kernels).  Returns both results."""
+    torch, P = env["torch"], env["P"]
+    lay = P.Layout(w.seg_offsets, w.seg_decay)
+    da, db = B.DeviceInputs(w), B.DeviceInputs(w)
+    torch.cuda.synchronize()
+    sa, sb = torch.cuda.Stream(), torch.cuda.Stream()
+    out = []
+    for d, s in ((da, sa), (db, sb)):
+        ss = torch.full((w.A * w.n_seg,), -1.0, dtype=torch.float32, device="cuda")
+        with torch.cuda.stream(s):
+            H.gpu_round(P, lay, w, d, seg_sumsq=ss)
+        out.append((d, ss))
+    torch.cuda.synchronize()
+    res = []
+    for d, ss in out:
+        st = _state(d)
+        st["ss"] = ss.cpu().numpy()
+        res.append(st)
+    lay.close()
+    return res
+
+
+@pytest.mark.parametrize("sizes,clip,scratch", [
+    ([1 << 20], 0.0, False),                               # one segment (the tiny round's shape)
+    ([300000, 17, 2047, 2049, 1 << 20, 5, 9, 70000], 0.0, False),  # 8 segments
+    ([300000, 17, 2047, 2049, 1 << 20, 5, 9, 70000], 1e-3, False),
+    ([300000, 17, 2047, 2049, 1 << 20, 5, 9, 70000], 1e-3, True),
+    ([1024 * 2048, 3], 1e-3, False),                       # a segment of exactly 1024 tiles
+])
+def test_folded_finalize_matches_separate_kernels(env, sizes, clip, scratch):
+    """Where a pass folds its finalize into its last workgroup (every
+    segment one finalize chunk, at most 8 segments), the per-segment sums,
+    the clip totals and so every output are bitwise those of the separate
+    finalize kernels; both equal the oracle."""
+    flags = (np.arange(len(sizes)) % 2).astype(np.uint8)
+    w = W.make_workload("fold", sizes, flags, R=4, G=2, A=3, max_grad_norm=clip,
+                        clip_scratch=scratch, seed=5)
+    a, b = _twin_rounds(env, w)
+    for k in ("master", "m", "v", "working", "ss"):
+        u = np.uint16 if k == "working" else np.uint32
+        assert np.array_equal(np.asarray(a[k]).view(u), np.asarray(b[k]).view(u)), k
+    host = B.HostInputs(w)
+    ref = H.oracle_round(env["orc"], w, host, want_sumsq=True)
+    H.assert_state_parity("fold", a, dict(master=host.master, m=host.m, v=host.v,
+                                          working=host.working), bitwise=True)
+    H.assert_sumsq("fold", a["ss"], ref.reshape(-1))
+
+
+def test_grad_sumsq_folded_total_matches(env):
+    """fl_grad_sumsq on a fold-eligible layout: the whole-shard total and the
+    per-segment sums from the folded pass equal those of the separate
+    kernels bitwise (second stream) and the oracle's within tolerance."""
+    torch, P, orc = env["torch"], env["P"], env["orc"]
+    sizes = [50000, 3, 1 << 19, 77777]
+    w = W.make_workload("fold_total", sizes, [1, 0, 1, 1], R=3, G=2, A=1, seed=9)
+    lay = P.Layout(w.seg_offsets, w.seg_decay)
+    d = B.DeviceInputs(w)
+    torch.cuda.synchronize()
+    outs = []
+    for s in (torch.cuda.Stream(), torch.cuda.Stream()):
+        tot = torch.full((1,), -1.0, dtype=torch.float64, device="cuda")
+        ss = torch.full((w.n_seg,), -1.0, dtype=torch.float32, device="cuda")
+        with torch.cuda.stream(s):
+            P.fl_grad_sumsq(lay, d.grads[:w.R], w.grad_scale, tot, ss)
+        outs.append((tot, ss))
+    torch.cuda.synchronize()
+    (t0, s0), (t1, s1) = outs
+    assert t0.cpu().numpy().view(np.uint64)[0] == t1.cpu().numpy().view(np.uint64)[0]
+    assert np.array_equal(s0.cpu().numpy().view(np.uint32), s1.cpu().numpy().view(np.uint32))
+    host = B.HostInputs(w)
+    g = orc.shard_reduce(host.grads[:w.R], w.grad_scale)
+    ref_ss = orc.seg_sumsq(w.seg_offsets, g)
+    H.assert_sumsq("fold_total segs", s0.cpu().numpy(), ref_ss)
+    H.assert_sumsq("fold_total", t0.cpu().numpy(), np.array([orc.total_sumsq(g)]))
+    lay.close()
+
+
+@pytest.mark.parametrize("clip", [0.0, 1e-3])
+def test_multi_chunk_finalize_against_oracle(env, clip):
+    """Segments of exactly 1024 tiles (one finalize chunk), 1025 tiles (two
+    chunks, so the per-segment fold of chunk sums runs) and about 5 M
+    elements (three chunks), between short ones; every per-segment sum of
+    squares against the oracle, unclipped and clipped."""
+    sizes = [1024 * 2048, 1025 * 2048, 5_000_003, 7, 300, 1, 4096]
+    flags = np.array([1, 1, 0, 1, 0, 1, 1], np.uint8)
+    w = W.make_workload("multi_chunk", sizes, flags, R=2, G=2, A=2, max_grad_norm=clip, seed=12)
+    _parity(env, w, "multi_chunk clip=%g" % clip)
