@@ -57,7 +57,9 @@ typedef enum {
   FL_ERR_LAYOUT = -3,  /* a replica's layout fingerprint differs from ours      */
   FL_ERR_DEVICE = -4,  /* current device is not the layout's device             */
   FL_ERR_HIP = -5,     /* a HIP runtime call or a kernel launch failed          */
-  FL_ERR_NOMEM = -6    /* host or device allocation failed                      */
+  FL_ERR_NOMEM = -6,   /* host or device allocation failed                      */
+  FL_ERR_SCRATCH = -7  /* fl_round_noalloc: the layout's per-segment workspace
+                          exceeds the library's static scratch                 */
 } fl_status;
 
 #define FL_MAX_PEERS 64  /* upper bound on R */
@@ -217,7 +219,7 @@ int fl_fedavg(const fl_layout* layout, int G, const uint16_t* const* replicas,
  *   layout's workspace for all its steps, or one stream-ordered temporary
  *   when that is not available to this stream (see fl_layout_create); under
  *   graph capture the temporary becomes a graph allocation.  Without them it
- *   allocates nothing.
+ *   allocates nothing.  fl_round_noalloc never allocates.
  * Configuration: 1 <= R <= FL_MAX_PEERS, 1 <= G <= FL_MAX_GROUPS, A >= 1,
  *   0 <= self_group < G, step0 >= 1, grad_scale finite, h and weights as
  *   above, replica_fp as in fl_fedavg, step_lr entries finite and >= 0,
@@ -256,6 +258,34 @@ typedef struct {
 int fl_round(const fl_layout* layout, const fl_round_cfg* cfg, const uint16_t* const* grads,
              const uint16_t* const* replicas, float* master, float* m, float* v,
              uint16_t* working, float* seg_sumsq, void* stream);
+
+/* ------------------------------------------------------------------------
+ * fl_round_noalloc -- fl_round for callers that cannot allocate device
+ * memory: code being captured into a HIP graph, tight serving loops, and
+ * harnesses that forbid allocation.  Same arguments, same arithmetic, same
+ * bits as fl_round; it calls no allocator, and the workspace of the
+ * per-segment sums of squares (seg_sumsq given, or clipping) is a static
+ * device array of the library, FL_NOALLOC_SCRATCH_BYTES (32 MiB) per GPU,
+ * held from the library's first use of that GPU until the process ends.
+ * Every fl_round_noalloc call on one GPU shares that array: calls that
+ * overlap in time on one GPU (two streams, two host threads) race and give
+ * undefined results; calls on one stream are ordered and safe.
+ * A layout whose workspace (32 bytes per (2048-element tile, segment) pair,
+ * plus 8 per segment and per finalize chunk, plus 264) exceeds the array
+ * returns FL_ERR_SCRATCH before anything is enqueued, when the call needs the
+ * workspace; with neither seg_sumsq nor clipping any layout is accepted.
+ * The array's address on a GPU is looked up, and its counter cleared, by the
+ * first fl_layout_create on that GPU.
+ * fl_noalloc_workspace_bytes returns the bytes a layout would need (0 for
+ * NULL or an empty layout).
+ * ---------------------------------------------------------------------- */
+#define FL_NOALLOC_SCRATCH_BYTES ((size_t)32 << 20)
+
+int fl_round_noalloc(const fl_layout* layout, const fl_round_cfg* cfg,
+                     const uint16_t* const* grads, const uint16_t* const* replicas,
+                     float* master, float* m, float* v, uint16_t* working, float* seg_sumsq,
+                     void* stream);
+size_t fl_noalloc_workspace_bytes(const fl_layout* layout);
 
 /* ------------------------------------------------------------------------
  * fl_lr_cosine -- the learning rate of optimiser step t (1-based) under

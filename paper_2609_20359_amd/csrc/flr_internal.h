@@ -109,6 +109,14 @@ hipError_t launch_fedavg(const FedArgs& a, int grid, hipStream_t st);
 hipError_t launch_seg_finalize(const LayoutDev& L, const double* partials, double* chunk_sums,
                                double* seg_dbl, float* out, double* total, hipStream_t st);
 hipError_t launch_sumsq_only(const StepArgs& a, int grid, hipStream_t st);
+
+// The static scratch of fl_round_noalloc (kNoallocScratchBytes per GPU; the
+// first kNoallocHeadBytes hold the folded finalize's counter).  The first
+// call for a device, with that device current, looks up the array's address
+// on it and clears the counter; later calls return the cached address.
+constexpr size_t kNoallocScratchBytes = (size_t)32 << 20;
+constexpr size_t kNoallocHeadBytes = 256;
+hipError_t noalloc_scratch(int device, void** ptr);
 hipError_t launch_zero_total(double* total, hipStream_t st);
 
 }  // namespace flr

@@ -36,6 +36,9 @@ struct fl_layout {
   hipStream_t ws_stream = nullptr;
   hipEvent_t ws_done = nullptr;
   bool ws_recorded = false;
+  // This device's static scratch of fl_round_noalloc (null if the lookup
+  // failed; fl_round_noalloc then reports FL_ERR_HIP when it needs it).
+  void* noalloc = nullptr;
 };
 
 namespace {
@@ -226,6 +229,17 @@ struct Workspace {
   fl_layout* owner = nullptr;   // the layout whose workspace this is (or null)
   void* own = nullptr;          // a stream-ordered allocation of this call
 
+  // The static scratch of fl_round_noalloc: the counter in its head, the
+  // rest after it.  Nothing is allocated and nothing needs releasing.
+  int use_static(const fl_layout* lay, hipStream_t stream) {
+    st = stream;
+    if (!lay->noalloc) return FL_ERR_HIP;
+    char* base = static_cast<char*>(lay->noalloc);
+    carve(lay->L, base + flr::kNoallocHeadBytes);
+    counter = reinterpret_cast<unsigned*>(base);
+    return FL_OK;
+  }
+
   void carve(const flr::LayoutDev& L, void* mem) {
     p = static_cast<double*>(mem);
     chunks = p + ws_slots(L);
@@ -288,6 +302,11 @@ struct Workspace {
     return rc;
   }
 };
+
+// Bytes of the static scratch a layout's workspace needs in fl_round_noalloc.
+size_t noalloc_bytes(const flr::LayoutDev& L) {
+  return flr::kNoallocHeadBytes + ws_bytes(L) - sizeof(double);
+}
 
 // Whether a pass with per-segment sums folds its finalize (every segment one
 // finalize chunk, few of them, and a zeroed counter to count workgroups).
@@ -426,11 +445,14 @@ const char* fl_status_string(int status) {
     case FL_ERR_DEVICE: return "FL_ERR_DEVICE: current device is not the layout's device";
     case FL_ERR_HIP: return "FL_ERR_HIP: HIP runtime or launch failure";
     case FL_ERR_NOMEM: return "FL_ERR_NOMEM: allocation failed";
+    case FL_ERR_SCRATCH:
+      return "FL_ERR_SCRATCH: the layout's per-segment workspace exceeds fl_round_noalloc's "
+             "static scratch";
     default: return "unknown fl_status";
   }
 }
 
-int fl_version(void) { return (1 << 16) | 5; }
+int fl_version(void) { return (1 << 16) | 6; }
 
 float fl_lr_cosine(int64_t t, int64_t total_steps, int64_t warmup_steps, float lr_max,
                    float lr_min) {
@@ -571,6 +593,12 @@ int fl_layout_create(int64_t n, int64_t n_seg, const int64_t* seg_offsets,
     return status_of(e);
   }
   lay->dev_mem = mem;
+  // set-up of fl_round_noalloc's static scratch on this device (once per
+  // device; a failure here only disables fl_round_noalloc's workspace)
+  if (flr::noalloc_scratch(lay->device, &lay->noalloc) != hipSuccess) {
+    (void)hipGetLastError();
+    lay->noalloc = nullptr;
+  }
   lay->L.seg_off = reinterpret_cast<const int64_t*>(p_off);
   lay->L.seg_piece0 = reinterpret_cast<const int64_t*>(p_pp);
   lay->L.seg_chunk0 = reinterpret_cast<const int64_t*>(p_sc);
@@ -948,7 +976,8 @@ int fl_fedopt(const fl_layout* layout, int G, const uint16_t* const* replicas,
 static int round_impl(const fl_layout* layout, const fl_round_cfg* cfg,
                       const fl_outer_hparams* outer, const uint16_t* const* grads,
                       const uint16_t* const* replicas, float* prev, float* buf, float* master,
-                      float* m, float* v, uint16_t* working, float* seg_sumsq, void* stream);
+                      float* m, float* v, uint16_t* working, float* seg_sumsq, void* stream,
+                      bool noalloc = false);
 
 int fl_round_outer(const fl_layout* layout, const fl_round_cfg* cfg, const fl_outer_hparams* outer,
                    const uint16_t* const* grads, const uint16_t* const* replicas, float* prev,
@@ -966,10 +995,24 @@ int fl_round(const fl_layout* layout, const fl_round_cfg* cfg, const uint16_t* c
                     working, seg_sumsq, stream);
 }
 
+int fl_round_noalloc(const fl_layout* layout, const fl_round_cfg* cfg,
+                     const uint16_t* const* grads, const uint16_t* const* replicas,
+                     float* master, float* m, float* v, uint16_t* working, float* seg_sumsq,
+                     void* stream) {
+  return round_impl(layout, cfg, nullptr, grads, replicas, nullptr, nullptr, master, m, v,
+                    working, seg_sumsq, stream, true);
+}
+
+size_t fl_noalloc_workspace_bytes(const fl_layout* layout) {
+  if (!layout || layout->L.n == 0) return 0;
+  return noalloc_bytes(layout->L);
+}
+
 static int round_impl(const fl_layout* layout, const fl_round_cfg* cfg,
                       const fl_outer_hparams* outer, const uint16_t* const* grads,
                       const uint16_t* const* replicas, float* prev, float* buf, float* master,
-                      float* m, float* v, uint16_t* working, float* seg_sumsq, void* stream) {
+                      float* m, float* v, uint16_t* working, float* seg_sumsq, void* stream,
+                      bool noalloc) {
   if (!layout || !cfg || !grads || !replicas) return FL_ERR_INVALID;
   const fl_round_cfg& c = *cfg;
   const int64_t n = layout->L.n;
@@ -1023,6 +1066,9 @@ static int round_impl(const fl_layout* layout, const fl_round_cfg* cfg,
     for (int k = 0; k < c.A + 2; ++k)
       if (!c.phase_events[k]) return FL_ERR_INVALID;
   if ((rc = check_device(layout)) != FL_OK) return rc;
+  const bool needs_ws = n > 0 && (seg_sumsq || c.max_grad_norm > 0.f);
+  if (noalloc && needs_ws && noalloc_bytes(layout->L) > flr::kNoallocScratchBytes)
+    return FL_ERR_SCRATCH;
 
   hipStream_t st = static_cast<hipStream_t>(stream);
   auto record = [&](int k) -> int {
@@ -1030,7 +1076,7 @@ static int round_impl(const fl_layout* layout, const fl_round_cfg* cfg,
     return status_of(hipEventRecord(static_cast<hipEvent_t>(c.phase_events[k]), st));
   };
   Workspace ws;
-  if (n > 0 && (seg_sumsq || c.max_grad_norm > 0.f) && (rc = ws.acquire(layout, st)) != FL_OK)
+  if (needs_ws && (rc = noalloc ? ws.use_static(layout, st) : ws.acquire(layout, st)) != FL_OK)
     return rc;
   for (int a = 0; a < c.A && rc == FL_OK; ++a) {
     rc = record(a);

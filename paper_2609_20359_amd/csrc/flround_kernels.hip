@@ -21,6 +21,14 @@
 //     that straddle a segment boundary (rare) resolve segments per element.
 #include "flr_internal.h"
 
+#include <mutex>
+
+// Workspace of fl_round_noalloc, for callers that cannot allocate: one array
+// per GPU in the code object, held until the process ends.  Host code uses
+// only the per-device address that noalloc_scratch() looks up, never this
+// name (which on the host side is a stand-in, not a device address).
+static __device__ __align__(256) unsigned char scratch[flr::kNoallocScratchBytes];
+
 namespace flr {
 namespace {
 
@@ -718,6 +726,26 @@ hipError_t launch_zero_total(double* total, hipStream_t st) {
 
 hipError_t launch_sumsq_only(const StepArgs& a, int grid, hipStream_t st) {
   return dispatch_step<4, true>(a, grid, st);
+}
+
+hipError_t noalloc_scratch(int device, void** ptr) {
+  constexpr int kMaxDevices = 64;
+  static std::mutex mu;
+  static void* addr[kMaxDevices] = {};
+  if (device < 0 || device >= kMaxDevices || !ptr) return hipErrorInvalidValue;
+  std::lock_guard<std::mutex> lock(mu);
+  if (!addr[device]) {
+    void* p = nullptr;
+    hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    if (!p) return hipErrorInvalidSymbol;
+    e = hipMemset(p, 0, kNoallocHeadBytes);  // the folded finalize's counter
+    if (e == hipSuccess) e = hipDeviceSynchronize();
+    if (e != hipSuccess) return e;
+    addr[device] = p;
+  }
+  *ptr = addr[device];
+  return hipSuccess;
 }
 
 }  // namespace flr

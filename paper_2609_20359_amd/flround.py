@@ -20,6 +20,8 @@ FL_ERR_LAYOUT = -3
 FL_ERR_DEVICE = -4
 FL_ERR_HIP = -5
 FL_ERR_NOMEM = -6
+FL_ERR_SCRATCH = -7
+FL_NOALLOC_SCRATCH_BYTES = 32 << 20
 
 FL_MAX_PEERS = 64
 FL_MAX_GROUPS = 64
@@ -30,7 +32,8 @@ EXPORTS = ("fl_status_string", "fl_version", "fl_layout_create", "fl_layout_dest
            "fl_layout_fingerprint", "fl_shard_reduce", "fl_adamw_step", "fl_local_step",
            "fl_fedavg", "fl_round", "fl_set_blocks_per_cu", "fl_shard_reduce_wire",
            "fl_broadcast_recv", "fl_round_hsdp", "fl_fedopt", "fl_round_outer",
-           "fl_lr_cosine", "fl_grad_sumsq", "fl_local_step_clipped")
+           "fl_lr_cosine", "fl_grad_sumsq", "fl_local_step_clipped", "fl_round_noalloc",
+           "fl_noalloc_workspace_bytes")
 
 _P = ctypes.c_void_p
 
@@ -105,6 +108,10 @@ def lib():
                                     ctypes.c_int, _P, ctypes.c_float, _P, _P, _P, _P, _P, _P]
         L.fl_fedavg.argtypes = [_P, ctypes.c_int, _P, _P, _P, _P, _P, _P]
         L.fl_round.argtypes = [_P, ctypes.POINTER(RoundCfg), _P, _P, _P, _P, _P, _P, _P, _P]
+        L.fl_round_noalloc.argtypes = [_P, ctypes.POINTER(RoundCfg), _P, _P, _P, _P, _P, _P, _P,
+                                       _P]
+        L.fl_noalloc_workspace_bytes.argtypes = [_P]
+        L.fl_noalloc_workspace_bytes.restype = ctypes.c_size_t
         L.fl_shard_reduce_wire.argtypes = [_P, ctypes.c_int, _P, ctypes.c_float, _P, _P]
         L.fl_broadcast_recv.argtypes = [_P, _P, _P, _P, _P]
         L.fl_round_hsdp.argtypes = [_P, ctypes.POINTER(RoundCfg), ctypes.POINTER(HsdpCfg), _P, _P,
@@ -331,6 +338,28 @@ def fl_round(layout, cfg, grads, replicas, master, m, v, working, seg_sumsq=None
                         _buf(m, n, 4, "m"), _buf(v, n, 4, "v"), _buf(working, n, 2, "working"),
                         _buf(seg_sumsq, cfg.A * layout.n_seg, 4, "seg_sumsq"), _stream(stream))
     _check(rc, "fl_round")
+
+
+def fl_round_noalloc(layout, cfg, grads, replicas, master, m, v, working, seg_sumsq=None,
+                     stream=None):
+    """fl_round with the per-segment workspace in the library's static
+    scratch: allocates nothing (see include/flround.h)."""
+    n = layout.n
+    _check_cfg(layout, cfg)
+    rc = lib().fl_round_noalloc(layout.handle, ctypes.byref(cfg),
+                                _bufs(grads, cfg.A * cfg.R, n, 2, "grads"),
+                                _bufs(replicas, cfg.G, n, 2, "replicas"),
+                                _buf(master, n, 4, "master"), _buf(m, n, 4, "m"),
+                                _buf(v, n, 4, "v"), _buf(working, n, 2, "working"),
+                                _buf(seg_sumsq, cfg.A * layout.n_seg, 4, "seg_sumsq"),
+                                _stream(stream))
+    _check(rc, "fl_round_noalloc")
+
+
+def noalloc_workspace_bytes(layout):
+    """Bytes of fl_round_noalloc's static scratch the layout's workspace
+    needs (FL_NOALLOC_SCRATCH_BYTES is the limit)."""
+    return int(lib().fl_noalloc_workspace_bytes(layout.handle))
 
 
 def fl_shard_reduce_wire(layout, peer_grads, grad_scale, wire_out, stream=None):

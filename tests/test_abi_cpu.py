@@ -33,7 +33,7 @@ def test_library_exports_every_declared_symbol():
 
 def test_status_strings_and_version():
     assert P.status_string(0) == "FL_OK"
-    for code in range(-6, 0):
+    for code in range(-7, 0):
         assert P.status_string(code).startswith("FL_ERR_")
     assert "unknown" in P.status_string(7)
     assert P.lib().fl_version() >> 16 == 1
