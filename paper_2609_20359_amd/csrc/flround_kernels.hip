@@ -195,11 +195,16 @@ __device__ __forceinline__ int find_seg(const int64_t* off, int lo, int hi, int6
   return lo;
 }
 
-// A (piece, wave) partial: stored at device (agent) scope, so that it goes to
-// the device's coherence point instead of staying in one XCD's L2, where the
-// folded finalize of another workgroup could not see it.
-__device__ __forceinline__ void put_partial(double* p, double v) {
-  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+// A (piece, wave) partial.  When the pass folds its finalize (coherent), it
+// is stored at device (agent) scope, so that it goes to the device's
+// coherence point instead of staying in one XCD's L2, where the workgroup
+// that folds could not see it; otherwise a plain store, read by a later
+// kernel.
+__device__ __forceinline__ void put_partial(double* p, double v, bool coherent) {
+  if (coherent)
+    __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  else
+    *p = v;
 }
 
 // Fixed-tree total of the (piece, wave) partials of finalize chunk c: thread
@@ -298,6 +303,7 @@ __global__ void __launch_bounds__(kBlock) k_step(const StepArgs a) {
   const int tid = threadIdx.x;
   const bool clip = (MODE == 0 || MODE == 2) && a.clip_total != nullptr;
   const float coef = clip ? clip_coef(a.clip_total, a.clip_max) : 1.0f;
+  const bool fold = SUMSQ && a.fold_counter != nullptr;
   for (int64_t t = blockIdx.x; t < a.L.n_tiles; t += gridDim.x) {
     const TileInfo ti = a.L.tiles[t];
     const int64_t base = t * kTile + (int64_t)tid * kVec;
@@ -404,7 +410,7 @@ __global__ void __launch_bounds__(kBlock) k_step(const StepArgs a) {
 #pragma unroll
         for (int e = 0; e < 8; ++e) if (e < cnt) acc = acc + (double)g[e] * (double)g[e];
         const double tot = wave_sum(acc);
-        if ((tid & 63) == 0) put_partial(a.partials + (int64_t)ti.piece0 * kWaves + wid, tot);
+        if ((tid & 63) == 0) put_partial(a.partials + (int64_t)ti.piece0 * kWaves + wid, tot, fold);
       } else {
         for (int j = 0; j < ti.nseg; ++j) {
           const int sj = ti.seg0 + j;
@@ -413,7 +419,8 @@ __global__ void __launch_bounds__(kBlock) k_step(const StepArgs a) {
           for (int e = 0; e < 8; ++e)
             if (e < cnt && seg[e] == sj) acc = acc + (double)g[e] * (double)g[e];
           const double tot = wave_sum(acc);
-          if ((tid & 63) == 0) put_partial(a.partials + ((int64_t)ti.piece0 + j) * kWaves + wid, tot);
+          if ((tid & 63) == 0) put_partial(a.partials + ((int64_t)ti.piece0 + j) * kWaves + wid, tot,
+                                            fold);
         }
       }
     }
