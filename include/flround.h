@@ -223,7 +223,7 @@ int fl_fedavg(const fl_layout* layout, int G, const uint16_t* const* replicas,
  * Configuration: 1 <= R <= FL_MAX_PEERS, 1 <= G <= FL_MAX_GROUPS, A >= 1,
  *   0 <= self_group < G, step0 >= 1, grad_scale finite, h and weights as
  *   above, replica_fp as in fl_fedavg, step_lr entries finite and >= 0,
- *   max_grad_norm finite.
+ *   max_grad_norm finite and >= 0.
  * phase_events: NULL, or host array of A+2 hipEvent_t created by the caller;
  *   event a (a < A) is recorded on `stream` before local step a, event A
  *   before FedAvg, event A+1 after it (per-phase timing of the round, like
@@ -243,7 +243,8 @@ typedef struct {
   const float* step_lr;      /* NULL or host, A learning rates, one per local
                                 step (overrides h.lr; e.g. fl_lr_cosine)   */
   float max_grad_norm;       /* > 0: clip each local step's gradient to this
-                                global norm (fl_local_step_clipped); 0: off */
+                                global norm (fl_local_step_clipped); 0: off;
+                                negative or non-finite: FL_ERR_INVALID      */
   float* grad_scratch;       /* NULL, or device, N floats distinct from every
                                 other buffer: with max_grad_norm > 0 the
                                 sum-of-squares pass also stores each step's

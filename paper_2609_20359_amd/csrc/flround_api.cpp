@@ -149,7 +149,7 @@ fl_adamw_hparams step_hparams(const fl_round_cfg& c, int a) {
 }
 
 bool step_lrs_ok(const fl_round_cfg& c) {
-  if (!std::isfinite(c.max_grad_norm)) return false;
+  if (!std::isfinite(c.max_grad_norm) || !(c.max_grad_norm >= 0.f)) return false;
   if (!c.step_lr) return true;
   for (int a = 0; a < c.A; ++a)
     if (!std::isfinite(c.step_lr[a]) || !(c.step_lr[a] >= 0.f)) return false;

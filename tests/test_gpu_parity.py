@@ -326,6 +326,8 @@ def test_errors_are_returned_before_any_launch(env):
     assert status(lambda: run(cfg(step0=0))) == -1
     assert status(lambda: run(cfg(self_group=2))) == -1
     assert status(lambda: run(cfg(R=65))) == -1
+    assert status(lambda: run(cfg(max_grad_norm=-1.0))) == -1
+    assert status(lambda: run(cfg(max_grad_norm=float("inf")))) == -1
     assert status(lambda: run(cfg(), gg=[g[0], unaligned])) == -2
     assert status(lambda: run(cfg(), rr=[None, None])) == -1
     assert status(lambda: run(cfg(replica_fp=[0, other.fingerprint]))) == -3
