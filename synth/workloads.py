@@ -331,10 +331,21 @@ def llama8b_s8_clip(seed=0):
                          seed=seed, distinct_grads=False, max_grad_norm=1.0, clip_scratch=True)
 
 
+def llama8b_s8_clip_noscratch(seed=0):
+    """The clipped Llama-3.1-8B S=8 round without the gradient scratch: a
+    sum-of-squares pass over the R peer gradients, then the fused step
+    scaled by the clip coefficient (the peer gradients are read twice)."""
+    sizes, dec = llama31_8b_segments(8)
+    return make_workload("llama31_8b_fsdp_s8_r8_g4_a8_clip1_noscratch", sizes, dec, R=8, G=4,
+                         A=8, seed=seed, distinct_grads=False, max_grad_norm=1.0,
+                         clip_scratch=False)
+
+
 ALL = dict(tiny=tiny, llama8b_s8=llama8b_s8, fedavg_heavy=fedavg_heavy, hsdp_s4=hsdp_s4,
            stress=stress, hsdp_s4_h2=hsdp_s4_h2,
            hsdp_s4_h2_recv=lambda seed=0: hsdp_s4_h2(seed, member=False),
-           llama8b_s8_outer=llama8b_s8_outer, llama8b_s8_clip=llama8b_s8_clip)
+           llama8b_s8_outer=llama8b_s8_outer, llama8b_s8_clip=llama8b_s8_clip,
+           llama8b_s8_clip_noscratch=llama8b_s8_clip_noscratch)
 
 
 def sample_indices(w, n_random=1 << 16, seed=1, full_segments=4, max_full=4096):
