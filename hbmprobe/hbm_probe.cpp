@@ -29,6 +29,10 @@
 //   step_R8_tiled  as step_R8, but the three fp32 state arrays interleaved per
 //              2048-element tile ([tile][master | m | v]), i.e. one 24 KB
 //              read-modify-write chunk per tile instead of three streams
+//   <pattern>_w  a pattern whose every wave waits for its previous
+//              iteration's stores to complete before issuing its next loads
+//              (copy, triad, step_R8/R4/R2, wire_R4, reduce_R8, fedavg_G4,
+//              fedopt_G4, bcast, rmw3)
 // each with plain and nontemporal stores, for 1, 2, 3, 4 and 8 workgroups per CU
 // (or the one count given).
 // Buffers are sized for the given element count (default: the
@@ -132,10 +136,13 @@ void run_tiled(Streams s, int cus, long elems) {
 // NRD bf16 streams read, NRMW fp32 streams read+written, NWH bf16 streams
 // written, NWF fp32 streams written.  fp32 streams hold 2 vectors per bf16
 // vector.  All indices < nvec (bf16) or < 2 * nvec (fp32).
-template <int NRD, int NRMW, int NWH, int NWF, bool NTS>
+template <int NRD, int NRMW, int NWH, int NWF, bool NTS, bool WAIT = false>
 __global__ void __launch_bounds__(256) k_pattern(Streams s) {
   const long stride = (long)gridDim.x * 256;
   for (long i = (long)blockIdx.x * 256 + threadIdx.x; i < s.nvec; i += stride) {
+    // WAIT: the previous iteration's stores complete before this
+    // iteration's loads are issued (s_waitcnt vmcnt(0))
+    if (WAIT) __builtin_amdgcn_s_waitcnt(0xF70);
     u32x4 x = {(unsigned)i, 0u, 0u, 0u};
 #pragma unroll
     for (int k = 0; k < NRD; ++k) x += __builtin_nontemporal_load(s.rd[k] + i);
@@ -192,7 +199,7 @@ float time_ms(F launch, int reps) {
   return ms / reps;
 }
 
-template <int NRD, int NRMW, int NWH, int NWF>
+template <int NRD, int NRMW, int NWH, int NWF, bool WAIT = false>
 void run(const char* name, Streams s, int cus, long elems) {
   if (!selected(name)) return;
   const double bytes = (double)elems * (2.0 * NRD + 8.0 * NRMW + 2.0 * NWH + 4.0 * NWF);
@@ -202,8 +209,9 @@ void run(const char* name, Streams s, int cus, long elems) {
     std::printf("| %-9s | %-5s |", name, nts ? "nt" : "plain");
     for (int bpc : g_bpc) {
       const int grid = bpc * cus;
-      float ms = nts ? time_ms([&] { k_pattern<NRD, NRMW, NWH, NWF, true><<<grid, 256>>>(s); }, 5)
-                     : time_ms([&] { k_pattern<NRD, NRMW, NWH, NWF, false><<<grid, 256>>>(s); }, 5);
+      float ms =
+          nts ? time_ms([&] { k_pattern<NRD, NRMW, NWH, NWF, true, WAIT><<<grid, 256>>>(s); }, 5)
+              : time_ms([&] { k_pattern<NRD, NRMW, NWH, NWF, false, WAIT><<<grid, 256>>>(s); }, 5);
       CK(hipGetLastError());
       const double gbs = bytes / (ms * 1e-3) / 1e9;
       std::printf(" %7.1f |", gbs);
@@ -281,6 +289,18 @@ int main(int argc, char** argv) {
   run<2, 0, 1, 1>("bcast", s, cus, elems);
   run<0, 3, 0, 0>("rmw3", s, cus, elems);
   run_tiled(s, cus, elems);
+  // the same patterns with each wave's stores completing before its next loads
+  run<1, 0, 1, 0, true>("copy_w", s, cus, elems);
+  run<2, 0, 1, 0, true>("triad_w", s, cus, elems);
+  run<8, 3, 1, 0, true>("step_R8_w", s, cus, elems);
+  run<4, 3, 1, 0, true>("step_R4_w", s, cus, elems);
+  run<2, 3, 1, 0, true>("step_R2_w", s, cus, elems);
+  run<4, 0, 1, 0, true>("wire_R4_w", s, cus, elems);
+  run<8, 0, 0, 1, true>("reduce_R8_w", s, cus, elems);
+  run<4, 0, 1, 1, true>("fedavg_G4_w", s, cus, elems);
+  run<4, 2, 1, 1, true>("fedopt_G4_w", s, cus, elems);
+  run<2, 0, 1, 1, true>("bcast_w", s, cus, elems);
+  run<0, 3, 0, 0, true>("rmw3_w", s, cus, elems);
 
   // the runtime's own device-to-device copy of one fp32 stream, as a vendor
   // reference point for the copy pattern (bytes read + written)
