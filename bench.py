@@ -22,7 +22,6 @@ sys.path.insert(0, ROOT)
 
 METRIC = "effective HBM GB/s (% of MI355X peak) and params/s per fl_round, 8B-shaped shard"
 PEAK_HBM_GBS = 8000.0   # MI355X HBM3E, 8 TB/s
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_local_step_llama31_8b_s8.md")
 KERNEL_SOURCES = [os.path.join(ROOT, "paper_2609_20359_amd", "csrc", f)
                   for f in ("flround_kernels.hip", "flr_internal.h")]
 
@@ -45,23 +44,23 @@ def kernel_source_hash():
     return h.hexdigest()[:16]
 
 
-def read_traffic(current_hash):
-    """Counter-measured HBM bytes per local-step launch (from the rocprofv3
-    --pmc summary committed under profiles/), or None if there is none or the
-    kernel source changed since it was taken."""
-    if not os.path.exists(TRAFFIC_FILE):
+def read_traffic(workload, current_hash):
+    """Counter-measured HBM bytes of one local step of the workload (from the
+    rocprofv3 --pmc summary committed under profiles/), or None if there is
+    none or the kernel source changed since it was taken."""
+    path = traffic_file(workload)
+    if not os.path.exists(path):
         return None
-    txt = open(TRAFFIC_FILE).read()
+    txt = open(path).read()
     fields = dict(re.findall(r"^- (\w+): (\S+)$", txt, flags=re.M))
     if fields.get("kernel_source_hash") != current_hash:
         return None
     try:
-        return float(fields["hbm_bytes_per_launch"])
+        return float(fields["hbm_bytes_per_local_step"])
     except (KeyError, ValueError):
         return None
 
 
-LOCAL_STEP_KERNEL = "k_step<8, 0, true>"
 COPY_KERNEL = "__amd_rocclr_copyBuffer"
 
 
@@ -98,8 +97,6 @@ def round_kernels(w):
 
 
 def traffic_file(workload):
-    if workload == "llama8b_s8":
-        return TRAFFIC_FILE
     return os.path.join(ROOT, "profiles", "traffic_%s.md" % W_ALL()[workload]().name)
 
 
@@ -146,7 +143,8 @@ def summarize_pmc(fetch_csv, write_csv, copy_mib, cmd_fetch, cmd_write, workload
              "scaled write GB | algorithmic read GB | algorithmic write GB | traffic / algorithmic |",
              "|---|---|---|---|---|---|---|---|---|"]
     out = {}
-    for name, alg_r, alg_w in round_kernels(w):
+    kernels = round_kernels(w)
+    for name, alg_r, alg_w in kernels:
         f, cnt = pick(fetch, name)
         wr, _ = pick(write, name)
         rb, wb = f * f_scale * 1024, wr * w_scale * 1024
@@ -154,11 +152,11 @@ def summarize_pmc(fetch_csv, write_csv, copy_mib, cmd_fetch, cmd_write, workload
         lines.append("| %s | %d | %.1f | %.1f | %.4f | %.4f | %.4f | %.4f | %.4f |" % (
             name, cnt, f, wr, rb / 1e9, wb / 1e9, alg_r / 1e9, alg_w / 1e9,
             (rb + wb) / (alg_r + alg_w)))
-    lines += ["", "Values read by bench.py (roofline.traffic of the local-step kernel):", "",
-              "- kernel_source_hash: %s" % kernel_source_hash()]
-    if LOCAL_STEP_KERNEL in out and workload == "llama8b_s8":
-        lines.append("- hbm_bytes_per_launch: %.0f" % out[LOCAL_STEP_KERNEL])
-    lines.append("")
+    step = kernels[:-1]
+    lines += ["", "Values read by bench.py (roofline.traffic: the HBM bytes of one local step, "
+              "the kernels %s):" % ", ".join(k for k, _, _ in step), "",
+              "- kernel_source_hash: %s" % kernel_source_hash(),
+              "- hbm_bytes_per_local_step: %.0f" % sum(out[k] for k, _, _ in step), ""]
     return "\n".join(lines)
 
 
@@ -229,12 +227,14 @@ def W_ALL():
     return W.ALL
 
 
-def cpu_baseline(w, n_sample):
-    """The oracle as it stands, timed on the host's cores: one full round on
-    the first n_sample elements of the same shard (same generator, same
-    segments), split into one contiguous chunk per thread; every thread runs
-    the unchanged single-threaded oracle on its chunk (ctypes releases the
-    GIL).  Also the one-thread rate on the first chunk."""
+def cpu_baseline(w, n_sample, min_seconds=10.0, max_rounds=10000):
+    """The oracle as it stands, timed on the host's cores: rounds on the first
+    n_sample elements of the same shard (same generator, same segments),
+    split into one contiguous chunk per thread; every thread runs the
+    unchanged single-threaded oracle on its chunk (ctypes releases the GIL).
+    Rounds are repeated on the evolving state until min_seconds have passed,
+    so that the rate is taken over several seconds of CPU work.  Also the
+    one-thread rate of one round on the first chunk."""
     import copy
     from concurrent.futures import ThreadPoolExecutor
 
@@ -265,17 +265,23 @@ def cpu_baseline(w, n_sample):
     dt1 = time.perf_counter() - t0
     n1 = int(bounds[1] - bounds[0])
     del first
+    rounds = 0
     with ThreadPoolExecutor(T) as ex:
         t0 = time.perf_counter()
-        list(ex.map(run, jobs))
-        dt = time.perf_counter() - t0
-    return dict(value=round(n_sample * per_param / dt / 1e9, 4), unit="GB/s", cores=T,
-                kind="oracle", params_per_s=round(n_sample / dt, 1), seconds=round(dt, 3),
+        while True:
+            list(ex.map(run, jobs))
+            rounds += 1
+            dt = time.perf_counter() - t0
+            if dt >= min_seconds or rounds >= max_rounds:
+                break
+    return dict(value=round(rounds * n_sample * per_param / dt / 1e9, 4), unit="GB/s", cores=T,
+                kind="oracle", params_per_s=round(rounds * n_sample / dt, 1),
+                seconds=round(dt, 3), rounds=rounds,
                 one_thread_gbs=round(n1 * per_param / dt1 / 1e9, 4),
-                sample="one round with per-segment sums (A=%d, R=%d, G=%d, H=%d) on the first "
+                sample="%d rounds with per-segment sums (A=%d, R=%d, G=%d, H=%d) on the first "
                        "%d elements of the same shard, as %d contiguous chunks run concurrently, "
                        "one thread each, by the single-threaded C oracle" % (
-                           w.A, w.R, w.G, w.H, n_sample, T))
+                           rounds, w.A, w.R, w.G, w.H, n_sample, T))
 
 
 def main():
@@ -285,6 +291,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="llama8b_s8")
     ap.add_argument("--cpu-sample", type=int, default=64 << 20)
+    ap.add_argument("--cpu-seconds", type=float, default=10.0,
+                    help="the oracle leg repeats rounds on its sample for at least this long")
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--blocks-per-cu", type=int, default=0,
                     help="workgroups per CU for every kernel (0: the library's defaults)")
@@ -386,7 +394,7 @@ def main():
     fed_bytes = w.n * w.fedavg_bytes_per_param()
     achieved = step_bytes / (avg_step * 1e-3) / 1e9
     src_hash = kernel_source_hash()
-    traffic = read_traffic(src_hash)
+    traffic = read_traffic(args.workload, src_hash)
     out = {
         "metric": METRIC,
         "value": round(gbs, 2),
@@ -426,8 +434,9 @@ def main():
     torch.cuda.empty_cache()
     if not args.no_cpu:
         log("cpu baseline: oracle on %d elements" % args.cpu_sample)
-        out["cpu_baseline"] = cpu_baseline(w, args.cpu_sample)
-        log("cpu baseline done: %.1f s" % out["cpu_baseline"]["seconds"])
+        out["cpu_baseline"] = cpu_baseline(w, args.cpu_sample, args.cpu_seconds)
+        log("cpu baseline done: %d rounds in %.1f s" % (out["cpu_baseline"]["rounds"],
+                                                        out["cpu_baseline"]["seconds"]))
     else:
         out["cpu_baseline"] = None
     print(json.dumps(out), flush=True)

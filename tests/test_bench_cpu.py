@@ -51,13 +51,24 @@ def test_the_8b_round_moves_350_bytes_per_parameter():
     assert w.round_bytes() == 351_323_750_400
 
 
-def test_committed_traffic_summary_matches_the_kernel_source():
-    t = bench.read_traffic(bench.kernel_source_hash())
+BENCH_WORKLOADS = ["tiny", "llama8b_s8", "fedavg_heavy", "hsdp_s4", "stress"]
+
+
+@pytest.mark.parametrize("name", BENCH_WORKLOADS)
+def test_committed_traffic_summary_matches_the_kernel_source(name):
+    """Every benchmarked workload has a counter summary for the current
+    kernels, and a full-size local step moves close to its algorithmic bytes
+    (the 1 Mi-element round stays partly in the caches)."""
+    t = bench.read_traffic(name, bench.kernel_source_hash())
     if t is None:
-        pytest.skip("the committed traffic summary predates the current kernel source; "
-                    "bench.py reports roofline.traffic as null until it is retaken")
-    alg = W.llama8b_s8().n * W.llama8b_s8().step_bytes_per_param()
-    assert 1.0 <= t / alg < 1.01
+        pytest.skip("the committed traffic summary of %s predates the current kernel source; "
+                    "bench.py reports roofline.traffic as null until it is retaken" % name)
+    w = W.ALL[name]()
+    ratio = t / (w.n * w.step_bytes_per_param())
+    if w.n >= 1 << 26:
+        assert 0.98 <= ratio < 1.05
+    else:
+        assert 0.0 < ratio < 1.05
 
 
 def test_kernel_source_hash_ignores_comments(tmp_path, monkeypatch):
@@ -92,8 +103,8 @@ def test_trace_summary_format(tmp_path):
 
 
 def test_cpu_baseline_runs_the_oracle_on_host_threads():
-    sys.path.insert(0, os.path.join(ROOT, "tests"))
-    cb = bench.cpu_baseline(W.llama8b_s8(), 1 << 16)
+    cb = bench.cpu_baseline(W.llama8b_s8(), 1 << 16, min_seconds=0.5)
     assert cb["kind"] == "oracle" and cb["unit"] == "GB/s"
+    assert cb["rounds"] >= 1 and cb["seconds"] >= 0.5
     assert cb["cores"] >= 1 and cb["value"] > 0 and cb["one_thread_gbs"] > 0
     assert "%d elements" % (1 << 16) in cb["sample"]
