@@ -354,7 +354,9 @@ def main():
 
     stream = torch.cuda.current_stream()
     K, Wm = args.steps, args.warmup
-    events = [P.HipEvents(w.A + 2) for _ in range(K)]
+    # phase events only time the kernels between them: recorded without the
+    # system-scope cache fence, which would add a cache write-back per event
+    events = [P.HipEvents(w.A + 2, P.HIP_EVENT_DISABLE_SYSTEM_FENCE) for _ in range(K)]
     # every round also returns the per-segment sums of squares of each local
     # step's reduced gradient (A x n_seg floats)
     seg_sumsq = torch.empty(w.A * w.n_seg, dtype=torch.float32, device="cuda")

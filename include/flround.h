@@ -89,15 +89,17 @@ int fl_version(void);
  *   or NULL for "every segment decays".  Uploads small per-segment and
  *   per-tile tables (about 16 bytes per 2048 elements) to the current device,
  *   and allocates the workspace of the per-segment sums of squares (32 bytes
- *   per (2048-element tile, segment) pair, plus 8 per segment; zeroed once);
- *   returns FL_ERR_NOMEM / FL_ERR_HIP if that fails.  *out receives a handle
- *   that may be used from several streams at once.
- *   The workspace serves the calls of one stream at a time: a call that needs
- *   it (seg_sumsq given, or clipping) uses it when it is free and the last
- *   call that used it was on the same stream (the two are then ordered);
- *   otherwise -- another stream, two host threads at once, or a stream being
- *   captured into a HIP graph -- the call takes a stream-ordered temporary of
- *   the same size instead, allocated and freed on its stream.
+ *   per (2048-element tile, segment) pair -- twice that when there are at
+ *   most 8 segments of at most 1024 tiles each -- plus 8 per segment and per
+ *   1024-tile chunk of a segment; zeroed once); returns FL_ERR_NOMEM /
+ *   FL_ERR_HIP if that fails.  *out receives a handle that may be used from
+ *   several streams at once.
+ *   The workspace serves one call at a time: a call that needs it (seg_sumsq
+ *   given, or clipping) uses it when no other host thread's call holds it,
+ *   after making its stream wait for the kernels of the last call that used
+ *   it when that call ran on another stream; a call made while it is held,
+ *   or on a stream being captured into a HIP graph, takes a stream-ordered
+ *   temporary of the same size instead, allocated and freed on its stream.
  * fl_layout_destroy: frees the handle and its device tables (NULL is OK).
  *   The caller must ensure no enqueued call still uses it.
  * ---------------------------------------------------------------------- */
@@ -136,10 +138,13 @@ typedef struct {
  * seg_sumsq: NULL, or device pointer to n_seg floats receiving, per segment,
  *   the sum of grad_out[i]^2 (exact double squares, fixed-tree double sums,
  *   rounded once to float): per-layer gradient-norm telemetry.  Uses the
- *   layout's workspace (see fl_layout_create).  When every segment spans at
- *   most 1024 tiles and there are at most 8 segments, the workgroup of the
- *   pass that finishes last computes the per-segment totals (the same fixed
- *   trees, the same bits) in place of a separate finalize launch.
+ *   layout's workspace (see fl_layout_create).  A small finalize kernel
+ *   folds the pass's per-tile partials into the per-segment totals.  In
+ *   fl_round, fl_round_outer, fl_round_noalloc and fl_round_hsdp, when every
+ *   segment spans at most 1024 tiles and there are at most 8 segments, one
+ *   extra workgroup of the round's next kernel (the next step, or the
+ *   FedAvg or broadcast pass) does that fold instead, with the same fixed
+ *   trees and the same bits, while the rest of the kernel streams.
  * 1 <= R <= FL_MAX_PEERS; grad_scale finite.
  * ---------------------------------------------------------------------- */
 int fl_shard_reduce(const fl_layout* layout, int R, const uint16_t* const* peer_grads,
@@ -271,12 +276,12 @@ int fl_round(const fl_layout* layout, const fl_round_cfg* cfg, const uint16_t* c
  * Every fl_round_noalloc call on one GPU shares that array: calls that
  * overlap in time on one GPU (two streams, two host threads) race and give
  * undefined results; calls on one stream are ordered and safe.
- * A layout whose workspace (32 bytes per (2048-element tile, segment) pair,
- * plus 8 per segment and per finalize chunk, plus 264) exceeds the array
- * returns FL_ERR_SCRATCH before anything is enqueued, when the call needs the
- * workspace; with neither seg_sumsq nor clipping any layout is accepted.
- * The array's address on a GPU is looked up, and its counter cleared, by the
- * first fl_layout_create on that GPU.
+ * A layout whose workspace (as in fl_layout_create, plus 8 bytes) exceeds
+ * the array returns FL_ERR_SCRATCH before anything is enqueued, when the call
+ * needs the workspace; with neither seg_sumsq nor clipping any layout is
+ * accepted.  Nothing in the array needs clearing: every slot a call reads it
+ * has written first.  The array's address on a GPU is looked up by the first
+ * fl_layout_create on that GPU.
  * fl_noalloc_workspace_bytes returns the bytes a layout would need (0 for
  * NULL or an empty layout).
  * ---------------------------------------------------------------------- */

@@ -12,7 +12,7 @@ constexpr int kVec = 8;                // elements per thread per tile (16 B of 
 constexpr int kTile = kBlock * kVec;   // elements per tile: 2048
 constexpr int kWaves = kBlock / 64;    // wave64s per workgroup: one partial slot each
 constexpr int kChunkPieces = 1024;    // pieces folded by one workgroup in the finalize
-constexpr int kFoldMaxChunks = 8;     // finalize folded into the pass up to this many chunks
+constexpr int kCarryMaxChunks = 8;    // finalize carried by the next kernel up to this many chunks
 constexpr int kMaxPeers = 64;
 constexpr int kMaxGroups = 64;
 
@@ -47,6 +47,19 @@ struct LayoutDev {
                               // [seg_chunk0[s], seg_chunk0[s+1])
 };
 
+// The finalize of the previous pass of a call, carried by the call's next
+// kernel: that kernel runs one extra workgroup (its last) which folds the
+// (piece, wave) partials the previous pass wrote, with the trees of
+// k_seg_chunks, while the other workgroups stream.  Only for layouts whose
+// every segment is one finalize chunk (chunk c is segment c) and that have at
+// most kCarryMaxChunks of them.  partials == null: nothing carried.
+struct Carry {
+  const double* partials;
+  const int64_t* chunk_p0;  // n_chunks + 1
+  int64_t n_chunks;
+  float* out;               // n_chunks floats: the per-segment sums
+};
+
 // Per-step AdamW scalars, computed on the host in double, rounded to float.
 struct AdamScalars {
   float b1, omb1, b2, omb2;
@@ -71,15 +84,7 @@ struct StepArgs {
                        // (null: not requested)
   const double* clip_total;  // MODE 0: whole-shard sum of squares, clipping on
   float clip_max;            // its max norm
-  // Finalize folded into the pass (null: separate finalize kernels).  Only
-  // for layouts whose every segment is one finalize chunk and that have at
-  // most kFoldMaxChunks of them.  fold_counter must read 0 when the pass
-  // starts; the workgroup that finishes last folds the partials exactly as
-  // k_seg_chunks and k_total do and sets it back to 0.
-  unsigned* fold_counter;
-  double* fold_seg;     // n_seg doubles: per-segment totals
-  float* fold_out;      // n_seg floats (may be null)
-  double* fold_total;   // whole-shard total (may be null)
+  Carry carry;
 };
 
 struct FedArgs {
@@ -94,15 +99,25 @@ struct FedArgs {
   float* buf;
   float eta, mu;
   int nesterov;
+  Carry carry;
+};
+
+struct BcastArgs {
+  int64_t n;
+  const float* recv;
+  float* master;
+  uint16_t* working;
+  Carry carry;
 };
 
 hipError_t launch_local_step(const StepArgs& a, int grid, hipStream_t st);
 hipError_t launch_reduce(const StepArgs& a, int grid, hipStream_t st);
 hipError_t launch_adamw(const StepArgs& a, int grid, hipStream_t st);
 hipError_t launch_reduce_wire(const StepArgs& a, int grid, hipStream_t st);
-hipError_t launch_bcast_recv(int64_t n, const float* recv, float* master, uint16_t* working,
-                             int grid, hipStream_t st);
+hipError_t launch_bcast_recv(const BcastArgs& a, int grid, hipStream_t st);
 hipError_t launch_fedavg(const FedArgs& a, int grid, hipStream_t st);
+// The launch helpers take `grid` workgroups for the stream and add one for a
+// carried finalize (a.carry.partials set).
 // Per-segment totals from the (piece, wave) partials: chunk_sums
 // (L.n_chunks doubles) and seg_dbl (L.n_seg doubles) are temporaries; out
 // (n_seg floats) and total (one double, the whole shard) may be null.
@@ -110,12 +125,11 @@ hipError_t launch_seg_finalize(const LayoutDev& L, const double* partials, doubl
                                double* seg_dbl, float* out, double* total, hipStream_t st);
 hipError_t launch_sumsq_only(const StepArgs& a, int grid, hipStream_t st);
 
-// The static scratch of fl_round_noalloc (kNoallocScratchBytes per GPU; the
-// first kNoallocHeadBytes hold the folded finalize's counter).  The first
-// call for a device, with that device current, looks up the array's address
-// on it and clears the counter; later calls return the cached address.
+// The static scratch of fl_round_noalloc (kNoallocScratchBytes per GPU).
+// The first call for a device, with that device current, looks up the
+// array's address on it; later calls return the cached address.  Nothing in
+// it needs to start at zero: every slot is written before it is read.
 constexpr size_t kNoallocScratchBytes = (size_t)32 << 20;
-constexpr size_t kNoallocHeadBytes = 256;
 hipError_t noalloc_scratch(int device, void** ptr);
 hipError_t launch_zero_total(double* total, hipStream_t st);
 

@@ -207,49 +207,55 @@ int check_peers(int R, const uint16_t* const* peers, int64_t n) {
   return FL_OK;
 }
 
+// Whether a pass's finalize may be carried by the next kernel of the same
+// call (see flr::Carry): every segment one finalize chunk, few of them.
+bool carry_ok(const flr::LayoutDev& L) {
+  return L.n_chunks == L.n_seg && L.n_chunks >= 1 && L.n_chunks <= flr::kCarryMaxChunks;
+}
+
 // Workspace of the per-segment sums of squares: the (piece, wave) partials
-// (kWaves doubles per piece), one double per finalize chunk, one per segment,
-// the whole-shard total, and the counter of a finalize folded into the pass.
+// (kWaves doubles per piece; two sets where the finalize may be carried, so
+// that a pass writes one while the next kernel's carried finalize reads the
+// other), one double per finalize chunk, one per segment, and the
+// whole-shard total.
 size_t ws_slots(const flr::LayoutDev& L) {
   return (size_t)(L.n_pieces > 0 ? L.n_pieces : 1) * flr::kWaves;
 }
 size_t ws_bytes(const flr::LayoutDev& L) {
   const size_t nch = (size_t)(L.n_chunks > 0 ? L.n_chunks : 1);
   const size_t nseg = (size_t)(L.n_seg > 0 ? L.n_seg : 1);
-  return (ws_slots(L) + nch + nseg + 1 + 1) * sizeof(double);
+  return (ws_slots(L) * (carry_ok(L) ? 2 : 1) + nch + nseg + 1) * sizeof(double);
 }
 
 struct Workspace {
   double* p = nullptr;
+  double* p2 = nullptr;         // the second set of partials (null: no carry)
   double* chunks = nullptr;
   double* seg = nullptr;
   double* total = nullptr;
-  unsigned* counter = nullptr;  // null: no folded finalize
   hipStream_t st = nullptr;
   fl_layout* owner = nullptr;   // the layout whose workspace this is (or null)
   void* own = nullptr;          // a stream-ordered allocation of this call
 
-  // The static scratch of fl_round_noalloc: the counter in its head, the
-  // rest after it.  Nothing is allocated and nothing needs releasing.
+  // The static scratch of fl_round_noalloc.  Nothing is allocated and
+  // nothing needs releasing.
   int use_static(const fl_layout* lay, hipStream_t stream) {
     st = stream;
     if (!lay->noalloc) return FL_ERR_HIP;
-    char* base = static_cast<char*>(lay->noalloc);
-    carve(lay->L, base + flr::kNoallocHeadBytes);
-    counter = reinterpret_cast<unsigned*>(base);
+    carve(lay->L, lay->noalloc);
     return FL_OK;
   }
 
   void carve(const flr::LayoutDev& L, void* mem) {
     p = static_cast<double*>(mem);
-    chunks = p + ws_slots(L);
+    p2 = carry_ok(L) ? p + ws_slots(L) : nullptr;
+    chunks = p + ws_slots(L) * (p2 ? 2 : 1);
     seg = chunks + (L.n_chunks > 0 ? L.n_chunks : 1);
     total = seg + (L.n_seg > 0 ? L.n_seg : 1);
-    counter = reinterpret_cast<unsigned*>(total + 1);
   }
 
   // The layout's workspace when this stream may use it, else a stream-ordered
-  // allocation (without the fold counter, which would need zeroing).
+  // allocation.
   int acquire(const fl_layout* layc, hipStream_t stream) {
     fl_layout* lay = const_cast<fl_layout*>(layc);
     st = stream;
@@ -259,15 +265,20 @@ struct Workspace {
     if (cs == hipStreamCaptureStatusNone && lay->ws_mem &&
         lay->ws_busy.compare_exchange_strong(expected, true, std::memory_order_acquire)) {
       if (!lay->ws_recorded || lay->ws_stream == stream) {
-        if (lay->ws_recorded && hipStreamWaitEvent(stream, lay->ws_done, 0) != hipSuccess) {
-          lay->ws_busy.store(false, std::memory_order_release);
-          return FL_ERR_HIP;
-        }
+        // the last call that used it ran on this stream: stream order
+        // already puts its kernels first
+        owner = lay;
+        carve(lay->L, lay->ws_mem);
+        return FL_OK;
+      }
+      if (hipStreamWaitEvent(stream, lay->ws_done, 0) == hipSuccess) {
+        // another stream used it last: this stream waits for those kernels
         owner = lay;
         carve(lay->L, lay->ws_mem);
         return FL_OK;
       }
       lay->ws_busy.store(false, std::memory_order_release);
+      return FL_ERR_HIP;
     }
     const hipError_t e = hipMallocAsync(&own, ws_bytes(lay->L), st);
     if (e != hipSuccess) {
@@ -275,7 +286,6 @@ struct Workspace {
       return status_of(e);
     }
     carve(lay->L, own);
-    counter = nullptr;
     return FL_OK;
   }
 
@@ -297,34 +307,43 @@ struct Workspace {
       rc = status_of(hipFreeAsync(own, st));
       own = nullptr;
     }
-    p = chunks = seg = total = nullptr;
-    counter = nullptr;
+    p = p2 = chunks = seg = total = nullptr;
     return rc;
   }
 };
 
 // Bytes of the static scratch a layout's workspace needs in fl_round_noalloc.
-size_t noalloc_bytes(const flr::LayoutDev& L) {
-  return flr::kNoallocHeadBytes + ws_bytes(L) - sizeof(double);
+size_t noalloc_bytes(const flr::LayoutDev& L) { return ws_bytes(L); }
+
+// The partials set for a pass: the one a carried finalize in the same launch
+// does not read.
+double* free_slot(const Workspace& ws, const flr::Carry& c) {
+  return (ws.p2 && c.partials == ws.p) ? ws.p2 : ws.p;
 }
 
-// Whether a pass with per-segment sums folds its finalize (every segment one
-// finalize chunk, few of them, and a zeroed counter to count workgroups).
-bool fold_ok(const flr::LayoutDev& L, const Workspace& ws) {
-  return ws.counter != nullptr && L.n_chunks == L.n_seg && L.n_chunks >= 1 &&
-         L.n_chunks <= flr::kFoldMaxChunks;
+// Move a pending carried finalize into a kernel's arguments.
+template <typename Args>
+void take_carry(Args& a, flr::Carry* pending) {
+  if (pending && pending->partials) {
+    a.carry = *pending;
+    pending->partials = nullptr;
+  }
 }
 
-// Point a pass with per-segment sums at its finalize outputs: folded into the
-// pass when fold_ok, else left to launch_seg_finalize (returns false).
-bool set_fold(flr::StepArgs& a, const fl_layout* lay, const Workspace& ws, float* out,
-              bool total) {
-  if (!fold_ok(lay->L, ws)) return false;
-  a.fold_counter = ws.counter;
-  a.fold_seg = ws.seg;
-  a.fold_out = out;
-  a.fold_total = total ? ws.total : nullptr;
-  return true;
+// After a pass with per-segment sums: leave the finalize to the next kernel
+// of the call (pending non-null and the layout allows it), else enqueue the
+// finalize kernels now.
+int finish_sums(const fl_layout* lay, const Workspace& ws, double* partials, float* out,
+                flr::Carry* pending, hipStream_t st) {
+  if (pending && ws.p2) {
+    pending->partials = partials;
+    pending->chunk_p0 = lay->L.chunk_p0;
+    pending->n_chunks = lay->L.n_chunks;
+    pending->out = out;
+    return FL_OK;
+  }
+  return status_of(flr::launch_seg_finalize(lay->L, partials, ws.chunks, ws.seg, out, nullptr,
+                                            st));
 }
 
 flr::StepArgs step_args(const fl_layout* lay) {
@@ -341,24 +360,28 @@ flr::StepArgs step_args(const fl_layout* lay) {
 // g_scratch (N floats), the first pass also stores the reduced gradient and
 // the step is the AdamW-only pass over it, so the peer gradients are read
 // once: 2R + 4 then 30 bytes per element instead of 2R then 2R + 26.
+// pending (may be null): the finalize carried between the kernels of one
+// call; the first kernel enqueued here runs the one pending, and an
+// unclipped step with per-segment sums may leave its own there.
 int enqueue_local_step(const fl_layout* lay, const fl_adamw_hparams& h, int64_t step, int R,
                        const uint16_t* const* peers, float grad_scale, float* master, float* m,
                        float* v, uint16_t* working, const Workspace& ws, float* seg_sumsq,
-                       hipStream_t st, float clip_max = 0.f, float* g_scratch = nullptr) {
+                       hipStream_t st, float clip_max = 0.f, float* g_scratch = nullptr,
+                       flr::Carry* pending = nullptr) {
   flr::StepArgs a = step_args(lay);
   for (int r = 0; r < R; ++r) a.grads[r] = peers[r];
   a.R = R;
   a.grad_scale = grad_scale;
   const int grid = grid_for(lay, lay->L.n_tiles);
   int rc = FL_OK;
+  take_carry(a, pending);
   if (clip_max > 0.f && g_scratch) {
-    a.partials = ws.p;
+    a.partials = free_slot(ws, a.carry);
     a.g_out = g_scratch;
-    const bool folded = set_fold(a, lay, ws, seg_sumsq, true);
     rc = status_of(flr::launch_reduce(a, grid_for(lay, lay->L.n_tiles, reduce_blocks_per_cu(R)),
                                       st));
-    if (rc == FL_OK && !folded)
-      rc = status_of(flr::launch_seg_finalize(lay->L, ws.p, ws.chunks, ws.seg, seg_sumsq,
+    if (rc == FL_OK)
+      rc = status_of(flr::launch_seg_finalize(lay->L, a.partials, ws.chunks, ws.seg, seg_sumsq,
                                               ws.total, st));
     flr::StepArgs b = step_args(lay);
     b.s = adam_scalars(h, step);
@@ -373,15 +396,14 @@ int enqueue_local_step(const fl_layout* lay, const fl_adamw_hparams& h, int64_t 
     return rc;
   }
   if (clip_max > 0.f) {
-    a.partials = ws.p;
-    const bool folded = set_fold(a, lay, ws, seg_sumsq, true);
+    a.partials = free_slot(ws, a.carry);
     rc = status_of(flr::launch_sumsq_only(a, grid_for(lay, lay->L.n_tiles,
                                                       sumsq_blocks_per_cu(R)), st));
-    if (rc == FL_OK && !folded)
-      rc = status_of(flr::launch_seg_finalize(lay->L, ws.p, ws.chunks, ws.seg, seg_sumsq,
+    if (rc == FL_OK)
+      rc = status_of(flr::launch_seg_finalize(lay->L, a.partials, ws.chunks, ws.seg, seg_sumsq,
                                               ws.total, st));
     a.partials = nullptr;
-    a.fold_counter = nullptr;
+    a.carry = flr::Carry{};
     a.clip_total = ws.total;
     a.clip_max = clip_max;
     seg_sumsq = nullptr;
@@ -391,15 +413,9 @@ int enqueue_local_step(const fl_layout* lay, const fl_adamw_hparams& h, int64_t 
   a.m = m;
   a.v = v;
   a.working = working;
-  bool folded = false;
-  if (seg_sumsq) {
-    a.partials = ws.p;
-    folded = set_fold(a, lay, ws, seg_sumsq, false);
-  }
+  if (seg_sumsq) a.partials = free_slot(ws, a.carry);
   if (rc == FL_OK) rc = status_of(flr::launch_local_step(a, grid, st));
-  if (rc == FL_OK && seg_sumsq && !folded)
-    rc = status_of(flr::launch_seg_finalize(lay->L, ws.p, ws.chunks, ws.seg, seg_sumsq, nullptr,
-                                            st));
+  if (rc == FL_OK && seg_sumsq) rc = finish_sums(lay, ws, a.partials, seg_sumsq, pending, st);
   return rc;
 }
 
@@ -411,9 +427,10 @@ bool outer_ok(const fl_outer_hparams* o) {
 int enqueue_fedavg(const fl_layout* lay, int G, const uint16_t* const* reps, const float* wn,
                    float* master, uint16_t* working, hipStream_t st,
                    const fl_outer_hparams* outer = nullptr, float* prev = nullptr,
-                   float* buf = nullptr) {
+                   float* buf = nullptr, flr::Carry* pending = nullptr) {
   flr::FedArgs f;
   std::memset(&f, 0, sizeof f);
+  take_carry(f, pending);
   if (outer) {
     f.prev = prev;
     f.buf = buf;
@@ -430,6 +447,18 @@ int enqueue_fedavg(const fl_layout* lay, int G, const uint16_t* const* reps, con
   f.master = master;
   f.working = working;
   return status_of(flr::launch_fedavg(f, fedavg_grid(lay), st));
+}
+
+int enqueue_bcast(const fl_layout* lay, const float* recv, float* master, uint16_t* working,
+                  hipStream_t st, flr::Carry* pending = nullptr) {
+  flr::BcastArgs b;
+  std::memset(&b, 0, sizeof b);
+  take_carry(b, pending);
+  b.n = lay->L.n;
+  b.recv = recv;
+  b.master = master;
+  b.working = working;
+  return status_of(flr::launch_bcast_recv(b, fedavg_grid(lay), st));
 }
 
 }  // namespace
@@ -652,10 +681,9 @@ int fl_shard_reduce(const fl_layout* layout, int R, const uint16_t* const* peer_
   a.grad_scale = grad_scale;
   a.g_out = grad_out;
   a.partials = ws.p;
-  const bool folded = seg_sumsq && set_fold(a, layout, ws, seg_sumsq, false);
   rc = status_of(flr::launch_reduce(a, grid_for(layout, layout->L.n_tiles,
                                                 reduce_blocks_per_cu(R)), st));
-  if (rc == FL_OK && seg_sumsq && !folded)
+  if (rc == FL_OK && seg_sumsq)
     rc = status_of(flr::launch_seg_finalize(layout->L, ws.p, ws.chunks, ws.seg, seg_sumsq,
                                             nullptr, st));
   const int rc2 = ws.release();
@@ -751,11 +779,9 @@ int fl_grad_sumsq(const fl_layout* layout, int R, const uint16_t* const* peer_gr
   a.R = R;
   a.grad_scale = grad_scale;
   a.partials = ws.p;
-  const bool folded = set_fold(a, layout, ws, seg_sumsq, true);
-  if (folded) a.fold_total = total_sumsq;
   rc = status_of(flr::launch_sumsq_only(a, grid_for(layout, layout->L.n_tiles,
                                                     sumsq_blocks_per_cu(R)), st));
-  if (rc == FL_OK && !folded)
+  if (rc == FL_OK)
     rc = status_of(flr::launch_seg_finalize(layout->L, ws.p, ws.chunks, ws.seg, seg_sumsq,
                                             total_sumsq, st));
   const int rc2 = ws.release();
@@ -825,8 +851,7 @@ int fl_broadcast_recv(const fl_layout* layout, const float* recv_master, float* 
   if ((rc = dev_ptr(working, n)) != FL_OK) return rc;
   if ((rc = check_device(layout)) != FL_OK) return rc;
   if (n == 0) return FL_OK;
-  return status_of(flr::launch_bcast_recv(n, recv_master, master, working, fedavg_grid(layout),
-                                          static_cast<hipStream_t>(stream)));
+  return enqueue_bcast(layout, recv_master, master, working, static_cast<hipStream_t>(stream));
 }
 
 int fl_round_hsdp(const fl_layout* layout, const fl_round_cfg* cfg, const fl_hsdp_cfg* hc,
@@ -907,6 +932,7 @@ int fl_round_hsdp(const fl_layout* layout, const fl_round_cfg* cfg, const fl_hsd
   Workspace ws;
   if (n > 0 && (seg_sumsq || c.max_grad_norm > 0.f) && (rc = ws.acquire(layout, st)) != FL_OK)
     return rc;
+  flr::Carry pending{};  // a step's finalize, run by the call's next kernel
   for (int a = 0; a < c.A && rc == FL_OK; ++a) {
     rc = record(a);
     if (rc != FL_OK || n == 0) continue;
@@ -914,7 +940,8 @@ int fl_round_hsdp(const fl_layout* layout, const fl_round_cfg* cfg, const fl_hsd
     const uint16_t* const* ga = grads + (size_t)a * (size_t)c.R;
     if (hc->H == 1) {
       rc = enqueue_local_step(layout, step_hparams(c, a), c.step0 + a, c.R, ga, c.grad_scale,
-                              master, m, v, working, ws, ss, st, c.max_grad_norm, g_scratch);
+                              master, m, v, working, ws, ss, st, c.max_grad_norm, g_scratch,
+                              &pending);
       continue;
     }
     // tier 1: the sharding group's reduction, in the bf16 wire format
@@ -932,15 +959,16 @@ int fl_round_hsdp(const fl_layout* layout, const fl_round_cfg* cfg, const fl_hsd
       wires[k] = (k == hc->replica) ? wire : replica_wires[(size_t)a * (size_t)hc->H + (size_t)k];
     if (rc == FL_OK)
       rc = enqueue_local_step(layout, step_hparams(c, a), c.step0 + a, hc->H, wires,
-                              hc->hsdp_scale, master, m, v, working, ws, ss, st, c.max_grad_norm);
+                              hc->hsdp_scale, master, m, v, working, ws, ss, st, c.max_grad_norm,
+                              nullptr, &pending);
   }
   if (rc == FL_OK) rc = record(c.A);
   if (rc == FL_OK && n > 0) {
     if (member)
-      rc = enqueue_fedavg(layout, c.G, reps, wn, master, working, st);
+      rc = enqueue_fedavg(layout, c.G, reps, wn, master, working, st, nullptr, nullptr, nullptr,
+                          &pending);
     else
-      rc = status_of(flr::launch_bcast_recv(n, bcast_master, master, working, fedavg_grid(layout),
-                                            st));
+      rc = enqueue_bcast(layout, bcast_master, master, working, st, &pending);
   }
   if (rc == FL_OK) rc = record(c.A + 1);
   const int rc2 = ws.release();
@@ -1078,17 +1106,18 @@ static int round_impl(const fl_layout* layout, const fl_round_cfg* cfg,
   Workspace ws;
   if (needs_ws && (rc = noalloc ? ws.use_static(layout, st) : ws.acquire(layout, st)) != FL_OK)
     return rc;
+  flr::Carry pending{};  // a step's finalize, run by the call's next kernel
   for (int a = 0; a < c.A && rc == FL_OK; ++a) {
     rc = record(a);
     if (rc == FL_OK && n > 0)
       rc = enqueue_local_step(layout, step_hparams(c, a), c.step0 + a, c.R,
                               grads + (size_t)a * (size_t)c.R, c.grad_scale, master, m, v, working, ws,
                               seg_sumsq ? seg_sumsq + (size_t)a * (size_t)layout->L.n_seg : nullptr,
-                              st, c.max_grad_norm, g_scratch);
+                              st, c.max_grad_norm, g_scratch, &pending);
   }
   if (rc == FL_OK) rc = record(c.A);
   if (rc == FL_OK && n > 0)
-    rc = enqueue_fedavg(layout, c.G, reps, wn, master, working, st, outer, prev, buf);
+    rc = enqueue_fedavg(layout, c.G, reps, wn, master, working, st, outer, prev, buf, &pending);
   if (rc == FL_OK) rc = record(c.A + 1);
   const int rc2 = ws.release();
   return rc != FL_OK ? rc : rc2;

@@ -195,44 +195,24 @@ __device__ __forceinline__ int find_seg(const int64_t* off, int lo, int hi, int6
   return lo;
 }
 
-// A (piece, wave) partial.  When the pass folds its finalize (coherent), it
-// is stored at device (agent) scope, so that it goes to the device's
-// coherence point instead of staying in one XCD's L2, where the workgroup
-// that folds could not see it; otherwise a plain store, read by a later
-// kernel.
-__device__ __forceinline__ void put_partial(double* p, double v, bool coherent) {
-  if (coherent)
-    __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  else
-    *p = v;
-}
-
 // Fixed-tree total of the (piece, wave) partials of finalize chunk c: thread
 // j folds pieces j, j + 256, ... (each piece's kWaves slots in order), a
 // wave64 butterfly, then the 4 wave totals in order.  Called by all threads
-// of the workgroup; the result is valid in thread 0.  COHERENT: read the
-// partials at device scope (the folded finalize, which runs in the pass
-// that wrote them); otherwise they were written by an earlier kernel.
-template <bool COHERENT>
-__device__ __forceinline__ double chunk_fold(const LayoutDev& L, const double* partials,
+// of the workgroup; the result is valid in thread 0.  The partials were
+// written by an earlier kernel.
+__device__ __forceinline__ double chunk_fold(const int64_t* chunk_p0, const double* partials,
                                              int64_t c, double* red) {
-  const int64_t p0 = L.chunk_p0[c];
-  const int64_t p1 = L.chunk_p0[c + 1];
+  const int64_t p0 = chunk_p0[c];
+  const int64_t p1 = chunk_p0[c + 1];
   double acc = 0.0;
   for (int64_t p = p0 + threadIdx.x; p < p1; p += kBlock) {
     const double* q = partials + p * kWaves;
-    if constexpr (COHERENT) {
-#pragma unroll
-      for (int k = 0; k < kWaves; ++k)
-        acc = acc + __hip_atomic_load(q + k, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    } else {
-      const f64x2 w0 = *reinterpret_cast<const f64x2*>(q);
-      const f64x2 w1 = *reinterpret_cast<const f64x2*>(q + 2);
-      acc = acc + w0.x;
-      acc = acc + w0.y;
-      acc = acc + w1.x;
-      acc = acc + w1.y;
-    }
+    const f64x2 w0 = *reinterpret_cast<const f64x2*>(q);
+    const f64x2 w1 = *reinterpret_cast<const f64x2*>(q + 2);
+    acc = acc + w0.x;
+    acc = acc + w0.y;
+    acc = acc + w1.x;
+    acc = acc + w1.y;
   }
   acc = wave_sum(acc);
   if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = acc;
@@ -257,41 +237,27 @@ __device__ __forceinline__ double total_fold(int64_t n_seg, Get get, double* red
   return sum;
 }
 
-// The finalize of a pass with few single-chunk segments, run by the
-// workgroup that finishes the pass last (see StepArgs::fold_counter): every
-// workgroup waits until its partials (device-scope stores) are complete and
-// then counts itself in with a device-scope atomic; the one that counts last
-// reads all partials at device scope and writes the per-segment totals (and
-// their float roundings, and the whole-shard total), with the trees of
-// k_seg_chunks and k_total, so the bits equal those of the separate finalize
-// kernels.  No fence flushes the L2s: only the partials cross workgroups.
-__device__ void fold_finalize(const StepArgs& a) {
+// A carried finalize (see Carry): the last workgroup of a kernel launched
+// with one extra workgroup folds the previous pass's partials, chunk by
+// chunk, with the tree of k_seg_chunks, and writes each segment's float sum;
+// returns true in that workgroup (which then has nothing else to do).  Every
+// workgroup calls it first; the others stream over work units blockIdx.x ..
+// in steps of gridDim.x - carried, exactly as without the extra workgroup.
+// That keeps the workgroup -> tile mapping, and so the XCD that touches each
+// tile, the same in consecutive kernels: at small shard sizes the next pass
+// then finds the tile in that XCD's L2.  The partials come from an earlier
+// kernel of the same stream, so plain loads see them.
+__device__ __forceinline__ bool run_carry(const Carry& c) {
+  if (c.partials == nullptr || blockIdx.x != gridDim.x - 1) return false;
   __shared__ double red[4];
-  __shared__ double segs[kFoldMaxChunks];
-  __shared__ int last;
-  __builtin_amdgcn_s_waitcnt(0);  // this wave's partial stores have completed
-  __syncthreads();
-  if (threadIdx.x == 0)
-    last = __hip_atomic_fetch_add(a.fold_counter, 1u, __ATOMIC_RELAXED,
-                                  __HIP_MEMORY_SCOPE_AGENT) == gridDim.x - 1;
-  __syncthreads();
-  if (!last) return;
-  for (int64_t c = 0; c < a.L.n_chunks; ++c) {
-    const double sum = chunk_fold<true>(a.L, a.partials, c, red);
-    if (threadIdx.x == 0) {
-      segs[c] = sum;
-      a.fold_seg[c] = sum;
-      if (a.fold_out) a.fold_out[c] = (float)sum;
-    }
+  for (int64_t k = 0; k < c.n_chunks; ++k) {
+    const double sum = chunk_fold(c.chunk_p0, c.partials, k, red);
+    if (threadIdx.x == 0) c.out[k] = (float)sum;
   }
-  __syncthreads();
-  if (a.fold_total) {
-    const double tot = total_fold(a.L.n_seg, [&](int64_t s) { return segs[s]; }, red);
-    if (threadIdx.x == 0) *a.fold_total = tot;
-  }
-  if (threadIdx.x == 0)
-    __hip_atomic_store(a.fold_counter, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  return true;
 }
+
+__device__ __forceinline__ int carried(const Carry& c) { return c.partials != nullptr ? 1 : 0; }
 
 // MODE 0: fused reduce + AdamW + working copy; 1: reduce only (g_out); 2:
 // AdamW only (g_in); 3: reduce to the bf16 wire format (wire_out); 4: reduce
@@ -303,8 +269,9 @@ __global__ void __launch_bounds__(kBlock) k_step(const StepArgs a) {
   const int tid = threadIdx.x;
   const bool clip = (MODE == 0 || MODE == 2) && a.clip_total != nullptr;
   const float coef = clip ? clip_coef(a.clip_total, a.clip_max) : 1.0f;
-  const bool fold = SUMSQ && a.fold_counter != nullptr;
-  for (int64_t t = blockIdx.x; t < a.L.n_tiles; t += gridDim.x) {
+  if (run_carry(a.carry)) return;
+  const int cw = carried(a.carry);
+  for (int64_t t = blockIdx.x; t < a.L.n_tiles; t += (int64_t)gridDim.x - cw) {
     const TileInfo ti = a.L.tiles[t];
     const int64_t base = t * kTile + (int64_t)tid * kVec;
     const int64_t left = a.L.n - base;
@@ -410,7 +377,7 @@ __global__ void __launch_bounds__(kBlock) k_step(const StepArgs a) {
 #pragma unroll
         for (int e = 0; e < 8; ++e) if (e < cnt) acc = acc + (double)g[e] * (double)g[e];
         const double tot = wave_sum(acc);
-        if ((tid & 63) == 0) put_partial(a.partials + (int64_t)ti.piece0 * kWaves + wid, tot, fold);
+        if ((tid & 63) == 0) a.partials[(int64_t)ti.piece0 * kWaves + wid] = tot;
       } else {
         for (int j = 0; j < ti.nseg; ++j) {
           const int sj = ti.seg0 + j;
@@ -419,14 +386,10 @@ __global__ void __launch_bounds__(kBlock) k_step(const StepArgs a) {
           for (int e = 0; e < 8; ++e)
             if (e < cnt && seg[e] == sj) acc = acc + (double)g[e] * (double)g[e];
           const double tot = wave_sum(acc);
-          if ((tid & 63) == 0) put_partial(a.partials + ((int64_t)ti.piece0 + j) * kWaves + wid, tot,
-                                            fold);
+          if ((tid & 63) == 0) a.partials[((int64_t)ti.piece0 + j) * kWaves + wid] = tot;
         }
       }
     }
-  }
-  if constexpr (SUMSQ) {
-    if (a.fold_counter) fold_finalize(a);
   }
 }
 
@@ -438,8 +401,10 @@ __global__ void __launch_bounds__(kBlock) k_step(const StepArgs a) {
 // bits as MODE 3.
 template <int RT>
 __global__ void __launch_bounds__(kBlock) k_wire(const StepArgs a) {
+  if (run_carry(a.carry)) return;
+  const int cw = carried(a.carry);
   const int64_t nvec = (a.L.n + kVec - 1) / kVec;
-  const int64_t stride = (int64_t)gridDim.x * kBlock;
+  const int64_t stride = ((int64_t)gridDim.x - cw) * kBlock;
   for (int64_t v0 = (int64_t)blockIdx.x * kBlock + threadIdx.x; v0 < nvec; v0 += 2 * stride) {
     const int64_t v1 = v0 + stride;
     const int64_t b0 = v0 * kVec, b1 = v1 * kVec;
@@ -488,8 +453,10 @@ __global__ void __launch_bounds__(kBlock) k_wire(const StepArgs a) {
 //   master = prev = p; working = bf16(p).
 template <int GT, bool OUTER>
 __global__ void __launch_bounds__(kBlock) k_fedavg(const FedArgs a) {
+  if (run_carry(a.carry)) return;
+  const int cw = carried(a.carry);
   const int64_t nvec = (a.n + kVec - 1) / kVec;
-  const int64_t stride = (int64_t)gridDim.x * kBlock;
+  const int64_t stride = ((int64_t)gridDim.x - cw) * kBlock;
   for (int64_t vi = (int64_t)blockIdx.x * kBlock + threadIdx.x; vi < nvec; vi += stride) {
     const int64_t base = vi * kVec;
     const int64_t left = a.n - base;
@@ -579,7 +546,7 @@ __global__ void __launch_bounds__(kBlock) k_seg_chunks(const LayoutDev L, const 
                                                        double* chunk_sums, float* out) {
   __shared__ double red[4];
   for (int64_t c = blockIdx.x; c < L.n_chunks; c += gridDim.x) {
-    const double sum = chunk_fold<false>(L, partials, c, red);
+    const double sum = chunk_fold(L.chunk_p0, partials, c, red);
     if (threadIdx.x == 0) {
       chunk_sums[c] = sum;
       if (DIRECT && out) out[c] = (float)sum;
@@ -606,35 +573,39 @@ __global__ void __launch_bounds__(kBlock) k_total(const int64_t n_seg, const dou
 }
 
 // Broadcast receive: master = recv; working = bf16(recv).
-__global__ void __launch_bounds__(kBlock) k_bcast_recv(const int64_t n, const float* recv,
-                                                       float* master, uint16_t* working) {
+__global__ void __launch_bounds__(kBlock) k_bcast_recv(const BcastArgs a) {
+  if (run_carry(a.carry)) return;
+  const int cw = carried(a.carry);
+  const int64_t n = a.n;
   const int64_t nvec = (n + kVec - 1) / kVec;
-  const int64_t stride = (int64_t)gridDim.x * kBlock;
+  const int64_t stride = ((int64_t)gridDim.x - cw) * kBlock;
   for (int64_t vi = (int64_t)blockIdx.x * kBlock + threadIdx.x; vi < nvec; vi += stride) {
     const int64_t base = vi * kVec;
     const int64_t left = n - base;
     if (left >= kVec) {
       float x[8];
-      const f32x4 a = ld_once(reinterpret_cast<const f32x4*>(recv + base));
-      const f32x4 b = ld_once(reinterpret_cast<const f32x4*>(recv + base + 4));
-      x[0] = a.x; x[1] = a.y; x[2] = a.z; x[3] = a.w;
-      x[4] = b.x; x[5] = b.y; x[6] = b.z; x[7] = b.w;
-      store_f32x8(master + base, x);
-      st(reinterpret_cast<u32x4*>(working + base), pack_bf16x8(x));
+      const f32x4 u = ld_once(reinterpret_cast<const f32x4*>(a.recv + base));
+      const f32x4 w = ld_once(reinterpret_cast<const f32x4*>(a.recv + base + 4));
+      x[0] = u.x; x[1] = u.y; x[2] = u.z; x[3] = u.w;
+      x[4] = w.x; x[5] = w.y; x[6] = w.z; x[7] = w.w;
+      store_f32x8(a.master + base, x);
+      st(reinterpret_cast<u32x4*>(a.working + base), pack_bf16x8(x));
     } else {
       for (int e = 0; e < (int)left; ++e) {
-        const float x = recv[base + e];
-        master[base + e] = x;
-        working[base + e] = (uint16_t)to_bf16(x);
+        const float x = a.recv[base + e];
+        a.master[base + e] = x;
+        a.working[base + e] = (uint16_t)to_bf16(x);
       }
     }
   }
 }
 
+// grid workgroups for the stream, plus one for a carried finalize.
 template <typename Args>
 hipError_t launch(const void* fn, const Args& a, int grid, hipStream_t st) {
   void* args[] = {const_cast<Args*>(&a)};
-  return hipLaunchKernel(fn, dim3((unsigned)grid), dim3(kBlock), args, 0, st);
+  const unsigned g = (unsigned)grid + (a.carry.partials != nullptr ? 1u : 0u);
+  return hipLaunchKernel(fn, dim3(g), dim3(kBlock), args, 0, st);
 }
 
 template <int MODE, bool SUMSQ>
@@ -670,11 +641,8 @@ hipError_t launch_reduce_wire(const StepArgs& a, int grid, hipStream_t st) {
   }
 }
 
-hipError_t launch_bcast_recv(int64_t n, const float* recv, float* master, uint16_t* working,
-                             int grid, hipStream_t st) {
-  void* args[] = {&n, &recv, &master, &working};
-  return hipLaunchKernel((const void*)k_bcast_recv, dim3((unsigned)grid), dim3(kBlock), args, 0,
-                         st);
+hipError_t launch_bcast_recv(const BcastArgs& a, int grid, hipStream_t st) {
+  return launch((const void*)k_bcast_recv, a, grid, st);
 }
 
 hipError_t launch_adamw(const StepArgs& a, int grid, hipStream_t st) {
@@ -746,9 +714,6 @@ hipError_t noalloc_scratch(int device, void** ptr) {
     hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
     if (e != hipSuccess) return e;
     if (!p) return hipErrorInvalidSymbol;
-    e = hipMemset(p, 0, kNoallocHeadBytes);  // the folded finalize's counter
-    if (e == hipSuccess) e = hipDeviceSynchronize();
-    if (e != hipSuccess) return e;
     addr[device] = p;
   }
   *ptr = addr[device];

@@ -474,6 +474,7 @@ def hip_runtime():
         if h is None:
             raise RuntimeError("HIP runtime library not found")
         h.hipEventCreate.argtypes = [ctypes.POINTER(ctypes.c_void_p)]
+        h.hipEventCreateWithFlags.argtypes = [ctypes.POINTER(ctypes.c_void_p), ctypes.c_uint]
         h.hipEventDestroy.argtypes = [ctypes.c_void_p]
         h.hipEventRecord.argtypes = [ctypes.c_void_p, ctypes.c_void_p]
         h.hipEventSynchronize.argtypes = [ctypes.c_void_p]
@@ -483,16 +484,22 @@ def hip_runtime():
     return _hip
 
 
-class HipEvents:
-    """k raw hipEvent_t handles, for fl_round's phase_events."""
+# hipEventCreateWithFlags flag: no system-scope fence (cache write-back and
+# invalidation) when the event is recorded; for events that only time work.
+HIP_EVENT_DISABLE_SYSTEM_FENCE = 0x20000000
 
-    def __init__(self, k):
+
+class HipEvents:
+    """k raw hipEvent_t handles, for fl_round's phase_events (created with
+    hipEventCreateWithFlags(flags))."""
+
+    def __init__(self, k, flags=0):
         h = hip_runtime()
         self.handles = []
         for _ in range(k):
             e = ctypes.c_void_p()
-            if h.hipEventCreate(ctypes.byref(e)) != 0:
-                raise RuntimeError("hipEventCreate failed")
+            if h.hipEventCreateWithFlags(ctypes.byref(e), ctypes.c_uint(flags)) != 0:
+                raise RuntimeError("hipEventCreateWithFlags failed")
             self.handles.append(e.value)
 
     def elapsed_ms(self, i, j):

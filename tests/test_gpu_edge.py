@@ -78,8 +78,9 @@ def test_optimiser_edge_values(env, hp, step0):
 
 
 def test_two_streams_share_a_layout(env):
-    """Two rounds on two streams at once, one layout, each with its own
-    per-segment temporary; both match the oracle."""
+    """Two rounds on two streams, one layout: the second stream's call waits
+    for the first call's kernels and then reuses the layout's workspace;
+    both match the oracle."""
     torch, P, orc = env["torch"], env["P"], env["orc"]
     r = np.random.default_rng(23)
     sizes = r.integers(1, 200000, 30)
@@ -256,7 +257,7 @@ def test_every_path_is_independent_of_the_launch_shape(env, kind):
 
 def test_hundreds_of_thousands_of_segments(env):
     """300,000 segments of 1-8 elements: every tile straddles segments, and
-    the finalize folds 300,000 per-segment sums (clipped round, so the
+    the finalize kernels fold 300,000 per-segment sums (clipped round, so the
     whole-shard total too)."""
     r = np.random.default_rng(27)
     sizes = r.integers(1, 9, 300_000)
@@ -265,65 +266,68 @@ def test_hundreds_of_thousands_of_segments(env):
     _parity(env, w, "300k segments")
 
 
-def _twin_rounds(env, w, cfg_step0=1):
-    """The same round on two streams: the first stream to ask takes the
-    layout's workspace (finalize folded into the pass where the layout
-    allows it), the second a stream-ordered temporary (separate finalize
-    kernels).  Returns both results."""
-    torch, P = env["torch"], env["P"]
-    lay = P.Layout(w.seg_offsets, w.seg_decay)
-    da, db = B.DeviceInputs(w), B.DeviceInputs(w)
-    torch.cuda.synchronize()
-    sa, sb = torch.cuda.Stream(), torch.cuda.Stream()
-    out = []
-    for d, s in ((da, sa), (db, sb)):
-        ss = torch.full((w.A * w.n_seg,), -1.0, dtype=torch.float32, device="cuda")
-        with torch.cuda.stream(s):
-            H.gpu_round(P, lay, w, d, seg_sumsq=ss)
-        out.append((d, ss))
-    torch.cuda.synchronize()
-    res = []
-    for d, ss in out:
-        st = _state(d)
-        st["ss"] = ss.cpu().numpy()
-        res.append(st)
-    lay.close()
-    return res
+def _chain_of_calls(env, lay, w, d, ss):
+    """The round of w as the chain of standalone calls on the inputs d:
+    fl_local_step with per-segment sums (each pass followed by its finalize
+    kernel) A times, then fl_fedavg, or fl_fedopt with an outer step."""
+    P = env["P"]
+    for s in range(w.A):
+        P.fl_local_step(lay, w.hp, w.step0 + s, d.grads[s * w.R:(s + 1) * w.R], w.grad_scale,
+                        d.master, d.m, d.v, d.working, seg_sumsq=ss[s * w.n_seg:(s + 1) * w.n_seg])
+    reps = [d.working if k == w.self_group else d.replicas[k] for k in range(w.G)]
+    if w.outer is not None:
+        P.fl_fedopt(lay, reps, w.weights, w.outer, d.prev, d.buf, d.master, d.working)
+    else:
+        P.fl_fedavg(lay, reps, w.weights, d.master, d.working)
 
 
-@pytest.mark.parametrize("sizes,clip,scratch", [
-    ([1 << 20], 0.0, False),                               # one segment (the tiny round's shape)
-    ([300000, 17, 2047, 2049, 1 << 20, 5, 9, 70000], 0.0, False),  # 8 segments
-    ([300000, 17, 2047, 2049, 1 << 20, 5, 9, 70000], 1e-3, False),
-    ([300000, 17, 2047, 2049, 1 << 20, 5, 9, 70000], 1e-3, True),
-    ([1024 * 2048, 3], 1e-3, False),                       # a segment of exactly 1024 tiles
+@pytest.mark.parametrize("sizes,outer", [
+    ([1 << 20], False),                                          # one segment (the tiny round's shape)
+    ([300000, 17, 2047, 2049, 1 << 20, 5, 9, 70000], False),    # 8 segments
+    ([300000, 17, 2047, 2049, 1 << 20, 5, 9, 70000], True),     # the same with the outer step
+    ([1024 * 2048, 3], False),                                   # a segment of exactly 1024 tiles
+    ([1000, 1, 2, 3, 4, 5, 6, 7, 5000], False),                  # 9 segments: finalize kernels
+    ([1025 * 2048, 5], False),                                   # a two-chunk segment: the same
 ])
-def test_folded_finalize_matches_separate_kernels(env, sizes, clip, scratch):
-    """Where a pass folds its finalize into its last workgroup (every
-    segment one finalize chunk, at most 8 segments), the per-segment sums,
-    the clip totals and so every output are bitwise those of the separate
-    finalize kernels; both equal the oracle."""
+def test_carried_finalize_matches_the_chain_of_calls(env, sizes, outer):
+    """Where the round leaves each step's finalize to its next kernel (at
+    most 8 segments, each one finalize chunk), the per-segment sums and every
+    output are bitwise those of the chain of standalone calls, whose passes
+    are each followed by the finalize kernel; both equal the oracle."""
+    torch, P = env["torch"], env["P"]
     flags = (np.arange(len(sizes)) % 2).astype(np.uint8)
-    w = W.make_workload("fold", sizes, flags, R=4, G=2, A=3, max_grad_norm=clip,
-                        clip_scratch=scratch, seed=5)
-    a, b = _twin_rounds(env, w)
-    for k in ("master", "m", "v", "working", "ss"):
+    kw = dict(outer=dict(lr=0.7, momentum=0.9, nesterov=True)) if outer else {}
+    w = W.make_workload("carry", sizes, flags, R=4, G=2, A=3, seed=5, **kw)
+    _say(w.describe())
+    lay = P.Layout(w.seg_offsets, w.seg_decay)
+    d0, d1 = B.DeviceInputs(w), B.DeviceInputs(w)
+    s0 = torch.full((w.A * w.n_seg,), -1.0, dtype=torch.float32, device="cuda")
+    s1 = torch.full((w.A * w.n_seg,), -1.0, dtype=torch.float32, device="cuda")
+    torch.cuda.synchronize()
+    H.gpu_round(P, lay, w, d0, seg_sumsq=s0)
+    _chain_of_calls(env, lay, w, d1, s1)
+    torch.cuda.synchronize()
+    a, b = _state(d0), _state(d1)
+    a["ss"], b["ss"] = s0.cpu().numpy(), s1.cpu().numpy()
+    for k in a:
         u = np.uint16 if k == "working" else np.uint32
         assert np.array_equal(np.asarray(a[k]).view(u), np.asarray(b[k]).view(u)), k
     host = B.HostInputs(w)
     ref = H.oracle_round(env["orc"], w, host, want_sumsq=True)
-    H.assert_state_parity("fold", a, dict(master=host.master, m=host.m, v=host.v,
-                                          working=host.working), bitwise=True)
-    H.assert_sumsq("fold", a["ss"], ref.reshape(-1))
+    H.assert_state_parity("carry", a, dict(master=host.master, m=host.m, v=host.v,
+                                           working=host.working), bitwise=True)
+    H.assert_sumsq("carry", a["ss"], ref.reshape(-1))
+    lay.close()
 
 
-def test_grad_sumsq_folded_total_matches(env):
-    """fl_grad_sumsq on a fold-eligible layout: the whole-shard total and the
-    per-segment sums from the folded pass equal those of the separate
-    kernels bitwise (second stream) and the oracle's within tolerance."""
+def test_grad_sumsq_on_two_streams(env):
+    """fl_grad_sumsq on two streams in turn, one layout (the second waits for
+    the first's kernels and reuses the workspace): the whole-shard totals and
+    per-segment sums are bitwise equal and equal the oracle's within
+    tolerance."""
     torch, P, orc = env["torch"], env["P"], env["orc"]
     sizes = [50000, 3, 1 << 19, 77777]
-    w = W.make_workload("fold_total", sizes, [1, 0, 1, 1], R=3, G=2, A=1, seed=9)
+    w = W.make_workload("sumsq_streams", sizes, [1, 0, 1, 1], R=3, G=2, A=1, seed=9)
     lay = P.Layout(w.seg_offsets, w.seg_decay)
     d = B.DeviceInputs(w)
     torch.cuda.synchronize()
@@ -341,8 +345,8 @@ def test_grad_sumsq_folded_total_matches(env):
     host = B.HostInputs(w)
     g = orc.shard_reduce(host.grads[:w.R], w.grad_scale)
     ref_ss = orc.seg_sumsq(w.seg_offsets, g)
-    H.assert_sumsq("fold_total segs", s0.cpu().numpy(), ref_ss)
-    H.assert_sumsq("fold_total", t0.cpu().numpy(), np.array([orc.total_sumsq(g)]))
+    H.assert_sumsq("sumsq_streams segs", s0.cpu().numpy(), ref_ss)
+    H.assert_sumsq("sumsq_streams", t0.cpu().numpy(), np.array([orc.total_sumsq(g)]))
     lay.close()
 
 

@@ -63,9 +63,10 @@ def _round_pair(env, w):
 
 
 def test_noalloc_round_equals_fl_round_twice(env):
-    # first call: 400k elements in 6 segments (the finalize folded into the
-    # passes; per-segment sums); second: a smaller shard of 300 segments
-    # (separate finalize kernels) with clipping, in the same static scratch
+    # first call: 400k elements in 6 segments (each step's finalize carried by
+    # the next kernel; per-segment sums); second: a smaller shard of 300
+    # segments (separate finalize kernels) with clipping, in the same static
+    # scratch
     w1 = W.make_workload("noalloc_a", [150000, 17, 2049, 100000, 3, 147931],
                          [1, 0, 1, 1, 0, 1], R=4, G=3, A=3, seed=3,
                          weights=np.array([1, 2, 1], np.float32))
