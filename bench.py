@@ -120,10 +120,13 @@ def summarize_pmc(fetch_csv, write_csv, copy_mib, cmd_fetch, cmd_write, workload
     fetch, write = _pmc_means(fetch_csv), _pmc_means(write_csv)
 
     def pick(table, name):
-        for (k, g), v in table.items():
-            if name in k:
-                return v
-        raise KeyError(name)
+        """Mean and count over every dispatch of the kernel (all grid sizes:
+        a pass that carries the previous finalize has one more workgroup)."""
+        hits = [v for (k, g), v in table.items() if name in k]
+        if not hits:
+            raise KeyError(name)
+        cnt = sum(c for _, c in hits)
+        return sum(m * c for m, c in hits) / cnt, cnt
 
     copy_kib = copy_mib * 1024.0
     cands = [(k, g) for (k, g) in fetch if COPY_KERNEL in k]
