@@ -70,7 +70,9 @@ def _load(path, what):
 def host_lib():
     global _host
     if _host is None:
-        lib = _load(os.path.join(HERE, "libsynth_host.so"), "host generator")
+        # SYNTH_HOST_LIB names another build of synth_host.c (the sanitizer test's)
+        lib = _load(os.environ.get("SYNTH_HOST_LIB") or os.path.join(HERE, "libsynth_host.so"),
+                    "host generator")
         P = ctypes.POINTER(SynthSpec)
         lib.synth_host_fill.argtypes = [P, ctypes.c_int64, ctypes.c_int64, ctypes.c_void_p]
         lib.synth_host_fill_mt.argtypes = [P, ctypes.c_int64, ctypes.c_int64, ctypes.c_void_p,
