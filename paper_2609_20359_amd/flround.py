@@ -11,7 +11,9 @@ import ctypes
 import os
 
 HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(HERE, "libflround.so")
+# FLROUND_LIB names another build of the library to load (the sanitizer
+# test's host-instrumented build)
+LIB_PATH = os.environ.get("FLROUND_LIB") or os.path.join(HERE, "libflround.so")
 
 FL_OK = 0
 FL_ERR_INVALID = -1

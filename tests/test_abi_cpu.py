@@ -74,6 +74,28 @@ def test_layout_create_rejects_bad_layouts_without_a_gpu():
     assert L.fl_layout_create(10, 1, np.array([0, 10]).ctypes.data, None, None) == -1
 
 
+def test_layout_tables_are_built_before_the_device_is_needed():
+    """Valid layouts of several shapes go through the host-side table build
+    (tiles, pieces, finalize chunks) and only then ask for the device: with
+    no GPU the call returns FL_ERR_HIP and no handle."""
+    L = P.lib()
+    r = np.random.default_rng(5)
+    shapes = [
+        np.array([1], np.int64),                                  # one element
+        np.array([2048 * 1025 + 7], np.int64),                    # a two-chunk segment
+        np.ones(5000, np.int64),                                  # 5000 one-element segments
+        r.integers(1, 5000, 777).astype(np.int64),                # ragged
+        np.array([3, 2048 * 3, 1, 1, 2047, 2049, 5], np.int64),   # straddling tiles
+    ]
+    for sizes in shapes:
+        off = np.concatenate([[0], np.cumsum(sizes)]).astype(np.int64)
+        dec = (np.arange(sizes.size) % 2).astype(np.uint8)
+        h = ctypes.c_void_p()
+        rc = L.fl_layout_create(int(off[-1]), sizes.size, off.ctypes.data, dec.ctypes.data,
+                                ctypes.byref(h))
+        assert rc == -5 and not h.value
+
+
 def test_calls_reject_null_handles_without_a_gpu():
     L = P.lib()
     cfg = F.make_round_cfg(2, 2, 1, [1.0, 1.0], dict(lr=3e-4, beta1=0.9, beta2=0.95, eps=1e-8,
