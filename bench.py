@@ -181,15 +181,16 @@ def summarize_trace(stats_csv, cmd, workload="llama8b_s8"):
     return "\n".join(lines)
 
 
-PROBE_FILES = {1003782144: os.path.join(ROOT, "profiles", "hbm_ceiling_probe_llama31_8b_s8.md"),
-               2007564288: os.path.join(ROOT, "profiles", "hbm_ceiling_probe_llama31_8b_s4.md")}
+PROBE_FILES = {1003782144: os.path.join(ROOT, "profiles", "hbm_probe_reference_llama31_8b_s8.md"),
+               2007564288: os.path.join(ROOT, "profiles", "hbm_probe_reference_llama31_8b_s4.md")}
 
 
-def probe_ceiling(w, achieved):
-    """The attainable rate of the local step's access pattern with no
-    arithmetic, from the committed ceiling-probe summary for this shard
-    length, where the probe measured the pattern (a plain fused step: one
-    replica, no clipping); else None."""
+def probe_reference(w, achieved):
+    """The rate of the local step's access pattern with no arithmetic, in the
+    library's loop and launch structure (a same-design reference, not a
+    bound), from the committed probe summary for this shard length, where the
+    probe measured the pattern (a plain fused step: one replica, no
+    clipping); else None."""
     path = PROBE_FILES.get(w.n)
     pattern = "step_R%d" % w.R
     if not (w.H == 1 and w.max_grad_norm <= 0) or path is None or not os.path.exists(path):
@@ -432,7 +433,7 @@ def main():
             "traffic": traffic,
             "algorithmic_bytes": step_bytes,
             "kernel_source_hash": src_hash,
-            "probe_ceiling": probe_ceiling(w, achieved),
+            "probe_reference": probe_reference(w, achieved),
         },
     }
     del dev

@@ -85,12 +85,12 @@ def test_kernel_source_hash_ignores_comments(tmp_path, monkeypatch):
     assert hashes[0] == hashes[1] != hashes[2]
 
 
-def test_probe_ceiling_reads_the_committed_summaries():
-    pc = bench.probe_ceiling(W.llama8b_s8(), 5200.0)
+def test_probe_reference_reads_the_committed_summaries():
+    pc = bench.probe_reference(W.llama8b_s8(), 5200.0)
     assert pc is not None and 4000 < pc["gbs"] < 8000
     assert pc["frac"] == round(5200.0 / pc["gbs"], 4)
-    assert bench.probe_ceiling(W.hsdp_s4(), 5200.0) is not None
-    assert bench.probe_ceiling(W.stress(), 5200.0) is None   # no probe of that shard
+    assert bench.probe_reference(W.hsdp_s4(), 5200.0) is not None
+    assert bench.probe_reference(W.stress(), 5200.0) is None   # no probe of that shard
 
 
 def test_trace_summary_format(tmp_path):
