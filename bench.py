@@ -231,15 +231,14 @@ def W_ALL():
     return W.ALL
 
 
-def cpu_baseline(w, n_sample, min_seconds=10.0, max_rounds=10000):
+def cpu_baseline(w, n_sample, min_seconds=10.0, max_rounds=10000, n_one=16 << 20):
     """The oracle as it stands, timed on the host's cores: rounds on the first
     n_sample elements of the same shard (same generator, same segments),
     split into one contiguous chunk per thread; every thread runs the
     unchanged single-threaded oracle on its chunk (ctypes releases the GIL).
     Rounds are repeated on the evolving state until min_seconds have passed,
     so that the rate is taken over several seconds of CPU work.  Also the
-    one-thread rate of one round on the first chunk."""
-    import copy
+    one-thread rate of one round on the first n_one elements."""
     from concurrent.futures import ThreadPoolExecutor
 
     import numpy as np
@@ -263,12 +262,14 @@ def cpu_baseline(w, n_sample, min_seconds=10.0, max_rounds=10000):
         oracle.workload_round(orc, w, host, seg_off=off, seg_decay=dec, want_sumsq=True)
 
     per_param = w.A * w.step_bytes_per_param() + w.fedavg_bytes_per_param()
-    first = (copy.deepcopy(jobs[0][0]),) + jobs[0][1:]
+    # one thread, one round, on a slice of up to 16 Mi elements
+    n1 = min(n_one, n_sample)
+    off1, dec1, _ = w.span_layout(0, n1)
+    one = (B.HostInputs(w, span=(0, n1)), off1, dec1)   # inputs generated before the clock
     t0 = time.perf_counter()
-    run(first)
+    run(one)
     dt1 = time.perf_counter() - t0
-    n1 = int(bounds[1] - bounds[0])
-    del first
+    del one
     rounds = 0
     with ThreadPoolExecutor(T) as ex:
         t0 = time.perf_counter()
@@ -281,7 +282,7 @@ def cpu_baseline(w, n_sample, min_seconds=10.0, max_rounds=10000):
     return dict(value=round(rounds * n_sample * per_param / dt / 1e9, 4), unit="GB/s", cores=T,
                 kind="oracle", params_per_s=round(rounds * n_sample / dt, 1),
                 seconds=round(dt, 3), rounds=rounds,
-                one_thread_gbs=round(n1 * per_param / dt1 / 1e9, 4),
+                one_thread_gbs=round(n1 * per_param / dt1 / 1e9, 4), one_thread_elements=n1,
                 sample="%d rounds with per-segment sums (A=%d, R=%d, G=%d, H=%d) on the first "
                        "%d elements of the same shard, as %d contiguous chunks run concurrently, "
                        "one thread each, by the single-threaded C oracle" % (
@@ -358,9 +359,15 @@ def main():
 
     stream = torch.cuda.current_stream()
     K, Wm = args.steps, args.warmup
-    # phase events only time the kernels between them: recorded without the
+    # phase events only time the kernels between them: three per round (before
+    # the first local step, before FedAvg, after it), recorded without the
     # system-scope cache fence, which would add a cache write-back per event
-    events = [P.HipEvents(w.A + 2, P.HIP_EVENT_DISABLE_SYSTEM_FENCE) for _ in range(K)]
+    events = [P.HipEvents(3, P.HIP_EVENT_DISABLE_SYSTEM_FENCE) for _ in range(K)]
+
+    def phase_handles(ev):
+        h = ev.handles
+        return [h[0]] + [None] * (w.A - 1) + [h[1], h[2]]
+
     # every round also returns the per-segment sums of squares of each local
     # step's reduced gradient (A x n_seg floats)
     seg_sumsq = torch.empty(w.A * w.n_seg, dtype=torch.float32, device="cuda")
@@ -370,7 +377,7 @@ def main():
     torch.cuda.synchronize()
     log("warmup done (%d rounds)" % Wm)
 
-    cfgs = [runner.round_cfg(w, w.step0 + w.A * (Wm + k), phase_events=events[k].handles,
+    cfgs = [runner.round_cfg(w, w.step0 + w.A * (Wm + k), phase_events=phase_handles(events[k]),
                              dev=dev) for k in range(K)]
     start = torch.cuda.Event(enable_timing=True)
     stop = torch.cuda.Event(enable_timing=True)
@@ -384,12 +391,13 @@ def main():
     wall = time.perf_counter() - t_wall
     total_ms = start.elapsed_time(stop)
     ms_round = total_ms / K
-    round_ms = sorted(events[k].elapsed_ms(0, w.A + 1) for k in range(K))
+    round_ms = sorted(events[k].elapsed_ms(0, 2) for k in range(K))
     mid = K // 2
     median_ms = round_ms[mid] if K % 2 else 0.5 * (round_ms[mid - 1] + round_ms[mid])
-    step_ms = [events[k].elapsed_ms(a, a + 1) for k in range(K) for a in range(w.A)]
-    fed_ms = [events[k].elapsed_ms(w.A, w.A + 1) for k in range(K)]
-    avg_step = sum(step_ms) / len(step_ms)
+    # the A local steps of a round lie between its first two events
+    steps_ms = [events[k].elapsed_ms(0, 1) for k in range(K)]
+    fed_ms = [events[k].elapsed_ms(1, 2) for k in range(K)]
+    avg_step = sum(steps_ms) / (len(steps_ms) * w.A)
     avg_fed = sum(fed_ms) / len(fed_ms)
     log("timed %d rounds: %.3f ms/round (wall %.3f s); local step %.3f ms, fedavg %.3f ms"
         % (K, ms_round, wall, avg_step, avg_fed))

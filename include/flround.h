@@ -232,7 +232,9 @@ int fl_fedavg(const fl_layout* layout, int G, const uint16_t* const* replicas,
  * phase_events: NULL, or host array of A+2 hipEvent_t created by the caller;
  *   event a (a < A) is recorded on `stream` before local step a, event A
  *   before FedAvg, event A+1 after it (per-phase timing of the round, like
- *   the optimiser / aggregation split of Table 4).
+ *   the optimiser / aggregation split of Table 4).  A NULL entry records
+ *   nothing at its point (e.g. only events 0, A and A+1: every event
+ *   recorded between kernels costs GPU time).
  * ---------------------------------------------------------------------- */
 typedef struct {
   int R;                     /* peers in the sharding group                 */
@@ -244,7 +246,8 @@ typedef struct {
   int64_t step0;             /* step number of the round's first local step */
   const float* weights;      /* host, G FedAvg weights                      */
   const uint64_t* replica_fp;/* NULL or host, G fingerprints                */
-  void* const* phase_events; /* NULL or host, A+2 hipEvent_t                */
+  void* const* phase_events; /* NULL or host, A+2 hipEvent_t (entries may  */
+                             /* be NULL)                                    */
   const float* step_lr;      /* NULL or host, A learning rates, one per local
                                 step (overrides h.lr; e.g. fl_lr_cosine)   */
   float max_grad_norm;       /* > 0: clip each local step's gradient to this

@@ -481,7 +481,7 @@ const char* fl_status_string(int status) {
   }
 }
 
-int fl_version(void) { return (1 << 16) | 6; }
+int fl_version(void) { return (1 << 16) | 7; }
 
 float fl_lr_cosine(int64_t t, int64_t total_steps, int64_t warmup_steps, float lr_max,
                    float lr_min) {
@@ -919,14 +919,11 @@ int fl_round_hsdp(const fl_layout* layout, const fl_round_cfg* cfg, const fl_hsd
     for (const void* o : others)
       if (n > 0 && o == g_scratch) return FL_ERR_INVALID;
   }
-  if (c.phase_events)
-    for (int k = 0; k < c.A + 2; ++k)
-      if (!c.phase_events[k]) return FL_ERR_INVALID;
   if ((rc = check_device(layout)) != FL_OK) return rc;
 
   hipStream_t st = static_cast<hipStream_t>(stream);
   auto record = [&](int k) -> int {
-    if (!c.phase_events) return FL_OK;
+    if (!c.phase_events || !c.phase_events[k]) return FL_OK;
     return status_of(hipEventRecord(static_cast<hipEvent_t>(c.phase_events[k]), st));
   };
   Workspace ws;
@@ -1090,9 +1087,6 @@ static int round_impl(const fl_layout* layout, const fl_round_cfg* cfg,
   if (c.replica_fp)
     for (int g = 0; g < c.G; ++g)
       if (g != c.self_group && c.replica_fp[g] != layout->fingerprint) return FL_ERR_LAYOUT;
-  if (c.phase_events)
-    for (int k = 0; k < c.A + 2; ++k)
-      if (!c.phase_events[k]) return FL_ERR_INVALID;
   if ((rc = check_device(layout)) != FL_OK) return rc;
   const bool needs_ws = n > 0 && (seg_sumsq || c.max_grad_norm > 0.f);
   if (noalloc && needs_ws && noalloc_bytes(layout->L) > flr::kNoallocScratchBytes)
@@ -1100,7 +1094,7 @@ static int round_impl(const fl_layout* layout, const fl_round_cfg* cfg,
 
   hipStream_t st = static_cast<hipStream_t>(stream);
   auto record = [&](int k) -> int {
-    if (!c.phase_events) return FL_OK;
+    if (!c.phase_events || !c.phase_events[k]) return FL_OK;
     return status_of(hipEventRecord(static_cast<hipEvent_t>(c.phase_events[k]), st));
   };
   Workspace ws;

@@ -37,7 +37,7 @@ def test_status_strings_and_version():
         assert P.status_string(code).startswith("FL_ERR_")
     assert "unknown" in P.status_string(7)
     assert P.lib().fl_version() >> 16 == 1
-    assert P.lib().fl_version() & 0xFFFF >= 5   # fl_round_cfg.grad_scratch
+    assert P.lib().fl_version() & 0xFFFF >= 7   # NULL phase_events entries
 
 
 def test_fingerprint_host():

@@ -103,8 +103,9 @@ def test_trace_summary_format(tmp_path):
 
 
 def test_cpu_baseline_runs_the_oracle_on_host_threads():
-    cb = bench.cpu_baseline(W.llama8b_s8(), 1 << 16, min_seconds=0.5)
+    cb = bench.cpu_baseline(W.llama8b_s8(), 1 << 16, min_seconds=0.5, n_one=1 << 15)
     assert cb["kind"] == "oracle" and cb["unit"] == "GB/s"
     assert cb["rounds"] >= 1 and cb["seconds"] >= 0.5
     assert cb["cores"] >= 1 and cb["value"] > 0 and cb["one_thread_gbs"] > 0
     assert "%d elements" % (1 << 16) in cb["sample"]
+    assert cb["one_thread_elements"] == 1 << 15

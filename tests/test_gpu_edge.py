@@ -360,3 +360,30 @@ def test_multi_chunk_finalize_against_oracle(env, clip):
     flags = np.array([1, 1, 0, 1, 0, 1, 1], np.uint8)
     w = W.make_workload("multi_chunk", sizes, flags, R=2, G=2, A=2, max_grad_norm=clip, seed=12)
     _parity(env, w, "multi_chunk clip=%g" % clip)
+
+
+def test_phase_events_with_null_entries(env):
+    """Phase events only before the first local step, before FedAvg and after
+    it (NULL entries between them): the round's outputs equal an untimed
+    round's bit for bit, and the three events bracket the steps and
+    FedAvg."""
+    torch, P = env["torch"], env["P"]
+    w = W.make_workload("events", [300000, 17, 5000], [1, 0, 1], R=3, G=2, A=3, seed=4)
+    lay = P.Layout(w.seg_offsets, w.seg_decay)
+    d0, d1 = B.DeviceInputs(w), B.DeviceInputs(w)
+    s0 = torch.full((w.A * w.n_seg,), -1.0, dtype=torch.float32, device="cuda")
+    s1 = torch.full((w.A * w.n_seg,), -1.0, dtype=torch.float32, device="cuda")
+    ev = P.HipEvents(3, P.HIP_EVENT_DISABLE_SYSTEM_FENCE)
+    hs = [ev.handles[0], None, None, ev.handles[1], ev.handles[2]]
+    torch.cuda.synchronize()
+    H.gpu_round(P, lay, w, d0, seg_sumsq=s0, phase_events=hs)
+    H.gpu_round(P, lay, w, d1, seg_sumsq=s1)
+    torch.cuda.synchronize()
+    a, b = _state(d0), _state(d1)
+    a["ss"], b["ss"] = s0.cpu().numpy(), s1.cpu().numpy()
+    for k in a:
+        u = np.uint16 if k == "working" else np.uint32
+        assert np.array_equal(np.asarray(a[k]).view(u), np.asarray(b[k]).view(u)), k
+    assert ev.elapsed_ms(0, 1) > 0 and ev.elapsed_ms(1, 2) > 0
+    ev.close()
+    lay.close()
