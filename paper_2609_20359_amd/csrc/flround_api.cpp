@@ -27,10 +27,11 @@ struct fl_layout {
   void* dev_mem = nullptr;  // one allocation holding all device tables
   flr::LayoutDev L{};
   // Workspace of the per-segment sums of squares (see Workspace below),
-  // allocated with the layout and zeroed once.  It serves the calls of one
-  // stream at a time: the stream of the last call that used it (ws_stream,
-  // its kernels followed by ws_done); a call on another stream, or one being
-  // captured into a graph, takes a stream-ordered allocation of its own.
+  // allocated with the layout and zeroed once.  One call holds it at a time
+  // (ws_busy); the last one ran on ws_stream and recorded ws_done after its
+  // kernels, which a call on another stream waits for.  A call made while
+  // it is held, or one being captured into a graph, takes a stream-ordered
+  // allocation of its own.
   void* ws_mem = nullptr;
   std::atomic<bool> ws_busy{false};
   hipStream_t ws_stream = nullptr;
