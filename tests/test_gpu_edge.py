@@ -320,6 +320,19 @@ def test_carried_finalize_matches_the_chain_of_calls(env, sizes, outer):
     lay.close()
 
 
+@pytest.mark.parametrize("member,clip", [(True, 0.0), (False, 0.0), (True, 1e-3), (False, 1e-3)])
+def test_carried_finalize_in_hsdp_rounds(env, member, clip):
+    """FL+HSDP rounds (H = 2) on a layout whose finalize the round carries:
+    into the next step's kernel, then into FedAvg (member) or the broadcast
+    receive (receiver); clipped rounds use the finalize kernels instead.
+    Every output against the oracle."""
+    sizes = [300000, 17, 2047, 2049, 1 << 20, 5]
+    flags = (np.arange(len(sizes)) % 2).astype(np.uint8)
+    w = W.make_workload("carry_hsdp", sizes, flags, R=3, G=2, A=3, H=2, replica=1,
+                        hsdp_member=member, max_grad_norm=clip, seed=6)
+    _parity(env, w, "carry_hsdp member=%s clip=%g" % (member, clip))
+
+
 def test_grad_sumsq_on_two_streams(env):
     """fl_grad_sumsq on two streams in turn, one layout (the second waits for
     the first's kernels and reuses the workspace): the whole-shard totals and
