@@ -369,3 +369,36 @@ def test_many_rounds_stay_bitwise(env, kind):
         if w.outer is not None:
             assert np.array_equal(dev.buf.cpu().numpy().view(np.uint32), host.buf.view(np.uint32))
     lay.close()
+
+
+@pytest.mark.parametrize("kind", ["fsdp", "outer"])
+def test_resume_from_a_host_checkpoint(env, kind):
+    """Checkpoint and resume: after one round the state (master, m, v,
+    working; with the outer step also prev and buf) is copied to host memory,
+    as a checkpoint would, and loaded into fresh device buffers.  The next
+    round from the restored state equals the next round of the uninterrupted
+    run bit for bit: a round is a pure function of (state, inputs, step0)."""
+    torch, P = env["torch"], env["P"]
+    r = np.random.default_rng(44)
+    sizes = r.integers(1, 50_000, 7)
+    flags = r.integers(0, 2, sizes.size).astype(np.uint8)
+    kw = dict(outer=W.DILOCO_OUTER) if kind == "outer" else {}
+    w = W.make_workload("resume_" + kind, sizes, flags, R=3, G=3, A=2, step0=5, **kw)
+    lay = P.Layout(w.seg_offsets, w.seg_decay)
+    run = synth.buffers.DeviceInputs(w)
+    names = ["master", "m", "v", "working"] + (["prev", "buf"] if kind == "outer" else [])
+    H.gpu_round(P, lay, w, run, cfg=H.round_cfg(P, w, w.step0, dev=run))
+    torch.cuda.synchronize()
+    ckpt = {k: getattr(run, k).cpu().clone() for k in names}   # host copies
+    resumed = synth.buffers.DeviceInputs(w)
+    for k in names:
+        getattr(resumed, k).copy_(ckpt[k])
+    step1 = w.step0 + w.A
+    H.gpu_round(P, lay, w, run, cfg=H.round_cfg(P, w, step1, dev=run))
+    H.gpu_round(P, lay, w, resumed, cfg=H.round_cfg(P, w, step1, dev=resumed))
+    torch.cuda.synchronize()
+    for k in names:
+        a, b = getattr(run, k), getattr(resumed, k)
+        view = torch.int16 if k == "working" else torch.int32
+        assert torch.equal(a.view(view), b.view(view)), k
+    lay.close()
