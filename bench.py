@@ -210,6 +210,53 @@ def probe_reference(w, achieved):
             "frac": round(achieved / best, 4)}
 
 
+PROBE_EXE = os.path.join(ROOT, "hbmprobe", "hbm_probe")
+
+
+def step_pattern(w):
+    """The probe pattern of the workload's local step (a plain fused step
+    with R in {2, 4, 8}: one replica, no clipping), or None."""
+    if w.H == 1 and w.max_grad_norm <= 0 and w.R in (2, 4, 8):
+        return "step_R%d" % w.R
+    return None
+
+
+def probe_live(w, achieved, timeout=180):
+    """The same-design reference measured on this machine, now: hbm_probe (a
+    child process) moves the local step's access pattern over w.n elements
+    at one workgroup per CU with no arithmetic.  Returns the pattern, its
+    rate with nontemporal stores and the fraction of it the kernel reached,
+    or None when there is no pattern or probe."""
+    import subprocess
+
+    pattern = step_pattern(w)
+    if pattern is None or not os.path.exists(PROBE_EXE):
+        return None
+    r = subprocess.run([PROBE_EXE, str(w.n), pattern, "1"], capture_output=True, text=True,
+                       timeout=timeout)
+    if r.returncode != 0:
+        log("live probe failed (%d): %s" % (r.returncode, r.stdout[-300:] + r.stderr[-300:]))
+        return None
+    gbs = parse_probe_rate(r.stdout, pattern)
+    if gbs is None:
+        return None
+    return {"pattern": pattern, "gbs": gbs, "frac": round(achieved / gbs, 4),
+            "workgroups_per_cu": 1}
+
+
+def parse_probe_rate(text, pattern):
+    """GB/s of `pattern` with nontemporal stores at the first workgroups-per-CU
+    column of an hbm_probe table, or None."""
+    for line in text.splitlines():
+        cells = [c.strip() for c in line.strip().strip("|").split("|")]
+        if len(cells) >= 4 and cells[0] == pattern and cells[1] == "nt":
+            try:
+                return float(cells[2])
+            except ValueError:
+                return None
+    return None
+
+
 def step_label(w):
     """The kernels of one local step, as the roofline figure counts them."""
     fused = "k_step<%s=%d, fused, %s>" % ("R" if w.H == 1 else "H", w.R if w.H == 1 else w.H,
@@ -299,6 +346,8 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
                     help="the oracle leg repeats rounds on its sample for at least this long")
     ap.add_argument("--no-cpu", action="store_true")
+    ap.add_argument("--no-probe", action="store_true",
+                    help="skip the live same-design reference (hbm_probe) after the timed region")
     ap.add_argument("--blocks-per-cu", type=int, default=0,
                     help="workgroups per CU for every kernel (0: the library's defaults)")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
@@ -446,6 +495,11 @@ def main():
     }
     del dev
     torch.cuda.empty_cache()
+    if not args.no_probe:
+        out["roofline"]["probe_live"] = probe_live(w, achieved)
+        if out["roofline"]["probe_live"]:
+            log("live probe: %s at %.1f GB/s on this box" % (
+                out["roofline"]["probe_live"]["pattern"], out["roofline"]["probe_live"]["gbs"]))
     if not args.no_cpu:
         log("cpu baseline: oracle on %d elements" % args.cpu_sample)
         out["cpu_baseline"] = cpu_baseline(w, args.cpu_sample, args.cpu_seconds)

@@ -109,3 +109,18 @@ def test_cpu_baseline_runs_the_oracle_on_host_threads():
     assert cb["cores"] >= 1 and cb["value"] > 0 and cb["one_thread_gbs"] > 0
     assert "%d elements" % (1 << 16) in cb["sample"]
     assert cb["one_thread_elements"] == 1 << 15
+
+
+def test_live_probe_parsing_and_patterns():
+    table = ("| pattern | stores | 1/CU | best | of peak |\n|---|---|---|---|---|\n"
+             "| step_R8   | plain |  5286.4 |  5286.4 (1/CU) |  66.1 % |\n"
+             "| step_R8   | nt    |  5307.7 |  5307.7 (1/CU) |  66.3 % |\n"
+             "| step_R8_w | nt    |  4982.6 |  4982.6 (1/CU) |  62.3 % |\n")
+    assert bench.parse_probe_rate(table, "step_R8") == 5307.7
+    assert bench.parse_probe_rate(table, "step_R8_w") == 4982.6
+    assert bench.parse_probe_rate(table, "step_R4") is None
+    assert bench.step_pattern(W.llama8b_s8()) == "step_R8"
+    assert bench.step_pattern(W.hsdp_s4()) == "step_R4"
+    assert bench.step_pattern(W.stress()) is None                  # R = 16: no such pattern
+    assert bench.step_pattern(W.llama8b_s8_clip()) is None         # clipped: two passes
+    assert bench.step_pattern(W.hsdp_s4_h2()) is None              # FL+HSDP: wire + tier 2
