@@ -346,6 +346,8 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
                     help="the oracle leg repeats rounds on its sample for at least this long")
     ap.add_argument("--no-cpu", action="store_true")
+    ap.add_argument("--plain-placement", action="store_true",
+                    help="one allocation per array instead of the staggered arena")
     ap.add_argument("--no-probe", action="store_true",
                     help="skip the live same-design reference (hbm_probe) after the timed region")
     ap.add_argument("--blocks-per-cu", type=int, default=0,
@@ -392,9 +394,11 @@ def main():
     log("workload", w.describe())
     lay = P.Layout(w.seg_offsets, w.seg_decay)
     t0 = time.perf_counter()
-    dev = B.DeviceInputs(w)
+    # the shard's arrays in one allocation, staggered by 2 KiB (paper_2609_20359_amd.arena)
+    dev = B.DeviceInputs(w, place=None if args.plain_placement else P.place_arrays)
     torch.cuda.synchronize()
-    log("inputs resident: %.1f GB in %.1f s" % (dev.bytes() / 1e9, time.perf_counter() - t0))
+    log("inputs resident: %.1f GB in %.1f s (%s placement)" % (
+        dev.bytes() / 1e9, time.perf_counter() - t0, "plain" if args.plain_placement else "staggered"))
 
     if args.copy_calibration:
         src = torch.empty(args.copy_calibration << 18, dtype=torch.float32, device="cuda")
@@ -473,6 +477,7 @@ def main():
         "data": "synthetic",
         "config": dict(workload=w.name, n_params=w.n, segments=w.n_seg, R=w.R, G=w.G, A=w.A,
                        storage="bf16 gradients/replicas/working copy, fp32 master/m/v",
+                       placement="plain" if args.plain_placement else "arena, 2 KiB stagger",
                        bytes_per_round=bytes_round, parallelism="one GPU's shard"),
         "pct_of_peak": round(100.0 * gbs / PEAK_HBM_GBS, 2),
         "params_per_s": round(w.n / (ms_round * 1e-3), 1),

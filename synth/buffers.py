@@ -13,36 +13,50 @@ from .workloads import Workload
 
 
 class DeviceInputs:
-    def __init__(self, w: Workload, device="cuda:0"):
+    """Every input and state array of workload w on the device, filled by
+    the generator's device build.  place(n, dtypes, device) -> tensors
+    chooses where the arrays live (default: one allocation each)."""
+
+    def __init__(self, w: Workload, device="cuda:0", place=None):
         import torch
 
         n = w.n
         self.w = w
-        f32 = dict(dtype=torch.float32, device=device)
-        bf = dict(dtype=torch.bfloat16, device=device)
-        self.master = dev_fill(torch.empty(n, **f32), w.master_spec)
-        self.m = torch.zeros(n, **f32)
-        self.v = torch.zeros(n, **f32)
-        self.working = dev_fill(torch.empty(n, **bf), w.working_spec)
-        self.grad_arrays = [dev_fill(torch.empty(n, **bf), sp) for sp in w.grad_specs]
+        f32, bf = torch.float32, torch.bfloat16
+        wire_keys = []
+        for sp in w.wire_specs:
+            if sp is not None and sp.key() not in wire_keys:
+                wire_keys.append(sp.key())
+        plan = ([f32, f32, f32, bf] + [bf] * len(w.grad_specs) +
+                [bf] * sum(sp is not None for sp in w.replica_specs) + [bf] * len(wire_keys) +
+                ([bf] if w.H > 1 else []) + ([f32, f32] if w.outer else []) +
+                ([f32] if w.bcast_spec is not None else []) +
+                ([f32] if w.max_grad_norm > 0 and w.clip_scratch and w.H == 1 else []))
+        if place is None:
+            arrays = iter([torch.empty(n, dtype=d, device=device) for d in plan])
+        else:
+            arrays = iter(place(n, plan, device))
+        self.master = dev_fill(next(arrays), w.master_spec)
+        self.m = next(arrays).zero_()
+        self.v = next(arrays).zero_()
+        self.working = dev_fill(next(arrays), w.working_spec)
+        self.grad_arrays = [dev_fill(next(arrays), sp) for sp in w.grad_specs]
         self.grads = [self.grad_arrays[k] for k in w.grad_index]
-        self.replicas = [None if sp is None else dev_fill(torch.empty(n, **bf), sp)
+        self.replicas = [None if sp is None else dev_fill(next(arrays), sp)
                          for sp in w.replica_specs]
         filled = {}
-
-        def wire_buf(sp):
-            if sp.key() not in filled:
-                filled[sp.key()] = dev_fill(torch.empty(n, **bf), sp)
-            return filled[sp.key()]
-
-        self.replica_wires = [None if sp is None else wire_buf(sp) for sp in w.wire_specs] or None
-        self.wire = torch.empty(n, **bf) if w.H > 1 else None
-        self.prev = dev_fill(torch.empty(n, **f32), w.master_spec) if w.outer else None
-        self.buf = torch.zeros(n, **f32) if w.outer else None
-        self.bcast = None if w.bcast_spec is None else dev_fill(torch.empty(n, **f32),
-                                                                 w.bcast_spec)
-        self.grad_scratch = (torch.empty(n, **f32)
+        for sp in w.wire_specs:
+            if sp is not None and sp.key() not in filled:
+                filled[sp.key()] = dev_fill(next(arrays), sp)
+        self.replica_wires = [None if sp is None else filled[sp.key()]
+                              for sp in w.wire_specs] or None
+        self.wire = next(arrays) if w.H > 1 else None
+        self.prev = dev_fill(next(arrays), w.master_spec) if w.outer else None
+        self.buf = next(arrays).zero_() if w.outer else None
+        self.bcast = None if w.bcast_spec is None else dev_fill(next(arrays), w.bcast_spec)
+        self.grad_scratch = (next(arrays)
                              if w.max_grad_norm > 0 and w.clip_scratch and w.H == 1 else None)
+        assert next(arrays, None) is None
 
     def bytes(self):
         t = [self.master, self.m, self.v, self.working] + self.grad_arrays + \

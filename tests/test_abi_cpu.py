@@ -178,3 +178,30 @@ def test_binding_fails_loudly_without_the_library(monkeypatch, tmp_path):
         F.lib()
     with pytest.raises(RuntimeError, match="not built"):
         F.lr_cosine(1, 10, 1, 1e-3)
+
+
+def test_place_arrays_layout():
+    """The staggered placement: one allocation, array k at a 2 MiB boundary
+    plus k x 2 KiB, each a contiguous tensor of n elements of its dtype, no
+    two overlapping (checked on host memory)."""
+    import torch
+
+    from paper_2609_20359_amd import arena
+
+    n = 100_003
+    dtypes = [torch.float32, torch.float32, torch.bfloat16] + [torch.bfloat16] * 5
+    ts = arena.place_arrays(n, dtypes, device="cpu")
+    assert [t.dtype for t in ts] == dtypes
+    assert all(t.numel() == n and t.is_contiguous() for t in ts)
+    base = ts[0].data_ptr()
+    assert len({t.untyped_storage().data_ptr() for t in ts}) == 1   # one allocation
+    spans = []
+    for k, t in enumerate(ts):
+        assert (t.data_ptr() - base) % arena.ALIGN == k * arena.STRIDE
+        spans.append((t.data_ptr(), t.data_ptr() + n * t.element_size()))
+    spans.sort()
+    assert all(a[1] <= b[0] for a, b in zip(spans, spans[1:]))
+    for t in ts:
+        t.zero_()
+    ts[2].fill_(1.5)
+    assert all(float(t.float().abs().max()) == 0.0 for k, t in enumerate(ts) if k != 2)

@@ -1,6 +1,6 @@
-"""GPU parity at the workloads' full sizes, in the launch configuration the
-benchmark uses: one round on the whole shard, then every element of the
-result compared with the oracle.
+"""GPU parity at the workloads' full sizes, in the launch configuration and
+the array placement the benchmark uses: one round on the whole shard, then
+every element of the result compared with the oracle.
 
 The oracle runs chunk by chunk (64 Mi elements) on the host's threads.  Each
 chunk's inputs are the generator's values for that span: produced by the
@@ -79,7 +79,7 @@ def _whole_shard(env, w, name):
     torch, P, orc = env["torch"], env["P"], env["orc"]
     _say(name, w.describe())
     lay = P.Layout(w.seg_offsets, w.seg_decay)
-    dev = B.DeviceInputs(w)
+    dev = B.DeviceInputs(w, place=P.place_arrays)      # the benchmark's placement
     ss = torch.full((w.A * w.n_seg,), -1.0, dtype=torch.float32, device="cuda")
     H.gpu_round(P, lay, w, dev, seg_sumsq=ss)
     torch.cuda.synchronize()
