@@ -22,6 +22,13 @@ sys.path.insert(0, ROOT)
 
 METRIC = "effective HBM GB/s (% of MI355X peak) and params/s per fl_round, 8B-shaped shard"
 PEAK_HBM_GBS = 8000.0   # MI355X HBM3E, 8 TB/s
+# --placement: the function of paper_2609_20359_amd that allocates the shard's
+# arrays (None: torch's caching allocator) and how the config names it
+PLACEMENTS = {
+    "staggered": ("place_arrays", "one pool, array k at 2 MiB + k x 2 KiB"),
+    "separate": ("separate_arrays", "one exact-size hipMalloc per array"),
+    "torch": (None, "torch's caching allocator"),
+}
 KERNEL_SOURCES = [os.path.join(ROOT, "paper_2609_20359_amd", "csrc", f)
                   for f in ("flround_kernels.hip", "flr_internal.h")]
 
@@ -221,19 +228,21 @@ def step_pattern(w):
     return None
 
 
-def probe_live(w, achieved, timeout=180):
+def probe_live(w, achieved, stagger, timeout=180):
     """The same-design reference measured on this machine, now: hbm_probe (a
     child process) moves the local step's access pattern over w.n elements
-    at one workgroup per CU with no arithmetic.  Returns the pattern, its
-    rate with nontemporal stores and the fraction of it the kernel reached,
-    or None when there is no pattern or probe."""
+    at one workgroup per CU with no arithmetic, its streams placed as the
+    benchmark placed the shard's arrays (stagger bytes; 0: one exact-size
+    allocation each).  Returns the pattern, its rate with nontemporal stores and the
+    fraction of it the kernel reached, or None when there is no pattern or
+    probe."""
     import subprocess
 
     pattern = step_pattern(w)
     if pattern is None or not os.path.exists(PROBE_EXE):
         return None
-    r = subprocess.run([PROBE_EXE, str(w.n), pattern, "1"], capture_output=True, text=True,
-                       timeout=timeout)
+    r = subprocess.run([PROBE_EXE, str(w.n), pattern, "1", str(stagger)], capture_output=True,
+                       text=True, timeout=timeout)
     if r.returncode != 0:
         log("live probe failed (%d): %s" % (r.returncode, r.stdout[-300:] + r.stderr[-300:]))
         return None
@@ -241,7 +250,7 @@ def probe_live(w, achieved, timeout=180):
     if gbs is None:
         return None
     return {"pattern": pattern, "gbs": gbs, "frac": round(achieved / gbs, 4),
-            "workgroups_per_cu": 1}
+            "workgroups_per_cu": 1, "stagger_bytes": stagger}
 
 
 def parse_probe_rate(text, pattern):
@@ -346,8 +355,9 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
                     help="the oracle leg repeats rounds on its sample for at least this long")
     ap.add_argument("--no-cpu", action="store_true")
-    ap.add_argument("--plain-placement", action="store_true",
-                    help="one allocation per array instead of the staggered arena")
+    ap.add_argument("--placement", choices=sorted(PLACEMENTS), default="staggered",
+                    help="how the shard's arrays are allocated (paper_2609_20359_amd.arena): "
+                    "one staggered pool, separate exact-size hipMallocs, or torch's allocator")
     ap.add_argument("--no-probe", action="store_true",
                     help="skip the live same-design reference (hbm_probe) after the timed region")
     ap.add_argument("--blocks-per-cu", type=int, default=0,
@@ -394,11 +404,14 @@ def main():
     log("workload", w.describe())
     lay = P.Layout(w.seg_offsets, w.seg_decay)
     t0 = time.perf_counter()
-    # the shard's arrays in one allocation, staggered by 2 KiB (paper_2609_20359_amd.arena)
-    dev = B.DeviceInputs(w, place=None if args.plain_placement else P.place_arrays)
+    place_fn, placement = PLACEMENTS[args.placement]
+    place = getattr(P, place_fn) if place_fn else None
+    # the live probe places its streams the same way (stagger 0: one each)
+    stagger = P.arena.STRIDE if args.placement == "staggered" else 0
+    dev = B.DeviceInputs(w, place=place)
     torch.cuda.synchronize()
-    log("inputs resident: %.1f GB in %.1f s (%s placement)" % (
-        dev.bytes() / 1e9, time.perf_counter() - t0, "plain" if args.plain_placement else "staggered"))
+    log("inputs resident: %.1f GB in %.1f s (%s)" % (
+        dev.bytes() / 1e9, time.perf_counter() - t0, placement))
 
     if args.copy_calibration:
         src = torch.empty(args.copy_calibration << 18, dtype=torch.float32, device="cuda")
@@ -477,7 +490,7 @@ def main():
         "data": "synthetic",
         "config": dict(workload=w.name, n_params=w.n, segments=w.n_seg, R=w.R, G=w.G, A=w.A,
                        storage="bf16 gradients/replicas/working copy, fp32 master/m/v",
-                       placement="plain" if args.plain_placement else "arena, 2 KiB stagger",
+                       placement=placement,
                        bytes_per_round=bytes_round, parallelism="one GPU's shard"),
         "pct_of_peak": round(100.0 * gbs / PEAK_HBM_GBS, 2),
         "params_per_s": round(w.n / (ms_round * 1e-3), 1),
@@ -501,7 +514,7 @@ def main():
     del dev
     torch.cuda.empty_cache()
     if not args.no_probe:
-        out["roofline"]["probe_live"] = probe_live(w, achieved)
+        out["roofline"]["probe_live"] = probe_live(w, achieved, stagger)
         if out["roofline"]["probe_live"]:
             log("live probe: %s at %.1f GB/s on this box" % (
                 out["roofline"]["probe_live"]["pattern"], out["roofline"]["probe_live"]["gbs"]))

@@ -39,12 +39,16 @@
 // 1,003,782,144-element shard of Llama-3.1-8B at S = 8; the S = 4 shard has
 // 2,007,564,288 elements and needs about 120 GB).
 //
-// usage: hbm_probe [elements [pattern[,pattern...] [workgroups per CU]]]
+// usage: hbm_probe [elements [pattern[,pattern...] [workgroups per CU [stagger]]]]
 //   with a pattern list only those patterns run (the runtime copy line is
 //   printed only without a list); a counter run names one pattern and one
 //   workgroup count so that every dispatch of the run is that pattern.
+//   stagger (bytes, a multiple of 256; default 0): place the streams in one
+//   allocation, stream k at a 2 MiB boundary plus k * stagger, as the
+//   library's staggered placement places a shard's arrays.
 #include <hip/hip_runtime.h>
 
+#include <cstdint>
 #include <cstdio>
 #include <cstdlib>
 #include <string>
@@ -78,7 +82,7 @@ static bool selected(const char* name) {
 struct Streams {
   const u32x4* rd[12];  // read-only 16-byte streams, in units of u32x4
   u32x4* rmw[4];        // read-modify-write streams (fp32, 2 x 16 B per thread)
-  u32x4* wr[2];         // write-only streams
+  u32x4* wr[2];         // write-only streams: wr[0] bf16 (2 B per element), wr[1] fp32
   u32x4* tiled;         // 3 fp32 arrays interleaved per 2048-element tile
   long nvec;            // 16-byte vectors per bf16 stream
 };
@@ -138,6 +142,7 @@ void run_tiled(Streams s, int cus, long elems) {
 // vector.  All indices < nvec (bf16) or < 2 * nvec (fp32).
 template <int NRD, int NRMW, int NWH, int NWF, bool NTS, bool WAIT = false>
 __global__ void __launch_bounds__(256) k_pattern(Streams s) {
+  static_assert(NWF <= 1 && NWH <= 1, "wr[1] is the one fp32 and wr[0] the one bf16 stream");
   const long stride = (long)gridDim.x * 256;
   for (long i = (long)blockIdx.x * 256 + threadIdx.x; i < s.nvec; i += stride) {
     // WAIT: the previous iteration's stores complete before this
@@ -247,6 +252,15 @@ int main(int argc, char** argv) {
     }
     g_bpc = {b};
   }
+  // stagger > 0: every stream carved from one allocation, stream k at a
+  // 2 MiB boundary plus k * stagger bytes, in the order of the library's
+  // staggered placement of a shard (master, m, v, working copy, then the
+  // peer gradients); 0: one allocation per stream
+  const long stagger = argc > 4 ? std::atol(argv[4]) : 0;
+  if (stagger < 0 || stagger % 256 != 0) {
+    std::printf("stagger must be a non-negative multiple of 256 bytes\n");
+    return 2;
+  }
   int cus = 0;
   CK(hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, 0));
   hipDeviceProp_t prop;
@@ -254,17 +268,48 @@ int main(int argc, char** argv) {
   Streams s;
   s.nvec = elems / 8;
   std::vector<void*> bufs;
-  auto alloc = [&](size_t b) {
-    void* p = nullptr;
-    CK(hipMalloc(&p, b));
-    CK(hipMemset(p, 0, b));
-    bufs.push_back(p);
-    return p;
-  };
-  for (int k = 0; k < 12; ++k) s.rd[k] = static_cast<const u32x4*>(alloc(elems * 2));
-  for (int k = 0; k < 4; ++k) s.rmw[k] = static_cast<u32x4*>(alloc(elems * 4));
-  for (int k = 0; k < 2; ++k) s.wr[k] = static_cast<u32x4*>(alloc(elems * 4));
-  s.tiled = static_cast<u32x4*>(alloc(elems * 12 + 3 * 2048 * 4));
+  // the streams in placement order: the three state arrays, the written
+  // bf16 stream, the twelve read streams, then the rest
+  const size_t tiled_bytes = (size_t)elems * 12 + 3 * 2048 * 4;
+  std::vector<size_t> sizes;
+  for (int k = 0; k < 3; ++k) sizes.push_back((size_t)elems * 4);   // rmw[0..2]
+  sizes.push_back((size_t)elems * 2);                                 // wr[0] (bf16 writes)
+  for (int k = 0; k < 12; ++k) sizes.push_back((size_t)elems * 2);  // rd[0..11]
+  sizes.push_back((size_t)elems * 4);                                 // rmw[3]
+  sizes.push_back((size_t)elems * 4);                                 // wr[1]
+  sizes.push_back(tiled_bytes);                                       // tiled
+  std::vector<void*> ptrs;
+  if (stagger == 0) {
+    for (size_t b : sizes) {
+      void* p = nullptr;
+      CK(hipMalloc(&p, b));
+      CK(hipMemset(p, 0, b));
+      bufs.push_back(p);
+      ptrs.push_back(p);
+    }
+  } else {
+    const size_t align = (size_t)2 << 20;
+    size_t total = align;
+    for (size_t b : sizes) total += (b + align - 1) / align * align + align;
+    void* pool = nullptr;
+    CK(hipMalloc(&pool, total));
+    CK(hipMemset(pool, 0, total));
+    bufs.push_back(pool);
+    char* base = static_cast<char*>(pool);
+    size_t off = (align - reinterpret_cast<uintptr_t>(base) % align) % align;
+    for (size_t k = 0; k < sizes.size(); ++k) {
+      // slot k: [off, off + roundup(size) + align); the stream starts
+      // (k * stagger) % align into it, so it ends inside the slot
+      ptrs.push_back(base + off + (k * (size_t)stagger) % align);
+      off += (sizes[k] + align - 1) / align * align + align;
+    }
+  }
+  for (int k = 0; k < 3; ++k) s.rmw[k] = static_cast<u32x4*>(ptrs[k]);
+  s.wr[0] = static_cast<u32x4*>(ptrs[3]);
+  for (int k = 0; k < 12; ++k) s.rd[k] = static_cast<const u32x4*>(ptrs[4 + k]);
+  s.rmw[3] = static_cast<u32x4*>(ptrs[16]);
+  s.wr[1] = static_cast<u32x4*>(ptrs[17]);
+  s.tiled = static_cast<u32x4*>(ptrs[18]);
   std::printf("# HBM ceiling probe: %s, %d CUs, %ld-element streams\n\n", prop.gcnArchName, cus,
               elems);
   std::printf("GB/s by workgroups per CU; bytes = bytes the pattern moves; peak 8000 GB/s.\n\n");
@@ -306,7 +351,7 @@ int main(int argc, char** argv) {
   // reference point for the copy pattern (bytes read + written)
   if (g_only.empty()) {
     void* src = static_cast<void*>(s.rmw[0]);
-    void* dst = static_cast<void*>(s.wr[0]);
+    void* dst = static_cast<void*>(s.wr[1]);
     const size_t bytes = (size_t)elems * 4;
     const float ms =
         time_ms([&] { CK(hipMemcpyAsync(dst, src, bytes, hipMemcpyDeviceToDevice, 0)); }, 5);

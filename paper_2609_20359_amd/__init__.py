@@ -14,7 +14,7 @@ from .flround import (FL_MAX_GROUPS, FL_MAX_PEERS, FL_NOALLOC_SCRATCH_BYTES,
                       fl_round_noalloc, fl_round_outer, fl_shard_reduce,
                       fl_shard_reduce_wire, lib, lr_cosine, make_hsdp_cfg, make_round_cfg,
                       noalloc_workspace_bytes, set_blocks_per_cu, status_string)
-from .arena import place_arrays
+from .arena import place_arrays, separate_arrays
 
 __all__ = ["FL_MAX_GROUPS", "FL_MAX_PEERS", "FL_NOALLOC_SCRATCH_BYTES",
            "HIP_EVENT_DISABLE_SYSTEM_FENCE", "FlError", "HipEvents", "Layout", "fingerprint",
@@ -22,4 +22,5 @@ __all__ = ["FL_MAX_GROUPS", "FL_MAX_PEERS", "FL_NOALLOC_SCRATCH_BYTES",
            "fl_local_step", "fl_local_step_clipped",
            "fl_round", "fl_round_hsdp", "fl_round_noalloc", "fl_round_outer", "fl_shard_reduce",
            "fl_shard_reduce_wire", "lib", "lr_cosine", "make_hsdp_cfg", "make_round_cfg",
-           "noalloc_workspace_bytes", "place_arrays", "set_blocks_per_cu", "status_string"]
+           "noalloc_workspace_bytes", "place_arrays", "set_blocks_per_cu", "separate_arrays",
+           "status_string"]

@@ -475,6 +475,10 @@ def hip_runtime():
                 continue
         if h is None:
             raise RuntimeError("HIP runtime library not found")
+        h.hipMalloc.argtypes = [ctypes.POINTER(ctypes.c_void_p), ctypes.c_size_t]
+        h.hipFree.argtypes = [ctypes.c_void_p]
+        h.hipGetDevice.argtypes = [ctypes.POINTER(ctypes.c_int)]
+        h.hipSetDevice.argtypes = [ctypes.c_int]
         h.hipEventCreate.argtypes = [ctypes.POINTER(ctypes.c_void_p)]
         h.hipEventCreateWithFlags.argtypes = [ctypes.POINTER(ctypes.c_void_p), ctypes.c_uint]
         h.hipEventDestroy.argtypes = [ctypes.c_void_p]

@@ -205,3 +205,12 @@ def test_place_arrays_layout():
         t.zero_()
     ts[2].fill_(1.5)
     assert all(float(t.float().abs().max()) == 0.0 for k, t in enumerate(ts) if k != 2)
+
+
+def test_separate_arrays_is_device_only():
+    """The exact-size placement allocates with hipMalloc; it refuses host
+    tensors rather than falling back to another allocator."""
+    import torch
+
+    with pytest.raises(ValueError, match="device memory"):
+        P.separate_arrays(10, [torch.float32], device="cpu")

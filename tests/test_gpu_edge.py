@@ -33,11 +33,11 @@ def _state(dev):
                 working=H.to_u16(dev.working))
 
 
-def _parity(env, w, tag):
+def _parity(env, w, tag, place=None):
     torch, P, orc = env["torch"], env["P"], env["orc"]
     _say(tag, w.describe())
     lay = P.Layout(w.seg_offsets, w.seg_decay)
-    dev = B.DeviceInputs(w)
+    dev = B.DeviceInputs(w, place=place)
     ss = torch.full((w.A * w.n_seg,), -1.0, dtype=torch.float32, device="cuda")
     H.gpu_round(P, lay, w, dev, seg_sumsq=ss)
     torch.cuda.synchronize()
@@ -400,3 +400,42 @@ def test_phase_events_with_null_entries(env):
     assert ev.elapsed_ms(0, 1) > 0 and ev.elapsed_ms(1, 2) > 0
     ev.close()
     lay.close()
+
+
+def test_separate_arrays_allocates_and_frees_exact_blocks(env):
+    """separate_arrays gives each array a device allocation of its own, wraps it
+    without a copy, and frees it with the tensor; a round on such arrays is
+    bitwise equal to the oracle."""
+    import gc
+
+    torch, P = env["torch"], env["P"]
+    _say("separate_arrays: allocation, release, round")
+    n = 64 << 20
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+    free0 = torch.cuda.mem_get_info()[0]
+    ts = P.separate_arrays(n, [torch.float32, torch.bfloat16, torch.bfloat16])
+    assert [t.dtype for t in ts] == [torch.float32, torch.bfloat16, torch.bfloat16]
+    assert all(t.is_cuda and t.numel() == n and t.is_contiguous() for t in ts)
+    assert len({t.untyped_storage().data_ptr() for t in ts}) == 3
+    assert all(t.data_ptr() % 256 == 0 for t in ts)
+    spans = sorted((t.data_ptr(), t.data_ptr() + n * t.element_size()) for t in ts)
+    assert all(a[1] <= b[0] for a, b in zip(spans, spans[1:]))
+    torch.cuda.synchronize()
+    assert free0 - torch.cuda.mem_get_info()[0] >= 6 * n       # 8n bytes, to reporting slack
+    ts[1].fill_(1.5)
+    ts[0].zero_()
+    ts[2].zero_()
+    assert float(ts[1].float().sum()) == 1.5 * n and float(ts[0].abs().sum()) == 0.0
+    del ts
+    gc.collect()
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()      # what the checks above took from torch's allocator
+    assert free0 - torch.cuda.mem_get_info()[0] < 2 * n    # the blocks were freed
+    assert P.separate_arrays(0, [torch.float32])[0].numel() == 0
+    r = np.random.default_rng(71)
+    sizes = r.integers(1, 90000, 40)
+    w = W.make_workload("placed", sizes, r.integers(0, 2, sizes.size).astype(np.uint8),
+                        R=4, G=2, A=2)
+    _parity(env, w, "placed", place=P.separate_arrays)
+    torch.cuda.empty_cache()
