@@ -40,9 +40,10 @@
 // 2,007,564,288 elements and needs about 120 GB).
 //
 // usage: hbm_probe [elements [pattern[,pattern...] [workgroups per CU [stagger]]]]
-//   with a pattern list only those patterns run (the runtime copy line is
-//   printed only without a list); a counter run names one pattern and one
-//   workgroup count so that every dispatch of the run is that pattern.
+//   with a pattern list only those patterns run (an empty list: all, and
+//   the runtime copy line, which is printed only without a list); a counter
+//   run names one pattern and one workgroup count so that every dispatch of
+//   the run is that pattern; a workgroup count of 0 keeps the default set.
 //   stagger (bytes, a multiple of 256; default 0): place the streams in one
 //   allocation, stream k at a 2 MiB boundary plus k * stagger, as the
 //   library's staggered placement places a shard's arrays.
@@ -246,11 +247,11 @@ int main(int argc, char** argv) {
   }
   if (argc > 3) {
     const int b = std::atoi(argv[3]);
-    if (b < 1 || b > 16) {
-      std::printf("workgroups per CU must be 1..16\n");
+    if (b < 0 || b > 16) {
+      std::printf("workgroups per CU must be 1..16 (0: the default set)\n");
       return 2;
     }
-    g_bpc = {b};
+    if (b > 0) g_bpc = {b};
   }
   // stagger > 0: every stream carved from one allocation, stream k at a
   // 2 MiB boundary plus k * stagger bytes, in the order of the library's
