@@ -297,8 +297,10 @@ struct Workspace {
         owner->ws_stream = st;
         owner->ws_recorded = true;
       } else {
-        // the next call must not assume this one's kernels are ordered
-        owner->ws_recorded = true;
+        // nothing marks where this call's kernels end: wait for them here,
+        // so that the next call may take the workspace on any stream
+        (void)hipStreamSynchronize(st);
+        owner->ws_recorded = false;
         owner->ws_stream = nullptr;
         rc = FL_ERR_HIP;
       }
