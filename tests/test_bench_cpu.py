@@ -124,3 +124,15 @@ def test_live_probe_parsing_and_patterns():
     assert bench.step_pattern(W.stress()) is None                  # R = 16: no such pattern
     assert bench.step_pattern(W.llama8b_s8_clip()) is None         # clipped: two passes
     assert bench.step_pattern(W.hsdp_s4_h2()) is None              # FL+HSDP: wire + tier 2
+
+
+def test_every_placement_choice_names_an_exported_function():
+    """bench.py --placement resolves each choice to a function the package
+    exports (None: torch's allocator); the default is the staggered pool."""
+    import paper_2609_20359_amd as P
+
+    assert set(bench.PLACEMENTS) == {"staggered", "separate", "torch"}
+    for name, (fn, label) in bench.PLACEMENTS.items():
+        assert label
+        assert fn is None or callable(getattr(P, fn)), name
+    assert bench.PLACEMENTS["staggered"][0] == "place_arrays"
